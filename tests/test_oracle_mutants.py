@@ -1,0 +1,97 @@
+"""Planted mistakes: every variant of the oracle below carries one plausible
+error (a dropped term, a wrong sign, index or table entry, a transposed
+operand, a broken tie-break), and the oracle pins must reject each of them.
+
+Each variant is a textual edit of a copy of the oracle source, built with the
+same flags in a temporary directory; the pin suites then run against it in a
+subprocess.  The unedited copy must pass.
+"""
+
+import os
+import subprocess
+import sys
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
+
+import pytest
+
+from oracle import oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+PINS = ["tests/test_oracle_pins.py", "tests/test_oracle_terms.py", "tests/test_oracle_reduce.py"]
+
+MUTANTS = {
+    "forward peak drops the optimizer-step unit": (
+        "const R BF = (base + Obuf) + Xd;", "const R BF = base + Xd;"),
+    "backward peak drops the recomputed layer": (
+        "const R BB = ((base + Gbuf) + Rc) + Xd;", "const R BB = (base + Gbuf) + Xd;"),
+    "delta with the wrong sign": ("const R d = T1 - t;", "const R d = t - T1;"),
+    "gradients sharded from ZeRO-1": (
+        "const R sg = (z >= 2) ? iD : R(1.0);", "const R sg = (z >= 1) ? iD : R(1.0);"),
+    "ZeRO-3 per-microbatch traffic 2 instead of 3": ("{0.0, 0.0, 1.0, 3.0}", "{0.0, 0.0, 1.0, 2.0}"),
+    "first microbatch uses the stable ZeRO traffic": (
+        "const R G2Gf = fma3(R(mf_tab[z]), r_, p2p);", "const R G2Gf = fma3(R(ms_tab[z]), r_, p2p);"),
+    "interference divides by a neighbour's factor": (
+        "X[j] = (sc[j] - ov) * R(psi[mask * 4 + j]);", "X[j] = (sc[j] - ov) * R(psi[mask * 4 + (j ^ 1)]);"),
+    "interference levels in ascending order": (
+        "for (int n = 4; n >= 2; --n) {", "for (int n = 2; n <= 4; ++n) {"),
+    "activation swap-in uses the kept fraction": (
+        "const R H2Ds = fma3(ra, A, HW) * iP;", "const R H2Ds = fma3(qa, A, HW) * iP;"),
+    "recomputation counted twice": ("R(exact(3 * l + c))", "R(exact(3 * l + 2 * c))"),
+    "stash ignores the accumulation steps": ("const R KA = R(exact(ke * Amb));", "const R KA = R(exact(k * Amb));"),
+    "host and device streams transposed": (
+        "const R Xs[4] = {C, G2Gs, H2Ds, D2Hs};", "const R Xs[4] = {C, G2Gs, D2Hs, H2Ds};"),
+    "objective weights the first microbatch": ("const R obj = fma3(Gd, t, d);", "const R obj = fma3(Gd, T1, d);"),
+    "frontier keeps equal objectives": ("if (bobj[j] < below)", "if (bobj[j] <= below)"),
+    "ties broken by the highest id": ("(o1 == o2 && i1 < i2)", "(o1 == o2 && i1 > i2)"),
+    "bucket edges shifted by one": ("(h.mem_bytes * (double)(j + 1))", "(h.mem_bytes * (double)(j + 2))"),
+    "norm parameters split over TP": (
+        "const int64_t Psi = (Pq + Pm) / TP + 2 * h * hkvr + Prep;",
+        "const int64_t Psi = (Pq + Pm + Prep) / TP + 2 * h * hkvr;"),
+    "one KV projection forgotten in the activations": ("+ 2 * hkvr + (m.flash", "+ hkvr + (m.flash"),
+    "optimizer-step fetch takes the weight bytes": (
+        "const R HX = fma3(ro, So, DG);", "const R HX = fma3(ro, So, DW);"),
+    "weights fetched once per microbatch": ("const R HWz = R(2.0) * Sw;", "const R HWz = Sw;"),
+    "logits missing from the backward peak": (
+        "const R BB = ((base + Gbuf) + Rc) + Xd;", "const R BB = ((base + Gbuf) + Rc);"),
+    "efficiency of the wrong microbatch": (
+        "R(X.inv_eta[g.hw][pr.mb_index])", "R(X.inv_eta[g.hw][0])"),
+    "pipeline sends counted once for middle stages": (
+        "(int64_t)((k > 1) + (k < PP))", "(int64_t)((k > 1) || (k < PP))"),
+}
+
+
+def _build(tmp, name, src):
+    path = os.path.join(tmp, name + ".cpp")
+    with open(path, "w") as f:
+        f.write(src)
+    lib = os.path.join(tmp, name + ".so")
+    subprocess.run(["g++", *O.CXXFLAGS, path, "-o", lib], check=True, capture_output=True)
+    return lib
+
+
+def _pins_pass(lib):
+    env = dict(os.environ, MIST_ORACLE_LIB=lib)
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", *PINS],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    return r.returncode == 0, r.stdout[-2000:]
+
+
+def test_planted_mistakes_are_caught():
+    with open(O.SRC) as f:
+        src = f.read()
+    jobs = {"unchanged": src}
+    for i, (what, (old, new)) in enumerate(MUTANTS.items()):
+        assert src.count(old) == 1, what
+        jobs["m%02d" % i] = src.replace(old, new)
+    names = {"m%02d" % i: what for i, what in enumerate(MUTANTS)}
+    with tempfile.TemporaryDirectory() as tmp:
+        def run(item):
+            key, text = item
+            return key, _pins_pass(_build(tmp, key, text))
+        with ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
+            results = dict(ex.map(run, jobs.items()))
+    ok, out = results.pop("unchanged")
+    assert ok, out
+    survivors = [names[k] for k, (passed, _) in sorted(results.items()) if passed]
+    assert not survivors, "pins did not catch: %s" % survivors
