@@ -1,0 +1,176 @@
+"""Benchmark of the tuner's hot path on one MI355X: configurations evaluated per second
+(cost model + feasibility filter + per-bucket and per-group reductions) and the FP64
+vector roofline fraction of the evaluation kernel.
+
+One step = one mist_eval_space over the whole space of the workload (default c2: GPT
+L32 h2560, 273,952,500 configurations, 4,527 groups), inputs resident on the GPU.
+Prints one JSON line.  The CPU baseline is the plain oracle timed on this host over a
+bounded, seeded sample of the same workload's groups.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "candidate configs evaluated/sec (eval+filter+reduce); % of FP64 vector peak"
+FP64_VECTOR_PEAK_TFLOPS = 78.6   # 256 CUs x 128 FP64 FLOP/clk (64 FMA lanes) x 2.4 GHz
+FLOPS_FILE = os.path.join(ROOT, "tests", "golden", "flops_per_config.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2503_19050_amd", "csrc", "mist_kernels.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def flops_per_config(name: str):
+    try:
+        with open(FLOPS_FILE) as f:
+            return json.load(f)["workloads"][name]["flops_per_config"]
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def traffic_record(name: str, n_launch_configs: int):
+    """HBM bytes per evaluation launch from the committed rocprofv3 counter runs, if they
+    were taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)[name]
+    except (OSError, KeyError, ValueError):
+        return None
+    if rec.get("kernel_sha") != kernel_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(wl: dict, seconds: float) -> dict:
+    """The oracle as it stands, one process, one thread, over seeded random groups until
+    about ``seconds`` of work."""
+    import numpy as np
+    from oracle import oracle as O
+
+    o = O.Oracle(wl)
+    order = np.random.default_rng(2025).permutation(o.n_groups)
+    keys = o.group_keys()
+    done = configs = 0
+    t0 = time.perf_counter()
+    for g in order:
+        o.run(int(g), int(g) + 1)
+        done += 1
+        configs += keys[int(g)]["size"]
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {
+        "value": configs / dt, "unit": "configs/s", "cores": 1, "kind": "oracle",
+        "sample": "%d of %d groups of %s in seeded random order, %d configs, %.1f s" % (
+            done, o.n_groups, wl["name"], configs, dt),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the evaluation of one space runs on a single device "
+              "(multi-GPU sharding by group is described in DESIGN.md, not run here)", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2503_19050_amd import mist
+    from paper_2503_19050_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    props = torch.cuda.get_device_properties(0)
+    wl = W.workload(args.workload)
+
+    t0 = time.perf_counter()
+    S = mist.from_workload(wl)
+    torch.cuda.synchronize()
+    build_ms = (time.perf_counter() - t0) * 1e3
+    info = S.launch_info()
+    log("workload", wl["name"], S.n_configs, "configs", S.n_groups, "groups", info)
+
+    for _ in range(args.warmup):
+        S.eval()
+    torch.cuda.synchronize()
+
+    S.set_timing(True)
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        S.eval()
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    k1_ms, k2_ms, n = S.read_timing()
+    assert n == args.steps
+    S.set_timing(False)
+
+    t0 = time.perf_counter()
+    best = S.best()
+    extract_ms = (time.perf_counter() - t0) * 1e3
+    feasible = sum(1 for b in best if b["id"] != mist.MIST_NONE)
+
+    ms_per_step = total_ms / args.steps
+    value = S.n_configs / (ms_per_step / 1e3)
+    k1_avg = k1_ms / n
+    k2_avg = k2_ms / n
+    fpc = flops_per_config(wl["name"])
+    roofline = None
+    if fpc is not None:
+        achieved = fpc * S.n_configs / (k1_avg / 1e3) / 1e12
+        traffic = traffic_record(wl["name"], S.n_configs)
+        roofline = {"bound": "alu", "achieved": achieved, "peak": FP64_VECTOR_PEAK_TFLOPS,
+                    "unit": "TFLOP/s", "frac": achieved / FP64_VECTOR_PEAK_TFLOPS, "traffic": traffic,
+                    "kernel": "k_eval", "flops_per_config": fpc}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline: oracle for about %.0f s" % args.cpu_seconds)
+        cpu = cpu_baseline(wl, args.cpu_seconds)
+
+    rec = {
+        "metric": METRIC, "value": value, "unit": "configs/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "%s: %s" % (wl["name"], wl["desc"]), "configs": S.n_configs,
+                   "groups": S.n_groups, "buckets": S.n_buckets, "tiles": info["tiles"],
+                   "block": info["block"], "units_per_tile": info["units_per_tile"]},
+        "eval_kernel_ms": k1_avg, "reduce_kernel_ms": k2_avg, "space_build_ms": build_ms,
+        "extract_best_ms": extract_ms, "feasible_groups": feasible,
+        "device": {"name": props.name, "cus": props.multi_processor_count,
+                   "arch": getattr(props, "gcnArchName", "")},
+        "roofline": roofline, "cpu_baseline": cpu,
+    }
+    S.close()
+    print(json.dumps(rec))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

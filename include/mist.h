@@ -1,0 +1,214 @@
+/*
+ * libmist — batched evaluation of Mist's intra-stage tuner on one MI355X (gfx950).
+ *
+ * Zhu et al., "Mist: Efficient Distributed Training of Large Language Models via
+ * Memory-Parallelism Co-Optimization", EuroSys '25.
+ *
+ * Problem (Sec. 5.3): given a model, a global batch B and a device mesh, intra-stage
+ * tuning scores every per-stage tuple of Table 2 — microbatch b, DP, TP, ZeRO level,
+ * recomputed layers, and the weight / gradient / optimizer-state / activation offload
+ * ratios — for every candidate stage, by its peak memory (the constraint of Eq. 4) and its
+ * stable-microbatch time t and first-microbatch delta d (Eq. 5-6) from the interference
+ * model (Algorithm 1, Sec. 5.2.2); it keeps the feasible minimum of G*t + d per stage and a
+ * time-versus-memory staircase over 64 memory buckets, which the inter-stage partitioner
+ * (Eq. 1-3) consumes.
+ *
+ * A "group" is one candidate stage: (hardware sample, G, PP, k, l) with k the 1F1B
+ * in-flight count of the stage position (k = PP first stage, 1 last) and l its layers.
+ * Groups are numbered in ascending order of hw, PP, G, k, l.  Within a group a
+ * configuration has the canonical local id
+ *     ((((((p*(l+1) + c)*4 + z)*R + wo)*R + go)*R + oo)*R + ao)
+ * with p the index of (b, TP) among the group's pairs in ascending order, c the recomputed
+ * layers, z the ZeRO level and wo, go, oo, ao indices into the ratio list of length R;
+ * its global id is the group's base plus the local id.
+ *
+ * Conventions
+ *  - Every entry point returns a mist_status; nothing aborts and no C++ exception crosses
+ *    the ABI.  On failure mist_last_error() returns a message (thread-local, valid until
+ *    the next call on the same thread).
+ *  - One mist_space must not be used from two threads at once; distinct spaces are
+ *    independent.
+ *  - Pointers named "host" are host memory owned by the caller.  Device memory is owned by
+ *    the space and released by mist_space_destroy.
+ */
+#ifndef MIST_H
+#define MIST_H
+
+#include <stdint.h>
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t mist_status;
+#define MIST_OK 0
+#define MIST_E_INVALID (-1) /* bad descriptor or argument */
+#define MIST_E_NOMEM (-2)   /* host or device allocation failed */
+#define MIST_E_DEVICE (-3)  /* a HIP call failed; the message carries hipGetErrorString */
+#define MIST_E_STATE (-4)   /* results requested before mist_eval_space */
+#define MIST_E_RANGE (-5)   /* index out of range or output capacity too small */
+
+#define MIST_ARCH_GPT 0   /* LayerNorm, GeLU MLP of width ffn, learned positions */
+#define MIST_ARCH_LLAMA 1 /* RMSNorm, SwiGLU MLP of width ffn, grouped-query attention */
+
+#define MIST_L_FULL 0     /* stage layer counts 1..L-PP+1 (PP = 1: L) */
+#define MIST_L_BALANCED 1 /* stage layer counts floor(L/PP) and ceil(L/PP) */
+
+#define MIST_MAX_BUCKETS 64
+#define MIST_MAX_RATIOS 32
+#define MIST_MAX_MB 16
+#define MIST_NONE UINT64_MAX /* id of an empty bucket or of a group with no feasible config */
+
+/* Model shape (Sec. 6.1, Table 4; the transformer of the symbolic trace, Sec. 5.2.1). */
+typedef struct mist_model_desc {
+  int32_t arch;      /* MIST_ARCH_GPT or MIST_ARCH_LLAMA */
+  int32_t n_layers;  /* L */
+  int64_t hidden;    /* h; divisible by heads */
+  int32_t heads;     /* attention heads */
+  int32_t kv_heads;  /* key/value heads; divides heads */
+  int64_t ffn;       /* MLP width f */
+  int64_t seq;       /* sequence length s */
+  int64_t vocab;     /* V */
+  int32_t bytes_w;   /* bytes per fp16/bf16 weight, gradient and activation element (2) */
+  int32_t bytes_opt; /* optimizer bytes per parameter: fp32 master + Adam m, v (12) */
+  int32_t flash;     /* 1: FlashAttention, no stored attention probabilities */
+} mist_model_desc;
+
+/* One hardware sample: the inputs of the runtime model (Sec. 5.2.1: compute from the
+ * operator database, communication as bytes / bandwidth) and of the interference model
+ * (Sec. 5.2.2: one slowdown factor per co-running combination and stream). */
+typedef struct mist_hw_desc {
+  double flops;      /* peak FLOP/s, > 0 */
+  double mem_bytes;  /* memory budget in bytes, > 0 (the Mem_Budget of Eq. 4) */
+  double pcie_bw;    /* host<->device bytes/s, > 0 */
+  double link_bw;    /* device<->device bytes/s, > 0 */
+  double eta_max;    /* compute efficiency eta(b) = eta_max*b*s/(b*s + n_half) */
+  double n_half;
+  double phi[16][4]; /* phi[mask][j]: slowdown of stream j (0 compute, 1 GPU-GPU, 2 host->
+                        device, 3 device->host) when the streams of mask co-run; >= 1 and
+                        finite; entries of absent streams and single-stream masks unused */
+} mist_hw_desc;
+
+/* The search space of Table 2 for every candidate stage. */
+typedef struct mist_space_desc {
+  int64_t n_devices;     /* D */
+  int64_t global_batch;  /* B */
+  const int32_t* mb;     /* host: microbatch sizes, strictly ascending, >= 1 */
+  int32_t n_mb;          /* 1..MIST_MAX_MB */
+  const double* ratios;  /* host: offload ratios, strictly ascending in [0, 1] */
+  int32_t n_ratios;      /* R, 1..MIST_MAX_RATIOS */
+  int32_t n_buckets;     /* NB, 1..MIST_MAX_BUCKETS; bucket edges E_j = M*(j+1)/NB */
+  int32_t l_rule;        /* MIST_L_FULL or MIST_L_BALANCED */
+} mist_space_desc;
+
+/* Device memory provider, e.g. PyTorch's caching allocator.  alloc returns NULL on
+ * failure; free receives exactly the pointers alloc returned. */
+typedef struct mist_allocator {
+  void* (*alloc)(size_t bytes, void* ctx);
+  void (*free)(void* ptr, void* ctx);
+  void* ctx;
+} mist_allocator;
+
+typedef struct mist_space mist_space;
+
+/* A decoded configuration (the per-stage tuple of Table 2 plus its group key). */
+typedef struct mist_config {
+  int32_t hw, G, PP, k, l;       /* group key */
+  int32_t b, tp, dp, zero, ckpt; /* microbatch, TP, DP, ZeRO level 0..3, recomputed layers */
+  int32_t wo_idx, go_idx, oo_idx, ao_idx; /* indices into the ratio list */
+  double wo, go, oo, ao;         /* the ratios */
+} mist_config;
+
+typedef struct mist_result {
+  uint64_t id;    /* MIST_NONE when no feasible configuration */
+  double obj;     /* G*t + d; +inf when none */
+  double t;       /* stable-microbatch time (s), Eq. 5 */
+  double d;       /* first-microbatch delta (s), Eq. 6 */
+  double mem;     /* max(forward peak, backward peak) in bytes, Eq. 4 */
+  int32_t bucket; /* memory bucket of mem; -1 when none */
+  int32_t pad;
+  mist_config cfg;
+} mist_result;
+
+typedef struct mist_group_key {
+  int32_t hw, G, PP, k, l, n_pairs;
+  uint64_t base;  /* id of the group's first configuration */
+  uint64_t size;  /* configurations in the group */
+} mist_group_key;
+
+/* Validates and copies the descriptors (the caller may free them afterwards), enumerates
+ * the groups, builds the tables and uploads them to the current HIP device.  hw points to
+ * n_hw >= 1 samples.  alloc may be NULL (hipMalloc/hipFree).  On success *out owns every
+ * device and host buffer.  Errors: MIST_E_INVALID, MIST_E_NOMEM, MIST_E_DEVICE. */
+mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n_hw,
+                              const mist_space_desc* s, const mist_allocator* alloc,
+                              mist_space** out);
+
+/* Enqueues the evaluation of every configuration (cost model, feasibility filter, per
+ * bucket and per group reductions; Sec. 5.3, Eq. 4-6, Algorithm 1) on hip_stream
+ * (a hipStream_t; NULL = the null stream) and returns without waiting.  Re-runnable; each
+ * run overwrites the previous results.  Errors: MIST_E_INVALID, MIST_E_DEVICE. */
+mist_status mist_eval_space(mist_space* S, void* hip_stream);
+
+/* Waits for the last evaluation and writes, for groups g0..g0+n-1, the feasible
+ * configuration of minimum obj (lowest id among equal obj) into host out[0..n-1]; a group
+ * without a feasible configuration gets id MIST_NONE, obj +inf, bucket -1.
+ * Errors: MIST_E_STATE (no evaluation yet), MIST_E_RANGE, MIST_E_DEVICE. */
+mist_status mist_get_best(mist_space* S, int64_t g0, int64_t n, mist_result* out);
+
+/* Waits for the last evaluation and writes the time-vs-memory staircase of group g into
+ * host out[0..*n_out-1] in increasing bucket order: bucket j is on it when it holds a
+ * feasible configuration whose obj is strictly below that of every lower bucket.  If cap
+ * is too small returns MIST_E_RANGE with *n_out set to the required count. */
+mist_status mist_get_pareto(mist_space* S, int64_t g, mist_result* out, int32_t cap,
+                            int32_t* n_out);
+
+/* Raw per-bucket table of groups g0..g0+n-1: host ids[n*NB] and objs[n*NB] (MIST_NONE /
+ * +inf for empty buckets) and host frontier masks[n] (bit j = bucket j on the staircase);
+ * any output pointer may be NULL.  Waits for the last evaluation.  Errors as get_best. */
+mist_status mist_get_buckets(mist_space* S, int64_t g0, int64_t n, uint64_t* ids, double* objs,
+                             uint64_t* masks);
+
+/* Sizes of the space: configurations, groups, buckets.  Any pointer may be NULL. */
+mist_status mist_space_info(const mist_space* S, uint64_t* n_configs, int64_t* n_groups,
+                            int32_t* n_buckets);
+
+/* Key of group g into host *out.  Errors: MIST_E_RANGE. */
+mist_status mist_get_group_key(const mist_space* S, int64_t g, mist_group_key* out);
+
+/* Decodes a global id into host *out (host-side arithmetic only).  Errors: MIST_E_RANGE. */
+mist_status mist_decode(const mist_space* S, uint64_t id, mist_config* out);
+
+/* Evaluates the configurations host ids[0..n-1] on the device with the same cost-model code
+ * as mist_eval_space and writes host out[4*i..4*i+3] = t, d, mem, obj.  Synchronous on
+ * hip_stream.  Errors: MIST_E_RANGE (an id >= the number of configurations), MIST_E_NOMEM,
+ * MIST_E_DEVICE. */
+mist_status mist_eval_ids(mist_space* S, const uint64_t* ids, int64_t n, double* out,
+                          void* hip_stream);
+
+/* Kernel timing.  mist_set_timing(S, 1) waits for pending work and starts recording HIP
+ * events around the two kernels of every later mist_eval_space, on the evaluation stream;
+ * mist_read_timing waits for the recorded evaluations and returns the summed durations (ms)
+ * of the evaluation kernel and of the group-reduction kernel and their count, then starts a
+ * new record.  mist_set_timing(S, 0) stops recording.  Errors: MIST_E_STATE (timing off),
+ * MIST_E_DEVICE. */
+mist_status mist_set_timing(mist_space* S, int32_t on);
+mist_status mist_read_timing(mist_space* S, double* eval_ms, double* reduce_ms, int64_t* n_evals);
+
+/* Launch geometry of the evaluation kernel: tiles (blocks), threads per block, units
+ * (pair, recomputed-layers slabs) per tile. */
+mist_status mist_launch_info(const mist_space* S, int64_t* n_tiles, int32_t* block,
+                             int32_t* units_per_tile);
+
+/* Frees every buffer of the space (through its allocator).  NULL is accepted. */
+mist_status mist_space_destroy(mist_space* S);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* mist_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MIST_H */

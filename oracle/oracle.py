@@ -230,7 +230,7 @@ def run_groups(wl: dict, groups, procs: int = 1) -> dict:
         parts = [(g0, o.run(g0, g1)) for g0, g1 in ranges]
     else:
         import multiprocessing as mp
-        ctx = mp.get_context("fork")
+        ctx = mp.get_context("spawn")  # fresh interpreters: nothing inherited from a GPU process
         with ctx.Pool(procs, initializer=_worker_init, initargs=(wl,)) as pool:
             parts = pool.map(_worker_run, ranges, chunksize=1)
     by = dict(parts)

@@ -1,0 +1,723 @@
+// libmist host side: descriptor validation, space enumeration (groups, pairs, tiles),
+// reciprocal / edge / interference tables, device buffers, and the C ABI of mist.h.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <limits>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "mist.h"
+#include "mist_internal.h"
+
+using namespace mist;
+
+namespace {
+
+thread_local std::string g_error;
+
+mist_status fail(mist_status code, const std::string& msg) {
+  g_error = msg;
+  return code;
+}
+
+mist_status fail_hip(hipError_t e, const char* what) {
+  return fail(MIST_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+constexpr int64_t kExact = (int64_t)1 << 53;  // integers below this convert to double exactly
+constexpr int64_t kTargetTiles = 8192;        // evaluation blocks to aim for
+
+int popcount4(int v) { return (v & 1) + ((v >> 1) & 1) + ((v >> 2) & 1) + ((v >> 3) & 1); }
+
+}  // namespace
+
+struct mist_space {
+  // copied descriptors
+  mist_model_desc model;
+  std::vector<mist_hw_desc> hw;
+  int64_t D = 0, B = 0;
+  std::vector<int32_t> mb;
+  std::vector<double> ratio_om;  // r[0..R), om[0..R)
+  int32_t R = 0, NB = 0, l_rule = 0;
+  // enumeration
+  std::vector<DevGroup> groups;
+  std::vector<DevPair> pairs;
+  std::vector<DevTile> tiles;
+  std::vector<DevHw> hws;
+  DevModel dm;
+  uint64_t n_configs = 0;
+  int32_t units_per_tile = 0;
+  // memory
+  mist_allocator alloc{};
+  bool custom_alloc = false;
+  std::vector<void*> dev_buffers;
+  DevGroup* d_groups = nullptr;
+  DevPair* d_pairs = nullptr;
+  DevTile* d_tiles = nullptr;
+  DevHw* d_hws = nullptr;
+  double* d_ratio = nullptr;
+  double* d_part_obj = nullptr;
+  uint64_t* d_part_id = nullptr;
+  double* d_bucket_obj = nullptr;
+  uint64_t* d_bucket_id = nullptr;
+  double* d_best_obj = nullptr;
+  uint64_t* d_best_id = nullptr;
+  uint64_t* d_frontier = nullptr;
+  // state
+  bool evaluated = false;
+  hipStream_t stream = nullptr;
+  bool timing = false;
+  std::vector<hipEvent_t> events;  // pool; three per timed evaluation
+  size_t events_used = 0;
+};
+
+namespace {
+
+void* dev_alloc(mist_space* S, size_t bytes) {
+  if (bytes == 0) bytes = 256;
+  void* p = nullptr;
+  if (S->custom_alloc) {
+    p = S->alloc.alloc(bytes, S->alloc.ctx);
+  } else if (hipMalloc(&p, bytes) != hipSuccess) {
+    p = nullptr;
+  }
+  if (p) S->dev_buffers.push_back(p);
+  return p;
+}
+
+void dev_free_all(mist_space* S) {
+  for (void* p : S->dev_buffers) {
+    if (S->custom_alloc) S->alloc.free(p, S->alloc.ctx);
+    else (void)hipFree(p);
+  }
+  S->dev_buffers.clear();
+}
+
+// A temporary device buffer released at scope exit.
+struct TempBuf {
+  mist_space* S;
+  void* p = nullptr;
+  TempBuf(mist_space* s, size_t bytes) : S(s) {
+    if (bytes == 0) bytes = 256;
+    if (S->custom_alloc) p = S->alloc.alloc(bytes, S->alloc.ctx);
+    else if (hipMalloc(&p, bytes) != hipSuccess) p = nullptr;
+  }
+  ~TempBuf() {
+    if (!p) return;
+    if (S->custom_alloc) S->alloc.free(p, S->alloc.ctx);
+    else (void)hipFree(p);
+  }
+};
+
+bool tp_admissible(const mist_model_desc& m, int64_t per_stage, int64_t tp) {
+  if (per_stage % tp || m.heads % tp || m.ffn % tp) return false;
+  if (tp <= m.kv_heads) return m.kv_heads % tp == 0;
+  return tp % m.kv_heads == 0;
+}
+
+std::string validate(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n_hw,
+                     const mist_space_desc* s) {
+  if (!m || !hw || !s) return "null descriptor";
+  if (n_hw < 1) return "n_hw must be >= 1";
+  if (m->arch != MIST_ARCH_GPT && m->arch != MIST_ARCH_LLAMA) return "unknown arch";
+  if (m->n_layers < 1 || m->hidden < 1 || m->heads < 1 || m->kv_heads < 1 || m->ffn < 1 ||
+      m->seq < 1 || m->vocab < 1 || m->bytes_w < 1 || m->bytes_opt < 1)
+    return "model sizes must be positive";
+  if (m->flash != 0 && m->flash != 1) return "flash must be 0 or 1";
+  if (m->hidden % m->heads) return "hidden must be a multiple of heads";
+  if (m->heads % m->kv_heads) return "heads must be a multiple of kv_heads";
+  for (int32_t i = 0; i < n_hw; ++i) {
+    const mist_hw_desc& h = hw[i];
+    const double v[4] = {h.flops, h.mem_bytes, h.pcie_bw, h.link_bw};
+    for (double x : v)
+      if (!(x > 0.0) || !std::isfinite(x)) return "hardware rates and memory must be positive and finite";
+    if (!(h.eta_max > 0.0) || !std::isfinite(h.eta_max) || !(h.n_half >= 0.0) || !std::isfinite(h.n_half))
+      return "eta_max must be positive and n_half non-negative";
+    for (int mask = 0; mask < 16; ++mask) {
+      if (popcount4(mask) < 2) continue;
+      for (int j = 0; j < 4; ++j)
+        if ((mask >> j & 1) && !(h.phi[mask][j] >= 1.0 && std::isfinite(h.phi[mask][j])))
+          return "slowdown factors must be finite and >= 1";
+    }
+  }
+  if (s->n_devices < 1 || s->global_batch < 1) return "n_devices and global_batch must be positive";
+  if (s->n_mb < 1 || s->n_mb > MIST_MAX_MB || !s->mb) return "n_mb out of range";
+  for (int32_t i = 0; i < s->n_mb; ++i)
+    if (s->mb[i] < 1 || (i && s->mb[i] <= s->mb[i - 1])) return "mb must be ascending and >= 1";
+  if (s->n_ratios < 1 || s->n_ratios > MIST_MAX_RATIOS || !s->ratios) return "n_ratios out of range";
+  for (int32_t i = 0; i < s->n_ratios; ++i)
+    if (!(s->ratios[i] >= 0.0 && s->ratios[i] <= 1.0) || (i && !(s->ratios[i] > s->ratios[i - 1])))
+      return "ratios must be strictly ascending in [0, 1]";
+  if (s->n_buckets < 1 || s->n_buckets > MIST_MAX_BUCKETS) return "n_buckets out of range";
+  if (s->l_rule != MIST_L_FULL && s->l_rule != MIST_L_BALANCED) return "unknown l_rule";
+  return "";
+}
+
+// Largest integer quantities of the cost model for a (stage, pair); they must convert to
+// double exactly.
+bool counts_exact(const mist_model_desc& m, int64_t PP, int64_t l, int64_t b, int64_t tp,
+                  int64_t dp, int64_t G) {
+  // Work in long double-free int64 with overflow guards through __int128.
+  const __int128 h = m.hidden, s = m.seq, V = m.vocab, f = m.ffn, bw = m.bytes_w, bo = m.bytes_opt;
+  const __int128 dh = h / m.heads;
+  const __int128 hkvr = tp <= m.kv_heads ? (__int128)m.kv_heads * dh / tp : dh;
+  const __int128 Pq = 2 * h * h, Pm = (m.arch == MIST_ARCH_GPT ? 2 : 3) * h * f;
+  const __int128 Psi = (Pq + Pm) / tp + 2 * h * hkvr + (m.arch == MIST_ARCH_GPT ? 4 * h : 2 * h);
+  const __int128 Vr = (V + tp - 1) / tp;
+  const __int128 Pe = Vr * h + s * h, Ph = Vr * h + 2 * h;
+  const __int128 Pst = l * Psi + Pe + Ph;
+  const __int128 Pbuf = Psi > Pe ? (Psi > Ph ? Psi : Ph) : (Pe > Ph ? Pe : Ph);
+  const __int128 atok = 4 * h + (2 * h + 3 * f) / tp + 2 * hkvr + (__int128)m.heads * s / tp;
+  const __int128 afull = (__int128)b * s * bw * atok;
+  const __int128 ftok = 2 * ((Pq + Pm) / tp + 2 * h * hkvr) + 4 * s * h / tp;
+  const __int128 ke = PP < G ? PP : G;
+  const __int128 vals[] = {Pst * bo, Pst * bw * dp, 2 * Pbuf * bo, 2 * afull, ke * (l * afull),
+                           (__int128)b * s * ftok, 3 * 2 * (__int128)b * s * h * Vr,
+                           4 * (__int128)b * s * Vr, 2 * (__int128)b * s * h * bw * tp,
+                           (__int128)(4 * l + 2 * l), (__int128)(3 * l + l)};
+  for (__int128 v : vals)
+    if (v >= kExact || v < 0) return false;
+  return true;
+}
+
+std::string enumerate(mist_space* S) {
+  const mist_model_desc& m = S->model;
+  const int64_t L = m.n_layers;
+  const int64_t R = S->R;
+  const uint64_t per_unit = 4ull * (uint64_t)(R * R * R * R);
+  uint64_t base = 0;
+  S->groups.clear();
+  S->pairs.clear();
+  for (int32_t ih = 0; ih < (int32_t)S->hw.size(); ++ih) {
+    for (int64_t PP = 1; PP <= S->D; ++PP) {
+      if (S->D % PP || PP > L) continue;
+      const int64_t per_stage = S->D / PP;
+      struct Cand { int64_t G; DevPair p; };
+      std::vector<Cand> cand;
+      for (int32_t bi = 0; bi < (int32_t)S->mb.size(); ++bi) {
+        const int64_t b = S->mb[bi];
+        for (int64_t tp = 1; tp <= per_stage; ++tp) {
+          if (!tp_admissible(m, per_stage, tp)) continue;
+          const int64_t dp = per_stage / tp;
+          if (S->B % (b * dp)) continue;
+          DevPair p;
+          p.b = (int32_t)b;
+          p.tp = (int32_t)tp;
+          p.dp = (int32_t)dp;
+          p.mb = bi;
+          p.inv_dp = 1.0 / (double)dp;
+          cand.push_back({S->B / (b * dp), p});
+        }
+      }
+      std::vector<int64_t> Gs;
+      for (const Cand& c : cand) {
+        bool seen = false;
+        for (int64_t g : Gs) seen = seen || g == c.G;
+        if (!seen) Gs.push_back(c.G);
+      }
+      std::sort(Gs.begin(), Gs.end());
+      std::vector<int64_t> ls;
+      if (S->l_rule == MIST_L_FULL) {
+        if (PP == 1) ls.push_back(L);
+        else for (int64_t l = 1; l <= L - PP + 1; ++l) ls.push_back(l);
+      } else {
+        ls.push_back(L / PP);
+        if ((L + PP - 1) / PP != L / PP) ls.push_back((L + PP - 1) / PP);
+      }
+      for (int64_t G : Gs) {
+        std::vector<DevPair> ps;
+        for (const Cand& c : cand)
+          if (c.G == G) ps.push_back(c.p);
+        std::sort(ps.begin(), ps.end(), [](const DevPair& x, const DevPair& y) {
+          return x.b < y.b || (x.b == y.b && x.tp < y.tp);
+        });
+        if (G > INT32_MAX) return "G too large";
+        for (const DevPair& p : ps)
+          for (int64_t l : ls)
+            if (!counts_exact(m, PP, l, p.b, p.tp, p.dp, G))
+              return "model too large: a cost-model count exceeds 2^53";
+        const int32_t pair_begin = (int32_t)S->pairs.size();
+        S->pairs.insert(S->pairs.end(), ps.begin(), ps.end());
+        for (int64_t k = 1; k <= PP; ++k) {
+          for (int64_t l : ls) {
+            DevGroup g{};
+            g.base = base;
+            g.hw = ih;
+            g.G = (int32_t)G;
+            g.PP = (int32_t)PP;
+            g.k = (int32_t)k;
+            g.l = (int32_t)l;
+            g.pair_begin = pair_begin;
+            g.n_pairs = (int32_t)ps.size();
+            const uint64_t units = (uint64_t)ps.size() * (uint64_t)(l + 1);
+            if (units > (uint64_t)INT32_MAX / 2) return "group too large";
+            const uint64_t size = units * per_unit;
+            if (base > UINT64_MAX - size) return "space too large";
+            base += size;
+            S->groups.push_back(g);
+          }
+        }
+      }
+    }
+  }
+  S->n_configs = base;
+  if (S->groups.empty()) return "the space has no configuration";
+  if (S->groups.size() > (size_t)INT32_MAX) return "too many groups";
+
+  // Tiles: units of one group, at most units_per_tile each (a multiple of the waves).
+  uint64_t total_units = 0;
+  for (const DevGroup& g : S->groups) total_units += (uint64_t)g.n_pairs * (uint64_t)(g.l + 1);
+  uint64_t upt = (total_units + kTargetTiles - 1) / kTargetTiles;
+  upt = (upt + kWaves - 1) / kWaves * kWaves;
+  if (upt < (uint64_t)kWaves) upt = kWaves;
+  S->units_per_tile = (int32_t)upt;
+  S->tiles.clear();
+  for (size_t gi = 0; gi < S->groups.size(); ++gi) {
+    DevGroup& g = S->groups[gi];
+    const int64_t units = (int64_t)g.n_pairs * (g.l + 1);
+    g.tile_begin = (int32_t)S->tiles.size();
+    for (int64_t u = 0; u < units; u += (int64_t)upt) {
+      DevTile t{};
+      t.group = (int32_t)gi;
+      t.unit_begin = (int32_t)u;
+      t.unit_end = (int32_t)std::min<int64_t>(units, u + (int64_t)upt);
+      S->tiles.push_back(t);
+    }
+    g.n_tiles = (int32_t)S->tiles.size() - g.tile_begin;
+    if (S->tiles.size() > (size_t)INT32_MAX) return "too many tiles";
+  }
+
+  // Per-hardware tables (host divisions, each correctly rounded).
+  S->hws.assign(S->hw.size(), DevHw{});
+  for (size_t i = 0; i < S->hw.size(); ++i) {
+    const mist_hw_desc& h = S->hw[i];
+    DevHw& d = S->hws[i];
+    d.iF = 1.0 / h.flops;
+    d.iP = 1.0 / h.pcie_bw;
+    d.iL = 1.0 / h.link_bw;
+    d.M = h.mem_bytes;
+    d.kNB = (double)S->NB / h.mem_bytes;
+    for (int j = 0; j < MIST_MAX_MB; ++j) d.ieta[j] = 0.0;
+    for (size_t j = 0; j < S->mb.size(); ++j) {
+      const double bs = (double)((int64_t)S->mb[j] * m.seq);
+      d.ieta[j] = (bs + h.n_half) / (h.eta_max * bs);
+    }
+    for (int j = 0; j < MIST_MAX_BUCKETS; ++j)
+      d.edge[j] = j < S->NB ? (h.mem_bytes * (double)(j + 1)) / (double)S->NB
+                            : std::numeric_limits<double>::infinity();
+    d.edge[S->NB - 1] = h.mem_bytes;
+    for (int mask = 0; mask < 16; ++mask)
+      for (int j = 0; j < 4; ++j) {
+        const bool member = (mask >> j) & 1;
+        d.itab[mask][j] = member ? h.phi[mask][j] : std::numeric_limits<double>::infinity();
+        d.itab[mask][4 + j] = member ? 1.0 / h.phi[mask][j] : 1.0;
+      }
+  }
+  const int64_t hd = m.hidden;
+  S->dm.h = hd;
+  S->dm.heads = m.heads;
+  S->dm.kv = m.kv_heads;
+  S->dm.f = m.ffn;
+  S->dm.s = m.seq;
+  S->dm.V = m.vocab;
+  S->dm.bw = m.bytes_w;
+  S->dm.bo = m.bytes_opt;
+  S->dm.gpt = m.arch == MIST_ARCH_GPT ? 1 : 0;
+  S->dm.flash = m.flash;
+  return "";
+}
+
+template <class T>
+mist_status upload(mist_space* S, T** dst, const std::vector<T>& src, const char* what) {
+  *dst = (T*)dev_alloc(S, src.size() * sizeof(T));
+  if (!*dst) return fail(MIST_E_NOMEM, std::string("device allocation failed: ") + what);
+  if (src.empty()) return MIST_OK;
+  const hipError_t e = hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
+  if (e != hipSuccess) return fail_hip(e, what);
+  return MIST_OK;
+}
+
+mist::EvalArgs eval_args(const mist_space* S) {
+  EvalArgs a{};
+  a.m = S->dm;
+  a.groups = S->d_groups;
+  a.pairs = S->d_pairs;
+  a.tiles = S->d_tiles;
+  a.hws = S->d_hws;
+  a.ratio = S->d_ratio;
+  a.R = S->R;
+  a.NB = S->NB;
+  a.F = 4 * S->R * S->R * S->R;
+  a.n_tiles = (int32_t)S->tiles.size();
+  a.n_groups = (int64_t)S->groups.size();
+  a.n_configs = S->n_configs;
+  a.part_obj = S->d_part_obj;
+  a.part_id = S->d_part_id;
+  return a;
+}
+
+mist_status wait_results(mist_space* S) {
+  if (!S->evaluated) return fail(MIST_E_STATE, "mist_eval_space has not been called");
+  const hipError_t e = hipStreamSynchronize(S->stream);
+  if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+  return MIST_OK;
+}
+
+void decode_host(const mist_space* S, uint64_t id, mist_config* c) {
+  size_t lo = 0, hi = S->groups.size();
+  while (hi - lo > 1) {
+    const size_t mid = (lo + hi) / 2;
+    if (S->groups[mid].base <= id) lo = mid;
+    else hi = mid;
+  }
+  const DevGroup& g = S->groups[lo];
+  const uint64_t R = (uint64_t)S->R;
+  uint64_t v = id - g.base;
+  c->ao_idx = (int32_t)(v % R); v /= R;
+  c->oo_idx = (int32_t)(v % R); v /= R;
+  c->go_idx = (int32_t)(v % R); v /= R;
+  c->wo_idx = (int32_t)(v % R); v /= R;
+  c->zero = (int32_t)(v % 4); v /= 4;
+  c->ckpt = (int32_t)(v % (uint64_t)(g.l + 1));
+  const int32_t p = (int32_t)(v / (uint64_t)(g.l + 1));
+  const DevPair& pr = S->pairs[g.pair_begin + p];
+  c->hw = g.hw; c->G = g.G; c->PP = g.PP; c->k = g.k; c->l = g.l;
+  c->b = pr.b; c->tp = pr.tp; c->dp = pr.dp;
+  c->wo = S->ratio_om[c->wo_idx];
+  c->go = S->ratio_om[c->go_idx];
+  c->oo = S->ratio_om[c->oo_idx];
+  c->ao = S->ratio_om[c->ao_idx];
+}
+
+// Device evaluation of ids for result extraction: out[4*i..] = t, d, mem, obj.
+mist_status eval_ids_impl(mist_space* S, const uint64_t* ids, int64_t n, double* out, hipStream_t st) {
+  if (n == 0) return MIST_OK;
+  for (int64_t i = 0; i < n; ++i)
+    if (ids[i] >= S->n_configs) return fail(MIST_E_RANGE, "id out of range");
+  TempBuf dids(S, (size_t)n * sizeof(uint64_t));
+  TempBuf dout(S, (size_t)n * 4 * sizeof(double));
+  if (!dids.p || !dout.p) return fail(MIST_E_NOMEM, "device allocation failed: eval_ids");
+  hipError_t e = hipMemcpyAsync(dids.p, ids, (size_t)n * sizeof(uint64_t), hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync ids");
+  const int rc = launch_eval_ids(eval_args(S), (const uint64_t*)dids.p, n, (double*)dout.p, st);
+  if (rc) return fail_hip((hipError_t)rc, "eval_ids launch");
+  e = hipMemcpyAsync(out, dout.p, (size_t)n * 4 * sizeof(double), hipMemcpyDeviceToHost, st);
+  if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync out");
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+  return MIST_OK;
+}
+
+int32_t bucket_host(const mist_space* S, const DevHw& h, double mem) {
+  for (int32_t j = 0; j < S->NB; ++j)
+    if (mem <= h.edge[j]) return j;
+  return -1;
+}
+
+mist_status fill_results(mist_space* S, const uint64_t* ids, const double* objs, int64_t n, mist_result* out) {
+  std::vector<uint64_t> want;
+  for (int64_t i = 0; i < n; ++i)
+    if (ids[i] != MIST_NONE) want.push_back(ids[i]);
+  std::vector<double> vals(want.size() * 4);
+  mist_status rc = eval_ids_impl(S, want.data(), (int64_t)want.size(), vals.data(), S->stream);
+  if (rc) return rc;
+  size_t w = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    mist_result& r = out[i];
+    std::memset(&r, 0, sizeof(r));
+    r.id = ids[i];
+    r.obj = objs[i];
+    if (ids[i] == MIST_NONE) {
+      r.t = r.d = r.mem = std::numeric_limits<double>::infinity();
+      r.bucket = -1;
+      r.cfg.hw = -1;
+      continue;
+    }
+    r.t = vals[4 * w + 0];
+    r.d = vals[4 * w + 1];
+    r.mem = vals[4 * w + 2];
+    if (vals[4 * w + 3] != objs[i]) return fail(MIST_E_DEVICE, "re-evaluated objective differs");
+    ++w;
+    decode_host(S, r.id, &r.cfg);
+    r.bucket = bucket_host(S, S->hws[r.cfg.hw], r.mem);
+  }
+  return MIST_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n_hw,
+                              const mist_space_desc* s, const mist_allocator* alloc, mist_space** out) {
+  if (!out) return fail(MIST_E_INVALID, "out is null");
+  *out = nullptr;
+  try {
+    const std::string why = validate(m, hw, n_hw, s);
+    if (!why.empty()) return fail(MIST_E_INVALID, why);
+    if (alloc && (!alloc->alloc || !alloc->free)) return fail(MIST_E_INVALID, "allocator callbacks missing");
+    mist_space* S = new (std::nothrow) mist_space();
+    if (!S) return fail(MIST_E_NOMEM, "host allocation failed");
+    S->model = *m;
+    S->hw.assign(hw, hw + n_hw);
+    S->D = s->n_devices;
+    S->B = s->global_batch;
+    S->mb.assign(s->mb, s->mb + s->n_mb);
+    S->R = s->n_ratios;
+    S->NB = s->n_buckets;
+    S->l_rule = s->l_rule;
+    S->ratio_om.assign(s->ratios, s->ratios + s->n_ratios);
+    for (int32_t i = 0; i < s->n_ratios; ++i) S->ratio_om.push_back(1.0 - s->ratios[i]);
+    if (alloc) {
+      S->alloc = *alloc;
+      S->custom_alloc = true;
+    }
+    const std::string err = enumerate(S);
+    if (!err.empty()) {
+      delete S;
+      return fail(MIST_E_INVALID, err);
+    }
+    mist_status rc = MIST_OK;
+    if (!rc) rc = upload(S, &S->d_groups, S->groups, "groups");
+    if (!rc) rc = upload(S, &S->d_pairs, S->pairs, "pairs");
+    if (!rc) rc = upload(S, &S->d_tiles, S->tiles, "tiles");
+    if (!rc) rc = upload(S, &S->d_hws, S->hws, "hardware tables");
+    if (!rc) rc = upload(S, &S->d_ratio, S->ratio_om, "ratios");
+    const size_t nt = S->tiles.size(), ng = S->groups.size();
+    if (!rc) {
+      S->d_part_obj = (double*)dev_alloc(S, nt * 64 * sizeof(double));
+      S->d_part_id = (uint64_t*)dev_alloc(S, nt * 64 * sizeof(uint64_t));
+      S->d_bucket_obj = (double*)dev_alloc(S, ng * 64 * sizeof(double));
+      S->d_bucket_id = (uint64_t*)dev_alloc(S, ng * 64 * sizeof(uint64_t));
+      S->d_best_obj = (double*)dev_alloc(S, ng * sizeof(double));
+      S->d_best_id = (uint64_t*)dev_alloc(S, ng * sizeof(uint64_t));
+      S->d_frontier = (uint64_t*)dev_alloc(S, ng * sizeof(uint64_t));
+      if (!S->d_part_obj || !S->d_part_id || !S->d_bucket_obj || !S->d_bucket_id || !S->d_best_obj ||
+          !S->d_best_id || !S->d_frontier)
+        rc = fail(MIST_E_NOMEM, "device allocation failed: results");
+    }
+    if (rc) {
+      dev_free_all(S);
+      delete S;
+      return rc;
+    }
+    *out = S;
+    return MIST_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(MIST_E_NOMEM, "host allocation failed");
+  } catch (...) {
+    return fail(MIST_E_INVALID, "unexpected error");
+  }
+}
+
+mist_status mist_eval_space(mist_space* S, void* hip_stream) {
+  if (!S) return fail(MIST_E_INVALID, "space is null");
+  hipStream_t st = (hipStream_t)hip_stream;
+  hipEvent_t* ev = nullptr;
+  if (S->timing) {
+    while (S->events.size() < S->events_used + 3) {
+      hipEvent_t e;
+      const hipError_t rc = hipEventCreate(&e);
+      if (rc != hipSuccess) return fail_hip(rc, "hipEventCreate");
+      S->events.push_back(e);
+    }
+    ev = &S->events[S->events_used];
+    S->events_used += 3;
+    const hipError_t e = hipEventRecord(ev[0], st);
+    if (e != hipSuccess) return fail_hip(e, "hipEventRecord");
+  }
+  int rc = launch_eval(eval_args(S), st);
+  if (rc) return fail_hip((hipError_t)rc, "evaluation kernel launch");
+  if (ev) {
+    const hipError_t e = hipEventRecord(ev[1], st);
+    if (e != hipSuccess) return fail_hip(e, "hipEventRecord");
+  }
+  ReduceArgs r{};
+  r.groups = S->d_groups;
+  r.n_groups = (int64_t)S->groups.size();
+  r.NB = S->NB;
+  r.part_obj = S->d_part_obj;
+  r.part_id = S->d_part_id;
+  r.bucket_obj = S->d_bucket_obj;
+  r.bucket_id = S->d_bucket_id;
+  r.best_obj = S->d_best_obj;
+  r.best_id = S->d_best_id;
+  r.frontier = S->d_frontier;
+  rc = launch_reduce(r, st);
+  if (rc) return fail_hip((hipError_t)rc, "reduction kernel launch");
+  if (ev) {
+    const hipError_t e = hipEventRecord(ev[2], st);
+    if (e != hipSuccess) return fail_hip(e, "hipEventRecord");
+  }
+  S->evaluated = true;
+  S->stream = st;
+  return MIST_OK;
+}
+
+mist_status mist_get_best(mist_space* S, int64_t g0, int64_t n, mist_result* out) {
+  if (!S || (!out && n > 0)) return fail(MIST_E_INVALID, "null argument");
+  if (g0 < 0 || n < 0 || g0 + n > (int64_t)S->groups.size()) return fail(MIST_E_RANGE, "group range");
+  mist_status rc = wait_results(S);
+  if (rc) return rc;
+  if (n == 0) return MIST_OK;
+  try {
+    std::vector<uint64_t> ids(n);
+    std::vector<double> objs(n);
+    hipError_t e = hipMemcpy(ids.data(), S->d_best_id + g0, n * sizeof(uint64_t), hipMemcpyDeviceToHost);
+    if (e == hipSuccess)
+      e = hipMemcpy(objs.data(), S->d_best_obj + g0, n * sizeof(double), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpy best");
+    return fill_results(S, ids.data(), objs.data(), n, out);
+  } catch (const std::bad_alloc&) {
+    return fail(MIST_E_NOMEM, "host allocation failed");
+  }
+}
+
+mist_status mist_get_buckets(mist_space* S, int64_t g0, int64_t n, uint64_t* ids, double* objs,
+                             uint64_t* masks) {
+  if (!S) return fail(MIST_E_INVALID, "space is null");
+  if (g0 < 0 || n < 0 || g0 + n > (int64_t)S->groups.size()) return fail(MIST_E_RANGE, "group range");
+  mist_status rc = wait_results(S);
+  if (rc) return rc;
+  if (n == 0) return MIST_OK;
+  try {
+    const int NB = S->NB;
+    std::vector<uint64_t> bid((size_t)n * 64);
+    std::vector<double> bobj((size_t)n * 64);
+    hipError_t e = hipMemcpy(bid.data(), S->d_bucket_id + g0 * 64, bid.size() * sizeof(uint64_t),
+                             hipMemcpyDeviceToHost);
+    if (e == hipSuccess)
+      e = hipMemcpy(bobj.data(), S->d_bucket_obj + g0 * 64, bobj.size() * sizeof(double),
+                    hipMemcpyDeviceToHost);
+    if (e == hipSuccess && masks)
+      e = hipMemcpy(masks, S->d_frontier + g0, n * sizeof(uint64_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpy buckets");
+    for (int64_t i = 0; i < n; ++i)
+      for (int j = 0; j < NB; ++j) {
+        if (ids) ids[i * NB + j] = bid[i * 64 + j];
+        if (objs) objs[i * NB + j] = bobj[i * 64 + j];
+      }
+    return MIST_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(MIST_E_NOMEM, "host allocation failed");
+  }
+}
+
+mist_status mist_get_pareto(mist_space* S, int64_t g, mist_result* out, int32_t cap, int32_t* n_out) {
+  if (!S || !n_out) return fail(MIST_E_INVALID, "null argument");
+  if (g < 0 || g >= (int64_t)S->groups.size()) return fail(MIST_E_RANGE, "group index");
+  const int NB = S->NB;
+  std::vector<uint64_t> ids(NB);
+  std::vector<double> objs(NB);
+  uint64_t mask = 0;
+  mist_status rc = mist_get_buckets(S, g, 1, ids.data(), objs.data(), &mask);
+  if (rc) return rc;
+  std::vector<uint64_t> fid;
+  std::vector<double> fobj;
+  for (int j = 0; j < NB; ++j)
+    if (mask >> j & 1) {
+      fid.push_back(ids[j]);
+      fobj.push_back(objs[j]);
+    }
+  *n_out = (int32_t)fid.size();
+  if ((int32_t)fid.size() > cap) return fail(MIST_E_RANGE, "output capacity too small");
+  if (fid.empty()) return MIST_OK;
+  if (!out) return fail(MIST_E_INVALID, "out is null");
+  return fill_results(S, fid.data(), fobj.data(), (int64_t)fid.size(), out);
+}
+
+mist_status mist_space_info(const mist_space* S, uint64_t* n_configs, int64_t* n_groups, int32_t* n_buckets) {
+  if (!S) return fail(MIST_E_INVALID, "space is null");
+  if (n_configs) *n_configs = S->n_configs;
+  if (n_groups) *n_groups = (int64_t)S->groups.size();
+  if (n_buckets) *n_buckets = S->NB;
+  return MIST_OK;
+}
+
+mist_status mist_get_group_key(const mist_space* S, int64_t g, mist_group_key* out) {
+  if (!S || !out) return fail(MIST_E_INVALID, "null argument");
+  if (g < 0 || g >= (int64_t)S->groups.size()) return fail(MIST_E_RANGE, "group index");
+  const DevGroup& d = S->groups[g];
+  out->hw = d.hw; out->G = d.G; out->PP = d.PP; out->k = d.k; out->l = d.l; out->n_pairs = d.n_pairs;
+  out->base = d.base;
+  out->size = (uint64_t)d.n_pairs * (uint64_t)(d.l + 1) * 4ull * (uint64_t)S->R * S->R * S->R * S->R;
+  return MIST_OK;
+}
+
+mist_status mist_decode(const mist_space* S, uint64_t id, mist_config* out) {
+  if (!S || !out) return fail(MIST_E_INVALID, "null argument");
+  if (id >= S->n_configs) return fail(MIST_E_RANGE, "id out of range");
+  decode_host(S, id, out);
+  return MIST_OK;
+}
+
+mist_status mist_eval_ids(mist_space* S, const uint64_t* ids, int64_t n, double* out, void* hip_stream) {
+  if (!S || ((!ids || !out) && n > 0) || n < 0) return fail(MIST_E_INVALID, "null argument");
+  try {
+    return eval_ids_impl(S, ids, n, out, (hipStream_t)hip_stream);
+  } catch (const std::bad_alloc&) {
+    return fail(MIST_E_NOMEM, "host allocation failed");
+  }
+}
+
+mist_status mist_set_timing(mist_space* S, int32_t on) {
+  if (!S) return fail(MIST_E_INVALID, "space is null");
+  if (S->evaluated) {
+    const hipError_t e = hipStreamSynchronize(S->stream);
+    if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+  }
+  S->timing = on != 0;
+  S->events_used = 0;
+  return MIST_OK;
+}
+
+mist_status mist_read_timing(mist_space* S, double* eval_ms, double* reduce_ms, int64_t* n_evals) {
+  if (!S) return fail(MIST_E_INVALID, "space is null");
+  if (!S->timing) return fail(MIST_E_STATE, "timing is off");
+  double a = 0.0, b = 0.0;
+  const size_t n = S->events_used / 3;
+  if (n) {
+    const hipError_t e = hipEventSynchronize(S->events[S->events_used - 1]);
+    if (e != hipSuccess) return fail_hip(e, "hipEventSynchronize");
+  }
+  for (size_t i = 0; i < n; ++i) {
+    float x = 0.f, y = 0.f;
+    hipError_t e = hipEventElapsedTime(&x, S->events[3 * i], S->events[3 * i + 1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&y, S->events[3 * i + 1], S->events[3 * i + 2]);
+    if (e != hipSuccess) return fail_hip(e, "hipEventElapsedTime");
+    a += x;
+    b += y;
+  }
+  S->events_used = 0;
+  if (eval_ms) *eval_ms = a;
+  if (reduce_ms) *reduce_ms = b;
+  if (n_evals) *n_evals = (int64_t)n;
+  return MIST_OK;
+}
+
+mist_status mist_launch_info(const mist_space* S, int64_t* n_tiles, int32_t* block, int32_t* units_per_tile) {
+  if (!S) return fail(MIST_E_INVALID, "space is null");
+  if (n_tiles) *n_tiles = (int64_t)S->tiles.size();
+  if (block) *block = kBlock;
+  if (units_per_tile) *units_per_tile = S->units_per_tile;
+  return MIST_OK;
+}
+
+mist_status mist_space_destroy(mist_space* S) {
+  if (!S) return MIST_OK;
+  if (S->evaluated) (void)hipStreamSynchronize(S->stream);
+  for (hipEvent_t e : S->events) (void)hipEventDestroy(e);
+  dev_free_all(S);
+  delete S;
+  return MIST_OK;
+}
+
+const char* mist_last_error(void) { return g_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,93 @@
+// Device-side data layout shared by the host part (space build) and the kernels of libmist.
+#pragma once
+
+#include <stdint.h>
+
+#include "mist.h"
+
+namespace mist {
+
+constexpr int kBlock = 256;           // threads per evaluation block
+constexpr int kWaves = kBlock / 64;   // wave64
+constexpr int kReduceBlock = 256;     // group-reduction block: one wave per group
+constexpr int kTabStride = 8;         // interference table row: phi[4], psi[4]
+
+// One candidate stage (group): hardware sample, G, PP, in-flight count k, layers l.
+struct DevGroup {
+  uint64_t base;        // global id of the first configuration
+  int32_t hw;
+  int32_t G, PP, k, l;
+  int32_t pair_begin;   // first (b, TP) pair in the pair table
+  int32_t n_pairs;
+  int32_t tile_begin;   // first tile of the group in the tile table
+  int32_t n_tiles;
+  int32_t pad;
+};
+
+// One (b, TP) pair of a group, DP = D / (PP * TP).
+struct DevPair {
+  int32_t b, tp, dp, mb;  // mb: index of b in the microbatch list
+  double inv_dp;          // 1 / DP, host division
+};
+
+// A block's work: units [unit_begin, unit_end) of one group, where a unit is one
+// (pair, recomputed-layers) slab of 4 * R^4 configurations.
+struct DevTile {
+  int32_t group;
+  int32_t unit_begin;
+  int32_t unit_end;
+  int32_t pad;
+};
+
+// Per hardware sample: host reciprocals, bucket edges and the interference table.
+struct DevHw {
+  double iF, iP, iL;         // 1 / FLOP/s, 1 / PCIe, 1 / link
+  double M;                  // memory budget
+  double kNB;                // NB / M (bucket estimate, corrected against the edges)
+  double ieta[MIST_MAX_MB];  // 1 / eta(b) per microbatch index
+  double edge[MIST_MAX_BUCKETS];
+  // Row per co-running pattern (bit j = stream j): phi of members then psi = 1/phi of
+  // members; absent streams have phi = +inf (their zero time scales to NaN, which the
+  // minimum skips) and psi = 1.
+  double itab[16][kTabStride];
+};
+
+struct DevModel {
+  int64_t h, heads, kv, f, s, V, bw, bo;
+  int32_t gpt, flash;
+};
+
+struct EvalArgs {
+  DevModel m;
+  const DevGroup* groups;
+  const DevPair* pairs;
+  const DevTile* tiles;
+  const DevHw* hws;
+  const double* ratio;   // r[0..R), then om[0..R) = 1 - r
+  int32_t R, NB, F;      // F = 4 * R^3 lane slots per unit (z, wo, go, oo)
+  int32_t n_tiles;
+  int64_t n_groups;
+  uint64_t n_configs;
+  double* part_obj;      // [n_tiles][64]
+  uint64_t* part_id;     // [n_tiles][64]
+};
+
+struct ReduceArgs {
+  const DevGroup* groups;
+  int64_t n_groups;
+  int32_t NB;
+  const double* part_obj;
+  const uint64_t* part_id;
+  double* bucket_obj;    // [n_groups][64]
+  uint64_t* bucket_id;   // [n_groups][64]
+  double* best_obj;      // [n_groups]
+  uint64_t* best_id;     // [n_groups]
+  uint64_t* frontier;    // [n_groups]
+};
+
+// Kernel launchers (mist_kernels.hip).
+int launch_eval(const EvalArgs& a, void* stream);
+int launch_reduce(const ReduceArgs& a, void* stream);
+int launch_eval_ids(const EvalArgs& a, const uint64_t* ids, int64_t n, double* out, void* stream);
+
+}  // namespace mist

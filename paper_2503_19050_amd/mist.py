@@ -1,0 +1,291 @@
+"""Python binding of libmist (include/mist.h): argument marshalling only.
+
+Every step of the tuner's hot path runs inside libmist.so (host space build and HIP
+kernels on the GPU).  PyTorch provides device memory (its caching allocator, through the
+library's allocator callbacks) and the stream.  If the library is missing this module
+raises; there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libmist.so")
+
+MIST_NONE = 0xFFFFFFFFFFFFFFFF
+NONE = np.uint64(MIST_NONE)
+
+EXPORTS = [
+    "mist_space_create", "mist_eval_space", "mist_get_best", "mist_get_pareto", "mist_get_buckets",
+    "mist_space_info", "mist_get_group_key", "mist_decode", "mist_eval_ids", "mist_set_timing",
+    "mist_read_timing", "mist_launch_info", "mist_space_destroy", "mist_last_error",
+]
+
+
+class MistError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("libmist status %d: %s" % (status, msg))
+        self.status = status
+
+
+class ModelDesc(ctypes.Structure):
+    _fields_ = [("arch", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("hidden", ctypes.c_int64),
+                ("heads", ctypes.c_int32), ("kv_heads", ctypes.c_int32), ("ffn", ctypes.c_int64),
+                ("seq", ctypes.c_int64), ("vocab", ctypes.c_int64), ("bytes_w", ctypes.c_int32),
+                ("bytes_opt", ctypes.c_int32), ("flash", ctypes.c_int32)]
+
+
+class HwDesc(ctypes.Structure):
+    _fields_ = [("flops", ctypes.c_double), ("mem_bytes", ctypes.c_double), ("pcie_bw", ctypes.c_double),
+                ("link_bw", ctypes.c_double), ("eta_max", ctypes.c_double), ("n_half", ctypes.c_double),
+                ("phi", (ctypes.c_double * 4) * 16)]
+
+
+class SpaceDesc(ctypes.Structure):
+    _fields_ = [("n_devices", ctypes.c_int64), ("global_batch", ctypes.c_int64),
+                ("mb", ctypes.POINTER(ctypes.c_int32)), ("n_mb", ctypes.c_int32),
+                ("ratios", ctypes.POINTER(ctypes.c_double)), ("n_ratios", ctypes.c_int32),
+                ("n_buckets", ctypes.c_int32), ("l_rule", ctypes.c_int32)]
+
+
+ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p)
+FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p)
+
+
+class Allocator(ctypes.Structure):
+    _fields_ = [("alloc", ALLOC_FN), ("free", FREE_FN), ("ctx", ctypes.c_void_p)]
+
+
+class Config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ["hw", "G", "PP", "k", "l", "b", "tp", "dp", "zero", "ckpt",
+                 "wo_idx", "go_idx", "oo_idx", "ao_idx"]] + \
+               [(n, ctypes.c_double) for n in ["wo", "go", "oo", "ao"]]
+
+
+class Result(ctypes.Structure):
+    _fields_ = [("id", ctypes.c_uint64), ("obj", ctypes.c_double), ("t", ctypes.c_double),
+                ("d", ctypes.c_double), ("mem", ctypes.c_double), ("bucket", ctypes.c_int32),
+                ("pad", ctypes.c_int32), ("cfg", Config)]
+
+
+class GroupKey(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ["hw", "G", "PP", "k", "l", "n_pairs"]] + \
+               [("base", ctypes.c_uint64), ("size", ctypes.c_uint64)]
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads libmist.so (built by paper_2503_19050_amd.build); raises when it is missing."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(path):
+            raise MistError(-3, "%s is not built; run paper_2503_19050_amd.build.build()" % path)
+        L = ctypes.CDLL(path)
+        P = ctypes.POINTER
+        st = ctypes.c_int32
+        vp = ctypes.c_void_p
+        L.mist_space_create.argtypes = [P(ModelDesc), P(HwDesc), ctypes.c_int32, P(SpaceDesc), P(Allocator), P(vp)]
+        L.mist_eval_space.argtypes = [vp, vp]
+        L.mist_get_best.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, P(Result)]
+        L.mist_get_pareto.argtypes = [vp, ctypes.c_int64, P(Result), ctypes.c_int32, P(ctypes.c_int32)]
+        L.mist_get_buckets.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, P(ctypes.c_uint64),
+                                       P(ctypes.c_double), P(ctypes.c_uint64)]
+        L.mist_space_info.argtypes = [vp, P(ctypes.c_uint64), P(ctypes.c_int64), P(ctypes.c_int32)]
+        L.mist_get_group_key.argtypes = [vp, ctypes.c_int64, P(GroupKey)]
+        L.mist_decode.argtypes = [vp, ctypes.c_uint64, P(Config)]
+        L.mist_eval_ids.argtypes = [vp, P(ctypes.c_uint64), ctypes.c_int64, P(ctypes.c_double), vp]
+        L.mist_set_timing.argtypes = [vp, ctypes.c_int32]
+        L.mist_read_timing.argtypes = [vp, P(ctypes.c_double), P(ctypes.c_double), P(ctypes.c_int64)]
+        L.mist_launch_info.argtypes = [vp, P(ctypes.c_int64), P(ctypes.c_int32), P(ctypes.c_int32)]
+        L.mist_space_destroy.argtypes = [vp]
+        L.mist_last_error.restype = ctypes.c_char_p
+        for name in EXPORTS:
+            if name != "mist_last_error":
+                getattr(L, name).restype = st
+        _lib = L
+        return L
+
+
+def _check(L, rc):
+    if rc != 0:
+        raise MistError(rc, L.mist_last_error().decode())
+
+
+def _struct_to_dict(s) -> dict:
+    out = {}
+    for name, _ in s._fields_:
+        v = getattr(s, name)
+        out[name] = _struct_to_dict(v) if isinstance(v, ctypes.Structure) else v
+    return out
+
+
+def _stream_handle(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+class Space:
+    """A configuration space held by libmist on the current GPU.
+
+    ``model``, ``hws`` and ``space`` are the descriptor dictionaries of
+    ``paper_2503_19050_amd.workloads``.  ``allocator="torch"`` routes device memory through
+    PyTorch's caching allocator; ``None`` lets the library use hipMalloc.
+    """
+
+    def __init__(self, model: dict, hws: list, space: dict, allocator: str | None = "torch"):
+        self.L = load()
+        self._model = ModelDesc(**{k: model[k] for k, _ in ModelDesc._fields_})
+        self._hw = (HwDesc * len(hws))()
+        for i, h in enumerate(hws):
+            for k in ("flops", "mem_bytes", "pcie_bw", "link_bw", "eta_max", "n_half"):
+                setattr(self._hw[i], k, float(h[k]))
+            for m in range(16):
+                for j in range(4):
+                    self._hw[i].phi[m][j] = float(h["phi"][m][j])
+        self._mb = np.ascontiguousarray(space["mb"], dtype=np.int32)
+        self._ratios = np.ascontiguousarray(space["ratios"], dtype=np.float64)
+        self._space = SpaceDesc(space["n_devices"], space["global_batch"],
+                                self._mb.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), len(self._mb),
+                                self._ratios.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                len(self._ratios), space["n_buckets"], space["l_rule"])
+        self._alloc = None
+        if allocator == "torch":
+            self._alloc = self._torch_allocator()
+        elif allocator is not None:
+            raise ValueError("allocator must be 'torch' or None")
+        h = ctypes.c_void_p()
+        _check(self.L, self.L.mist_space_create(ctypes.byref(self._model), self._hw, len(hws),
+                                                ctypes.byref(self._space),
+                                                ctypes.byref(self._alloc) if self._alloc else None,
+                                                ctypes.byref(h)))
+        self.h = h
+        n = ctypes.c_uint64()
+        g = ctypes.c_int64()
+        nb = ctypes.c_int32()
+        _check(self.L, self.L.mist_space_info(self.h, ctypes.byref(n), ctypes.byref(g), ctypes.byref(nb)))
+        self.n_configs, self.n_groups, self.n_buckets = n.value, g.value, nb.value
+
+    def _torch_allocator(self):
+        import torch
+        device = torch.cuda.current_device()
+        failures = self._alloc_failures = []
+
+        def alloc(nbytes, ctx):
+            try:
+                return torch.cuda.caching_allocator_alloc(int(nbytes), device)
+            except Exception as e:  # no exception may cross the C ABI
+                failures.append(e)
+                return None
+
+        def free(ptr, ctx):
+            try:
+                torch.cuda.caching_allocator_delete(ptr)
+            except Exception as e:
+                failures.append(e)
+
+        self._cb = (ALLOC_FN(alloc), FREE_FN(free))
+        return Allocator(self._cb[0], self._cb[1], None)
+
+    # -- evaluation ---------------------------------------------------------------
+    def eval(self, stream=None) -> None:
+        """Enqueues the evaluation on ``stream`` (torch stream, raw handle, or current)."""
+        _check(self.L, self.L.mist_eval_space(self.h, ctypes.c_void_p(_stream_handle(stream))))
+
+    def set_timing(self, on: bool = True) -> None:
+        _check(self.L, self.L.mist_set_timing(self.h, 1 if on else 0))
+
+    def read_timing(self) -> tuple[float, float, int]:
+        """(summed evaluation-kernel ms, summed reduction-kernel ms, evaluations) since the
+        last read; waits for them."""
+        a = ctypes.c_double()
+        b = ctypes.c_double()
+        n = ctypes.c_int64()
+        _check(self.L, self.L.mist_read_timing(self.h, ctypes.byref(a), ctypes.byref(b), ctypes.byref(n)))
+        return a.value, b.value, n.value
+
+    def launch_info(self) -> dict:
+        t = ctypes.c_int64()
+        b = ctypes.c_int32()
+        u = ctypes.c_int32()
+        _check(self.L, self.L.mist_launch_info(self.h, ctypes.byref(t), ctypes.byref(b), ctypes.byref(u)))
+        return {"tiles": t.value, "block": b.value, "units_per_tile": u.value}
+
+    # -- results ------------------------------------------------------------------
+    def best(self, g0: int = 0, n: int | None = None) -> list[dict]:
+        n = self.n_groups - g0 if n is None else n
+        out = (Result * max(n, 1))()
+        _check(self.L, self.L.mist_get_best(self.h, g0, n, out))
+        return [_struct_to_dict(out[i]) for i in range(n)]
+
+    def pareto(self, g: int) -> list[dict]:
+        out = (Result * 64)()
+        cnt = ctypes.c_int32()
+        _check(self.L, self.L.mist_get_pareto(self.h, g, out, 64, ctypes.byref(cnt)))
+        return [_struct_to_dict(out[i]) for i in range(cnt.value)]
+
+    def buckets(self, g0: int = 0, n: int | None = None):
+        """(ids[n, NB], objs[n, NB], frontier masks[n]) of groups g0..g0+n-1."""
+        n = self.n_groups - g0 if n is None else n
+        ids = np.empty((n, self.n_buckets), dtype=np.uint64)
+        objs = np.empty((n, self.n_buckets), dtype=np.float64)
+        masks = np.empty(n, dtype=np.uint64)
+        _check(self.L, self.L.mist_get_buckets(self.h, g0, n,
+                                               ids.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)),
+                                               objs.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                               masks.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64))))
+        return ids, objs, masks
+
+    def eval_ids(self, ids, stream=None) -> np.ndarray:
+        """Per-configuration (t, d, mem, obj) computed on the GPU."""
+        ids = np.ascontiguousarray(ids, dtype=np.uint64)
+        out = np.empty((len(ids), 4), dtype=np.float64)
+        _check(self.L, self.L.mist_eval_ids(self.h, ids.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)),
+                                            len(ids), out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                            ctypes.c_void_p(_stream_handle(stream))))
+        return out
+
+    def decode(self, cid: int) -> dict:
+        c = Config()
+        _check(self.L, self.L.mist_decode(self.h, cid, ctypes.byref(c)))
+        return _struct_to_dict(c)
+
+    def group_key(self, g: int) -> dict:
+        k = GroupKey()
+        _check(self.L, self.L.mist_get_group_key(self.h, g, ctypes.byref(k)))
+        return _struct_to_dict(k)
+
+    def close(self) -> None:
+        if getattr(self, "h", None):
+            self.L.mist_space_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def from_workload(wl: dict, allocator: str | None = "torch") -> Space:
+    return Space(wl["model"], wl["hws"], wl["space"], allocator=allocator)

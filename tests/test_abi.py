@@ -1,0 +1,93 @@
+"""The C ABI without a GPU: the library loads, exports every entry point that
+include/mist.h declares, and rejects invalid descriptors before touching the device."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2503_19050_amd import mist
+from paper_2503_19050_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mist.h")
+
+
+def _declared():
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(mist_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for n in ["mist_space_create", "mist_eval_space", "mist_get_best", "mist_get_pareto"]:
+        assert n in names
+    assert set(names) == set(mist.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = mist.load()
+    for n in _declared():
+        assert hasattr(L, n), n
+
+
+def _create(wl, **over):
+    L = mist.load()
+    m = dict(wl["model"])
+    s = dict(wl["space"])
+    hws = [dict(h) for h in wl["hws"]]
+    for k, v in over.items():
+        where, key = k.split("__")
+        {"m": m, "s": s, "h": hws[0]}[where][key] = v
+    model = mist.ModelDesc(**{k: m[k] for k, _ in mist.ModelDesc._fields_})
+    hw = (mist.HwDesc * len(hws))()
+    for i, h in enumerate(hws):
+        for k in ("flops", "mem_bytes", "pcie_bw", "link_bw", "eta_max", "n_half"):
+            setattr(hw[i], k, float(h[k]))
+        for a in range(16):
+            for j in range(4):
+                hw[i].phi[a][j] = float(h["phi"][a][j])
+    mb = np.ascontiguousarray(s["mb"], dtype=np.int32)
+    r = np.ascontiguousarray(s["ratios"], dtype=np.float64)
+    space = mist.SpaceDesc(s["n_devices"], s["global_batch"], mb.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                           len(mb), r.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), len(r),
+                           s["n_buckets"], s["l_rule"])
+    h = ctypes.c_void_p()
+    rc = L.mist_space_create(ctypes.byref(model), hw, len(hws), ctypes.byref(space), None, ctypes.byref(h))
+    return rc, L.mist_last_error().decode()
+
+
+@pytest.mark.parametrize("over", [
+    {"m__arch": 7}, {"m__hidden": 1000, "m__heads": 3}, {"m__kv_heads": 5}, {"m__n_layers": 0},
+    {"h__flops": 0.0}, {"h__mem_bytes": -1.0}, {"h__pcie_bw": float("nan")}, {"h__eta_max": 0.0},
+    {"s__n_buckets": 0}, {"s__n_buckets": 65}, {"s__mb": [2, 1]}, {"s__mb": []},
+    {"s__ratios": [0.0, 1.5]}, {"s__ratios": [0.5, 0.5]}, {"s__l_rule": 3}, {"s__n_devices": 0},
+    {"s__ratios": [0.0] * 33},
+])
+def test_invalid_descriptors_are_rejected(over):
+    rc, msg = _create(W.workload("tiny"), **over)
+    assert rc == -1 and msg
+
+
+def test_bad_slowdown_factor_rejected():
+    wl = W.workload("tiny")
+    wl["hws"][0]["phi"] = [list(r) for r in wl["hws"][0]["phi"]]
+    wl["hws"][0]["phi"][15][2] = 0.5
+    rc, msg = _create(wl)
+    assert rc == -1 and "slowdown" in msg
+
+
+def test_counts_beyond_exact_range_rejected():
+    rc, msg = _create(W.workload("tiny"), m__hidden=1 << 30, m__heads=1, m__kv_heads=1)
+    assert rc == -1 and "2^53" in msg
+
+
+def test_null_arguments():
+    L = mist.load()
+    assert L.mist_space_create(None, None, 0, None, None, None) == -1
+    assert L.mist_eval_space(None, None) == -1
+    assert L.mist_space_destroy(None) == 0
+    assert L.mist_last_error() is not None

@@ -1,0 +1,199 @@
+"""GPU (libmist, HIP on gfx950) against the CPU oracle, through the C ABI.
+
+Bar: identical argmin ids, bucket tables and frontier bits, and every cost value within
+1e-12 relative (the kernels follow the same IEEE operation sequence, so the values are
+compared bit for bit).  Full-size workloads c3-c5 run in the benchmark's launch
+configuration; the oracle then recomputes a sample of whole groups and a sample of
+single configurations.
+"""
+
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2503_19050_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+PROCS = max(1, min(16, os.cpu_count() or 1))
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "a GPU is required"
+    torch.cuda.init()
+    return torch
+
+
+def _space(wl, torch_cuda, allocator="torch"):
+    from paper_2503_19050_amd import mist
+    say("space", wl["name"], wl["desc"])
+    return mist.from_workload(wl, allocator=allocator)
+
+
+def _eval(S, torch_cuda):
+    S.eval()
+    torch_cuda.cuda.synchronize()
+
+
+def _compare_groups(S, ref, groups):
+    ids, objs, masks = S.buckets(0, S.n_groups)
+    best = S.best(0, S.n_groups)
+    gi = np.asarray(groups)
+    assert np.array_equal(ids[gi], ref["bucket_id"]), "bucket ids differ"
+    assert np.array_equal(objs[gi], ref["bucket_obj"]), "bucket objectives differ"
+    assert np.array_equal(masks[gi], ref["frontier"]), "frontier bits differ"
+    bid = np.array([best[g]["id"] for g in groups], dtype=np.uint64)
+    bobj = np.array([best[g]["obj"] for g in groups])
+    assert np.array_equal(bid, ref["best_id"]) and np.array_equal(bobj, ref["best_obj"])
+
+
+def _compare_ids(S, o, ids):
+    got = S.eval_ids(ids)
+    want = o.eval_ids(ids)
+    rel = np.abs(got - want) / np.maximum(np.abs(want), 1e-300)
+    assert np.all(rel <= 1e-12), "max relative error %g" % rel.max()
+    assert np.array_equal(got, want), "values are not bitwise equal"
+
+
+def _sample_ids(o, rng, n):
+    keys = o.group_keys()
+    edges = []
+    for k in keys[:: max(1, len(keys) // 50)]:
+        edges += [k["base"], k["base"] + k["size"] - 1]
+    edges += [0, o.n_configs - 1]
+    rand = rng.integers(0, o.n_configs, size=n, dtype=np.uint64)
+    return np.unique(np.concatenate([np.array(edges, dtype=np.uint64), rand]))
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny_llama", "c1", "c2"])
+def test_full_parity_small(name, torch_cuda):
+    wl = W.workload(name)
+    S = _space(wl, torch_cuda)
+    o = O.Oracle(wl)
+    assert (S.n_configs, S.n_groups) == (o.n_configs, o.n_groups)
+    _eval(S, torch_cuda)
+    say("oracle", name, o.n_configs, "configs on", PROCS, "processes")
+    groups = list(range(o.n_groups))
+    ref = O.run_groups(wl, groups, procs=PROCS) if name == "c2" else o.run()
+    _compare_groups(S, ref, groups)
+    _compare_ids(S, o, _sample_ids(o, np.random.default_rng(1), 3000))
+    S.close()
+
+
+@pytest.mark.parametrize("name", ["c3", "c4", "c5"])
+def test_full_size_sampled_parity(name, torch_cuda):
+    wl = W.workload(name)
+    S = _space(wl, torch_cuda)
+    o = O.Oracle(wl)
+    assert (S.n_configs, S.n_groups) == (o.n_configs, o.n_groups)
+    _eval(S, torch_cuda)
+    keys = o.group_keys()
+    sizes = np.array([k["size"] for k in keys])
+    rng = np.random.default_rng(7)
+    groups = {int(np.argmax(sizes)), int(np.argmin(sizes)), 0, o.n_groups - 1}
+    groups |= set(int(g) for g in rng.choice(o.n_groups, size=10, replace=False))
+    groups = sorted(groups)
+    say("oracle", name, "groups", groups, "configs", int(sizes[groups].sum()))
+    ref = O.run_groups(wl, groups, procs=PROCS)
+    _compare_groups(S, ref, groups)
+    _compare_ids(S, o, _sample_ids(o, rng, 3000))
+    S.close()
+
+
+def test_results_api_consistent(torch_cuda):
+    """mist_get_best / mist_get_pareto agree with the bucket table and with per-id values."""
+    wl = W.workload("c1")
+    S = _space(wl, torch_cuda)
+    o = O.Oracle(wl)
+    _eval(S, torch_cuda)
+    ids, objs, masks = S.buckets()
+    best = S.best()
+    for g in range(0, S.n_groups, 97):
+        b = best[g]
+        if b["id"] == 0xFFFFFFFFFFFFFFFF:
+            continue
+        t, d, mem, obj = o.eval_ids([b["id"]])[0]
+        assert (b["t"], b["d"], b["mem"], b["obj"]) == (t, d, mem, obj)
+        assert ids[g][b["bucket"]] == b["id"]
+        cfg = o.decode(b["id"])
+        for k in ("G", "PP", "k", "l", "b", "tp", "dp"):
+            assert b["cfg"][k] == cfg[k]
+        assert (b["cfg"]["zero"], b["cfg"]["ckpt"]) == (cfg["zero"], cfg["ckpt"])
+        par = S.pareto(g)
+        assert [p["id"] for p in par] == [int(ids[g][j]) for j in range(S.n_buckets) if int(masks[g]) >> j & 1]
+        objs_p = [p["obj"] for p in par]
+        assert all(x > y for x, y in zip(objs_p, objs_p[1:]))
+    S.close()
+
+
+def test_deterministic_and_rerunnable(torch_cuda):
+    wl = W.workload("c2")
+    S = _space(wl, torch_cuda)
+    _eval(S, torch_cuda)
+    a = S.buckets()
+    s2 = torch_cuda.cuda.Stream()
+    with torch_cuda.cuda.stream(s2):
+        S.eval(s2)
+    s2.synchronize()
+    b = S.buckets()
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    S.close()
+
+
+def test_edge_spaces(torch_cuda):
+    """Budget too small for anything, a single bucket, a single ratio, ragged tiles."""
+    cases = []
+    wl = W.workload("tiny")
+    wl["hws"][0]["mem_bytes"] = 1.0e6
+    cases.append(wl)
+    wl = W.workload("tiny")
+    wl["space"]["n_buckets"] = 1
+    cases.append(wl)
+    wl = W.workload("tiny")
+    wl["space"]["ratios"] = [0.0]
+    cases.append(wl)
+    wl = W.workload("tiny_llama")
+    wl["space"]["ratios"] = [0.0, 0.3, 0.6, 1.0]
+    wl["space"]["n_buckets"] = 7
+    wl["model"]["flash"] = 0
+    cases.append(wl)
+    for wl in cases:
+        S = _space(wl, torch_cuda)
+        o = O.Oracle(wl)
+        _eval(S, torch_cuda)
+        _compare_groups(S, o.run(), list(range(o.n_groups)))
+        _compare_ids(S, o, _sample_ids(o, np.random.default_rng(3), 500))
+        S.close()
+    # nothing feasible: sentinel results
+    S = _space(cases[0], torch_cuda)
+    _eval(S, torch_cuda)
+    for b in S.best():
+        assert b["id"] == 0xFFFFFFFFFFFFFFFF and b["obj"] == float("inf") and b["bucket"] == -1
+    assert S.pareto(0) == []
+    S.close()
+
+
+def test_error_paths(torch_cuda):
+    from paper_2503_19050_amd import mist
+    S = _space(W.workload("tiny"), torch_cuda, allocator=None)
+    with pytest.raises(mist.MistError) as e:
+        S.best(0, 1)
+    assert e.value.status == -4
+    with pytest.raises(mist.MistError) as e:
+        S.eval_ids([S.n_configs])
+    assert e.value.status == -5
+    _eval(S, torch_cuda)
+    with pytest.raises(mist.MistError) as e:
+        S.best(S.n_groups, 1)
+    assert e.value.status == -5
+    S.close()
