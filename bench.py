@@ -160,7 +160,7 @@ def main() -> int:
         "vs_baseline": None, "dtype": "f64", "data": "synthetic",
         "config": {"workload": "%s: %s" % (wl["name"], wl["desc"]), "configs": S.n_configs,
                    "groups": S.n_groups, "buckets": S.n_buckets, "tiles": info["tiles"],
-                   "block": info["block"], "units_per_tile": info["units_per_tile"]},
+                   "block": info["block"], "strips_per_tile": info["strips_per_tile"]},
         "eval_kernel_ms": k1_avg, "reduce_kernel_ms": k2_avg, "space_build_ms": build_ms,
         "extract_best_ms": extract_ms, "feasible_groups": feasible,
         "device": {"name": props.name, "cus": props.multi_processor_count,

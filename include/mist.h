@@ -56,7 +56,7 @@ typedef int32_t mist_status;
 #define MIST_L_BALANCED 1 /* stage layer counts floor(L/PP) and ceil(L/PP) */
 
 #define MIST_MAX_BUCKETS 64
-#define MIST_MAX_RATIOS 32
+#define MIST_MAX_RATIOS 16
 #define MIST_MAX_MB 16
 #define MIST_NONE UINT64_MAX /* id of an empty bucket or of a group with no feasible config */
 
@@ -196,10 +196,11 @@ mist_status mist_eval_ids(mist_space* S, const uint64_t* ids, int64_t n, double*
 mist_status mist_set_timing(mist_space* S, int32_t on);
 mist_status mist_read_timing(mist_space* S, double* eval_ms, double* reduce_ms, int64_t* n_evals);
 
-/* Launch geometry of the evaluation kernel: tiles (blocks), threads per block, units
- * (pair, recomputed-layers slabs) per tile. */
+/* Launch geometry of the evaluation kernel: tiles (blocks), threads per block, strips per
+ * tile (a strip is the R^2 configurations sharing pair, recomputed layers, ZeRO level,
+ * weight and gradient ratios). */
 mist_status mist_launch_info(const mist_space* S, int64_t* n_tiles, int32_t* block,
-                             int32_t* units_per_tile);
+                             int32_t* strips_per_tile);
 
 /* Frees every buffer of the space (through its allocator).  NULL is accepted. */
 mist_status mist_space_destroy(mist_space* S);

@@ -32,6 +32,7 @@ mist_status fail_hip(hipError_t e, const char* what) {
 
 constexpr int64_t kExact = (int64_t)1 << 53;  // integers below this convert to double exactly
 constexpr int64_t kTargetTiles = 8192;        // evaluation blocks to aim for
+constexpr int64_t kStripAlign = kBlock;       // strips per tile: a multiple of the block
 
 int popcount4(int v) { return (v & 1) + ((v >> 1) & 1) + ((v >> 2) & 1) + ((v >> 3) & 1); }
 
@@ -52,7 +53,7 @@ struct mist_space {
   std::vector<DevHw> hws;
   DevModel dm;
   uint64_t n_configs = 0;
-  int32_t units_per_tile = 0;
+  int32_t strips_per_tile = 0;
   // memory
   mist_allocator alloc{};
   bool custom_alloc = false;
@@ -270,23 +271,29 @@ std::string enumerate(mist_space* S) {
   if (S->groups.empty()) return "the space has no configuration";
   if (S->groups.size() > (size_t)INT32_MAX) return "too many groups";
 
-  // Tiles: units of one group, at most units_per_tile each (a multiple of the waves).
-  uint64_t total_units = 0;
-  for (const DevGroup& g : S->groups) total_units += (uint64_t)g.n_pairs * (uint64_t)(g.l + 1);
-  uint64_t upt = (total_units + kTargetTiles - 1) / kTargetTiles;
-  upt = (upt + kWaves - 1) / kWaves * kWaves;
-  if (upt < (uint64_t)kWaves) upt = kWaves;
-  S->units_per_tile = (int32_t)upt;
+  // Tiles: contiguous strips of one group, at most strips_per_tile each.
+  const uint64_t per_unit_strips = 4ull * (uint64_t)(R * R);
+  uint64_t total_strips = 0;
+  for (const DevGroup& g : S->groups) {
+    const uint64_t st = (uint64_t)g.n_pairs * (uint64_t)(g.l + 1) * per_unit_strips;
+    if (st > (uint64_t)INT32_MAX) return "group too large";
+    total_strips += st;
+  }
+  uint64_t spt = (total_strips + kTargetTiles - 1) / kTargetTiles;
+  spt = (spt + kStripAlign - 1) / kStripAlign * kStripAlign;
+  if (spt < (uint64_t)kStripAlign) spt = kStripAlign;
+  if (spt > (uint64_t)INT32_MAX / 2) spt = (uint64_t)INT32_MAX / 2 / kStripAlign * kStripAlign;
+  S->strips_per_tile = (int32_t)spt;
   S->tiles.clear();
   for (size_t gi = 0; gi < S->groups.size(); ++gi) {
     DevGroup& g = S->groups[gi];
-    const int64_t units = (int64_t)g.n_pairs * (g.l + 1);
+    const int64_t strips = (int64_t)g.n_pairs * (g.l + 1) * (int64_t)per_unit_strips;
     g.tile_begin = (int32_t)S->tiles.size();
-    for (int64_t u = 0; u < units; u += (int64_t)upt) {
+    for (int64_t u = 0; u < strips; u += (int64_t)spt) {
       DevTile t{};
       t.group = (int32_t)gi;
-      t.unit_begin = (int32_t)u;
-      t.unit_end = (int32_t)std::min<int64_t>(units, u + (int64_t)upt);
+      t.strip_begin = (int32_t)u;
+      t.strip_end = (int32_t)std::min<int64_t>(strips, u + (int64_t)spt);
       S->tiles.push_back(t);
     }
     g.n_tiles = (int32_t)S->tiles.size() - g.tile_begin;
@@ -308,15 +315,17 @@ std::string enumerate(mist_space* S) {
       const double bs = (double)((int64_t)S->mb[j] * m.seq);
       d.ieta[j] = (bs + h.n_half) / (h.eta_max * bs);
     }
+    const double inf = std::numeric_limits<double>::infinity();
     for (int j = 0; j < MIST_MAX_BUCKETS; ++j)
-      d.edge[j] = j < S->NB ? (h.mem_bytes * (double)(j + 1)) / (double)S->NB
-                            : std::numeric_limits<double>::infinity();
+      d.edge[j] = j < S->NB ? (h.mem_bytes * (double)(j + 1)) / (double)S->NB : inf;
     d.edge[S->NB - 1] = h.mem_bytes;
+    for (int j = 0; j < MIST_MAX_BUCKETS; ++j) d.edge_lo[j] = j == 0 ? -inf : d.edge[j - 1];
     for (int mask = 0; mask < 16; ++mask)
       for (int j = 0; j < 4; ++j) {
+        const bool update = popcount4(mask) >= 2;
         const bool member = (mask >> j) & 1;
-        d.itab[mask][j] = member ? h.phi[mask][j] : std::numeric_limits<double>::infinity();
-        d.itab[mask][4 + j] = member ? 1.0 / h.phi[mask][j] : 1.0;
+        d.itab[mask][j] = !update ? 1.0 : (member ? h.phi[mask][j] : inf);
+        d.itab[mask][4 + j] = (update && member) ? 1.0 / h.phi[mask][j] : 1.0;
       }
   }
   const int64_t hd = m.hidden;
@@ -353,7 +362,6 @@ mist::EvalArgs eval_args(const mist_space* S) {
   a.ratio = S->d_ratio;
   a.R = S->R;
   a.NB = S->NB;
-  a.F = 4 * S->R * S->R * S->R;
   a.n_tiles = (int32_t)S->tiles.size();
   a.n_groups = (int64_t)S->groups.size();
   a.n_configs = S->n_configs;
@@ -701,11 +709,11 @@ mist_status mist_read_timing(mist_space* S, double* eval_ms, double* reduce_ms, 
   return MIST_OK;
 }
 
-mist_status mist_launch_info(const mist_space* S, int64_t* n_tiles, int32_t* block, int32_t* units_per_tile) {
+mist_status mist_launch_info(const mist_space* S, int64_t* n_tiles, int32_t* block, int32_t* strips_per_tile) {
   if (!S) return fail(MIST_E_INVALID, "space is null");
   if (n_tiles) *n_tiles = (int64_t)S->tiles.size();
   if (block) *block = kBlock;
-  if (units_per_tile) *units_per_tile = S->units_per_tile;
+  if (strips_per_tile) *strips_per_tile = S->strips_per_tile;
   return MIST_OK;
 }
 

@@ -30,12 +30,14 @@ struct DevPair {
   double inv_dp;          // 1 / DP, host division
 };
 
-// A block's work: units [unit_begin, unit_end) of one group, where a unit is one
-// (pair, recomputed-layers) slab of 4 * R^4 configurations.
+// A block's work: strips [strip_begin, strip_end) of one group.  A strip is one
+// (pair, recomputed layers, ZeRO level, weight ratio, gradient ratio) combination and
+// holds the R^2 configurations of its (optimizer ratio, activation ratio) digits; strip s
+// of a group covers local ids [s * R^2, (s + 1) * R^2).
 struct DevTile {
   int32_t group;
-  int32_t unit_begin;
-  int32_t unit_end;
+  int32_t strip_begin;
+  int32_t strip_end;
   int32_t pad;
 };
 
@@ -45,10 +47,12 @@ struct DevHw {
   double M;                  // memory budget
   double kNB;                // NB / M (bucket estimate, corrected against the edges)
   double ieta[MIST_MAX_MB];  // 1 / eta(b) per microbatch index
-  double edge[MIST_MAX_BUCKETS];
-  // Row per co-running pattern (bit j = stream j): phi of members then psi = 1/phi of
-  // members; absent streams have phi = +inf (their zero time scales to NaN, which the
-  // minimum skips) and psi = 1.
+  double edge[MIST_MAX_BUCKETS];     // E_j; +inf past NB
+  double edge_lo[MIST_MAX_BUCKETS];  // E_{j-1}; -inf for j = 0
+  // Row per co-running pattern (bit j = stream j runs): phi[4] then psi[4].  Patterns of
+  // two or more streams: members carry phi and psi = 1/phi, other streams phi = +inf and
+  // psi = 1 (their 0 or NaN time scales to NaN, which min/max skip).  Patterns of at most
+  // one stream: phi = psi = 1 everywhere (no update).
   double itab[16][kTabStride];
 };
 
@@ -64,7 +68,7 @@ struct EvalArgs {
   const DevTile* tiles;
   const DevHw* hws;
   const double* ratio;   // r[0..R), then om[0..R) = 1 - r
-  int32_t R, NB, F;      // F = 4 * R^3 lane slots per unit (z, wo, go, oo)
+  int32_t R, NB;
   int32_t n_tiles;
   int64_t n_groups;
   uint64_t n_configs;

@@ -129,117 +129,138 @@ __device__ __forceinline__ ZeroK zero_level(const PairK& P, int z) {
   return Z;
 }
 
-// Everything of one configuration that does not depend on the activation offload ratio.
-struct OuterK {
+// Weight and gradient offload levels (fixed within a strip).
+struct WoGoK {
+  double Swg;          // resident weight + gradient bytes
+  double Wbuf, Gbuf;   // double-buffered fetched weights / gradient unit
+  double HW;           // weight bytes fetched per microbatch (forward and backward)
+  double DW;           // updated weight bytes written back after the step
+  double DG;           // gradient bytes offloaded per microbatch
+  double Og;           // gradient part of the optimizer-step unit
+};
+
+__device__ __forceinline__ WoGoK wogo_levels(const PairK& P, const ZeroK& Z, double rw, double qw,
+                                             double rg, double qg) {
+  WoGoK W;
+  const double Sww = qw * Z.Sw;
+  W.Wbuf = P.Wb2 * (1.0 - qw * Z.sw);
+  W.HW = rw * Z.HWz;
+  W.DW = rw * Z.Sw;
+  W.Swg = __builtin_fma(qg, Z.Sg, Sww);
+  W.Gbuf = P.Wb2 * (1.0 - qg * Z.sg);
+  W.DG = rg * Z.Sg;
+  W.Og = rg * Z.Obg;
+  return W;
+}
+
+// Optimizer-state offload level: everything of a configuration except its activation
+// ratio's terms.
+struct OoK {
   double Bmax;         // max(forward, backward) peak without the activation terms
-  double HW, DG;       // bytes: weights in, gradients out per microbatch
   double H2Dx, D2Hx;   // seconds: first-microbatch extras
 };
 
-__device__ __forceinline__ OuterK offload_levels(const PairK& P, const CkptK& K, const ZeroK& Z,
-                                                 double rw, double qw, double rg, double qg,
-                                                 double ro, double qo, double iP) {
-  // weight offload
-  const double Sww = qw * Z.Sw;
-  const double Wbuf = P.Wb2 * (1.0 - qw * Z.sw);
-  const double HW = rw * Z.HWz;
-  const double DW = rw * Z.Sw;
-  // gradient offload
-  const double Swg = __builtin_fma(qg, Z.Sg, Sww);
-  const double Gbuf = P.Wb2 * (1.0 - qg * Z.sg);
-  const double DG = rg * Z.Sg;
-  const double Og = rg * Z.Obg;
-  // optimizer-state offload
-  const double S = __builtin_fma(qo, Z.So, Swg);
-  const double Obuf = __builtin_fma(ro, Z.Obo, Og);
-  const double HX = __builtin_fma(ro, Z.So, DG);
-  const double DX = __builtin_fma(ro, Z.So, DW);
-  const double base = S + Wbuf;
+__device__ __forceinline__ OoK oo_level(const PairK& P, const CkptK& K, const ZeroK& Z,
+                                        const WoGoK& W, double ro, double qo, double iP) {
+  const double S = __builtin_fma(qo, Z.So, W.Swg);
+  const double Obuf = __builtin_fma(ro, Z.Obo, W.Og);
+  const double HX = __builtin_fma(ro, Z.So, W.DG);
+  const double DX = __builtin_fma(ro, Z.So, W.DW);
+  const double base = S + W.Wbuf;
   const double BF = (base + Obuf) + P.Xd;
-  const double BB = ((base + Gbuf) + K.Rc) + P.Xd;
-  OuterK O;
+  const double BB = ((base + W.Gbuf) + K.Rc) + P.Xd;
+  OoK O;
   // max(BF + x, BB + x) == max(BF, BB) + x: rounding to nearest is monotone.
   O.Bmax = __builtin_fmax(BF, BB);
-  O.HW = HW;
-  O.DG = DG;
   O.H2Dx = HX * iP;
   O.D2Hx = DX * iP;
   return O;
 }
 
-// Algorithm 1.  Repeatedly, while at least two streams still run, the streams of the
-// current co-running pattern are scaled by that pattern's slowdown factors, the smallest
-// scaled time overlaps all of them, and the others keep their remaining standalone time;
-// the leftover stream's time is added at the end.  Visiting n = 4..2 and updating when the
-// pattern has exactly n streams is the same as updating while the pattern has >= 2 streams,
-// since every update stops at least one stream.  Absent streams carry factor +inf: their
-// zero time scales to NaN, which the minimum skips and the final max(., 0) turns back to 0.
-__device__ __forceinline__ double interference(double x0, double x1, double x2, double x3,
-                                               const double* __restrict__ tab) {
-  double T = 0.0;
-#pragma unroll
-  for (int it = 0; it < 3; ++it) {
-    const int pat = (x0 != 0.0 ? 1 : 0) | (x1 != 0.0 ? 2 : 0) | (x2 != 0.0 ? 4 : 0) |
-                    (x3 != 0.0 ? 8 : 0);
-    if (__popc(pat) < 2) break;
-    const double* e = tab + pat * kTabStride;
-    const double s0 = x0 * e[0], s1 = x1 * e[1], s2 = x2 * e[2], s3 = x3 * e[3];
-    const double ov = __builtin_fmin(__builtin_fmin(s0, s1), __builtin_fmin(s2, s3));
-    x0 = __builtin_fmax((s0 - ov) * e[4], 0.0);
-    x1 = __builtin_fmax((s1 - ov) * e[5], 0.0);
-    x2 = __builtin_fmax((s2 - ov) * e[6], 0.0);
-    x3 = __builtin_fmax((s3 - ov) * e[7], 0.0);
-    T = T + ov;
-  }
-  T = T + x0;
-  T = T + x1;
-  T = T + x2;
-  T = T + x3;
-  return T;
-}
-
-struct Result {
-  double t, d, mem, obj;
+// ---------------------------------------------------------------------------------------
+// Algorithm 1.
+//
+// Visiting n = 4..2 and updating when the non-zero pattern has exactly n streams is the
+// same as updating while the pattern has at least two streams (each update stops at least
+// one stream), so three fixed rounds suffice.  A round reads the row of the current
+// pattern: rows of two or more streams scale members by phi, overlap the smallest scaled
+// time, and leave members (scaled - overlap) * psi; non-members (time 0, or NaN from an
+// earlier round) carry phi = +inf and become NaN, which min and max skip and "> 0"
+// rejects.  Rows of at most one stream have phi = psi = 1; such a round always meets an
+// exact zero (an unused stream, or the stream that finished last) so its overlap is 0 and
+// nothing changes.  At the end at most one stream is positive and the others are 0 or NaN,
+// so the oracle's final sum equals the running total plus the largest remaining time.
+// ---------------------------------------------------------------------------------------
+struct Streams {
+  double x0, x1, x2, x3;
 };
 
-__device__ __forceinline__ Result config_level(const CkptK& K, const ZeroK& Z, const OuterK& O,
-                                               double ra, double qa, double A2, double iP,
-                                               double Gd, const double* tab) {
-  Result r;
-  const double SO = __builtin_fma(ra, A2, qa * K.KA);  // stash + double-buffered offload
-  r.mem = O.Bmax + SO;
-  const double H2Ds = __builtin_fma(ra, K.A, O.HW) * iP;
-  const double D2Hs = __builtin_fma(ra, K.A, O.DG) * iP;
-  const double H2Df = H2Ds + O.H2Dx;
-  const double D2Hf = D2Hs + O.D2Hx;
-  r.t = interference(K.C, Z.G2Gs, H2Ds, D2Hs, tab);
-  const double T1 = interference(K.C, Z.G2Gf, H2Df, D2Hf, tab);
-  r.d = T1 - r.t;
-  r.obj = __builtin_fma(Gd, r.t, r.d);
-  return r;
+__device__ __forceinline__ double round_row(Streams& x, double f0, double f1, double f2, double f3,
+                                            double p0, double p1, double p2, double p3) {
+  const double s0 = x.x0 * f0, s1 = x.x1 * f1, s2 = x.x2 * f2, s3 = x.x3 * f3;
+  const double ov = __builtin_fmin(__builtin_fmin(s0, s1), __builtin_fmin(s2, s3));
+  x.x0 = (s0 - ov) * p0;
+  x.x1 = (s1 - ov) * p1;
+  x.x2 = (s2 - ov) * p2;
+  x.x3 = (s3 - ov) * p3;
+  return ov;
 }
 
-// Bucket j = min{j : mem <= edge[j]} for a feasible mem (mem <= edge[NB-1]).  The estimate
-// floor(mem * NB / M) is within one of j; the loops settle it against the edges.
-__device__ __forceinline__ int bucket_of(double mem, double kNB, const double* edge, int NB) {
-  int j = (int)(mem * kNB);
-  j = j < NB - 1 ? j : NB - 1;
-  while (j < NB - 1 && mem > edge[j]) ++j;
-  while (j > 0 && mem <= edge[j - 1]) --j;
-  return j;
+__device__ __forceinline__ double round_lookup(Streams& x, const double* __restrict__ tab) {
+  const int pat = (x.x0 > 0.0 ? 1 : 0) | (x.x1 > 0.0 ? 2 : 0) | (x.x2 > 0.0 ? 4 : 0) |
+                  (x.x3 > 0.0 ? 8 : 0);
+  const double* e = tab + pat * kTabStride;
+  return round_row(x, e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]);
+}
+
+__device__ __forceinline__ double remaining(const Streams& x) {
+  return __builtin_fmax(__builtin_fmax(x.x0, x.x1), __builtin_fmax(x.x2, x.x3));
+}
+
+// Three rounds with per-lane rows.
+__device__ __forceinline__ double interference(double c, double g, double h, double d,
+                                               const double* __restrict__ tab) {
+  Streams x{c, g, h, d};
+  double T = round_lookup(x, tab);
+  T = T + round_lookup(x, tab);
+  T = T + round_lookup(x, tab);
+  return T + remaining(x);
+}
+
+// First round with a known pattern whose row is in registers, then two looked-up rounds.
+struct Row {
+  double f0, f1, f2, f3, p0, p1, p2, p3;
+};
+
+__device__ __forceinline__ double interference_row(const Row& r, double c, double g, double h,
+                                                   double d, const double* __restrict__ tab) {
+  Streams x{c, g, h, d};
+  double T = round_row(x, r.f0, r.f1, r.f2, r.f3, r.p0, r.p1, r.p2, r.p3);
+  T = T + round_lookup(x, tab);
+  T = T + round_lookup(x, tab);
+  return T + remaining(x);
 }
 
 // ---------------------------------------------------------------------------------------
-// K1: one block per tile (units of one group).  Wave w takes units w, w+4, ...; a unit is
-// one (pair, c) slab; its lanes take the (z, wo, go, oo) slots; each lane walks the R
-// activation ratios.  Every wave keeps a private LDS table of the 64 bucket minima; the
-// block merges them into the tile's partials.
+// K1.  One block per tile (a range of strips of one group); each thread walks strips with
+// the block's stride.  A strip fixes (pair, c, z, wo, go) and holds the R x R
+// (optimizer ratio, activation ratio) configurations:
+//   - the stable time t does not depend on the optimizer ratio, so it is computed once per
+//     activation ratio and reused across the optimizer ratios;
+//   - the first microbatch's streams start in the same pattern for every configuration of
+//     the strip (compute, GPU-GPU iff that stream carries traffic, and both host streams
+//     iff any offload ratio is non-zero), except the one configuration whose four ratios
+//     are all zero, which takes the looked-up path.
+// Every wave keeps a private LDS table of the 64 bucket minima; candidates (rare) are
+// applied one lane at a time; the block merges the tables into the tile's partials.
 // ---------------------------------------------------------------------------------------
+template <int R>
 __global__ __launch_bounds__(kBlock) void k_eval(EvalArgs a) {
+  constexpr int R2 = R * R;
+  constexpr int SU = 4 * R2;  // strips per (pair, c) unit
   __shared__ double s_tab[16 * kTabStride];
   __shared__ double s_edge[MIST_MAX_BUCKETS];
-  __shared__ double s_r[MIST_MAX_RATIOS];
-  __shared__ double s_om[MIST_MAX_RATIOS];
+  __shared__ double s_edge_lo[MIST_MAX_BUCKETS];
   __shared__ double w_obj[kWaves][64];
   __shared__ uint64_t w_id[kWaves][64];
 
@@ -249,63 +270,96 @@ __global__ __launch_bounds__(kBlock) void k_eval(EvalArgs a) {
   const DevTile tile = a.tiles[blockIdx.x];
   const DevGroup g = a.groups[tile.group];
   const DevHw& hw = a.hws[g.hw];
-  const int R = a.R, NB = a.NB, F = a.F;
+  const int NB = a.NB;
+  const double* __restrict__ rr = a.ratio;      // uniform: scalar loads
+  const double* __restrict__ om = a.ratio + R;
 
   for (int i = tid; i < 16 * kTabStride; i += kBlock) s_tab[i] = (&hw.itab[0][0])[i];
-  if (tid < MIST_MAX_BUCKETS) s_edge[tid] = hw.edge[tid];
-  if (tid < R) {
-    s_r[tid] = a.ratio[tid];
-    s_om[tid] = a.ratio[R + tid];
+  if (tid < MIST_MAX_BUCKETS) {
+    s_edge[tid] = hw.edge[tid];
+    s_edge_lo[tid] = hw.edge_lo[tid];
   }
   w_obj[wave][lane] = __builtin_huge_val();
   w_id[wave][lane] = kNone;
   __syncthreads();
 
   const double iP = hw.iP, M = hw.M, kNB = hw.kNB;
-  const int64_t l = g.l;
+  const double top = (double)(NB - 1);
+  const int l = g.l;
   const int64_t ke = g.k < g.G ? g.k : g.G;
   const double Gd = (double)g.G;
+  const bool r0_zero = rr[0] == 0.0;
 
-  for (int u = tile.unit_begin + wave; u < tile.unit_end; u += kWaves) {
-    const int p = u / (g.l + 1);
-    const int c = u - p * (g.l + 1);
-    const DevPair pr = a.pairs[g.pair_begin + p];
-    const PairK P = pair_level(a.m, g.PP, g.k, l, pr, hw);
+  int cached_p = -1;
+  PairK P{};
+  for (int s = tile.strip_begin + tid; s < tile.strip_end; s += kBlock) {
+    const int unit = s / SU;
+    const int rem = s - unit * SU;
+    const int z = rem / R2;
+    const int rem2 = rem - z * R2;
+    const int iw = rem2 / R;
+    const int ig = rem2 - iw * R;
+    const int p = unit / (l + 1);
+    const int c = unit - p * (l + 1);
+    if (p != cached_p) {
+      P = pair_level(a.m, g.PP, g.k, l, a.pairs[g.pair_begin + p], hw);
+      cached_p = p;
+    }
     const CkptK K = ckpt_level(P, l, c, ke);
-    const uint64_t unit_id = g.base + (uint64_t)u * (uint64_t)F * (uint64_t)R;
+    const ZeroK Z = zero_level(P, z);
+    const double rw = rr[iw], rg = rr[ig];
+    const WoGoK W = wogo_levels(P, Z, rw, om[iw], rg, om[ig]);
 
-    for (int f = lane; f < F; f += 64) {
-      int v = f;
-      const int io = v % R;
-      v /= R;
-      const int ig = v % R;
-      v /= R;
-      const int iw = v % R;
-      const int z = v / R;
-      const ZeroK Z = zero_level(P, z);
-      const OuterK O = offload_levels(P, K, Z, s_r[iw], s_om[iw], s_r[ig], s_om[ig], s_r[io],
-                                      s_om[io], iP);
-      const uint64_t id0 = unit_id + (uint64_t)f * (uint64_t)R;
+    double tt[R];
+#pragma unroll
+    for (int ia = 0; ia < R; ++ia) {
+      const double H2Ds = __builtin_fma(rr[ia], K.A, W.HW) * iP;
+      const double D2Hs = __builtin_fma(rr[ia], K.A, W.DG) * iP;
+      tt[ia] = interference(K.C, Z.G2Gs, H2Ds, D2Hs, s_tab);
+    }
+    const double* e1 = s_tab + (Z.G2Gf > 0.0 ? 15 : 13) * kTabStride;
+    const Row row{e1[0], e1[1], e1[2], e1[3], e1[4], e1[5], e1[6], e1[7]};
+    const bool zero_strip = r0_zero && rw == 0.0 && rg == 0.0;
+    const uint64_t id_strip = g.base + (uint64_t)s * (uint64_t)R2;
 
+    for (int io = 0; io < R; ++io) {
+      const OoK O = oo_level(P, K, Z, W, rr[io], om[io], iP);
+      const bool zero_oo = zero_strip && io == 0;
+      const uint64_t id_oo = id_strip + (uint64_t)(io * R);
+#pragma unroll
       for (int ia = 0; ia < R; ++ia) {
-        const Result r = config_level(K, Z, O, s_r[ia], s_om[ia], P.A2, iP, Gd, s_tab);
-        const uint64_t id = id0 + (uint64_t)ia;
-        const bool feasible = r.mem <= M;
-        const int j = feasible ? bucket_of(r.mem, kNB, s_edge, NB) : 0;
-        bool cand = feasible && lex_less(r.obj, id, w_obj[wave][j], w_id[wave][j]);
+        const double ra = rr[ia];
+        const double SO = __builtin_fma(ra, P.A2, om[ia] * K.KA);  // stash + offload buffers
+        const double mem = O.Bmax + SO;
+        const double H2Df = __builtin_fma(ra, K.A, W.HW) * iP + O.H2Dx;
+        const double D2Hf = __builtin_fma(ra, K.A, W.DG) * iP + O.D2Hx;
+        double T1;
+        if (ia == 0 && zero_oo) T1 = interference(K.C, Z.G2Gf, H2Df, D2Hf, s_tab);
+        else T1 = interference_row(row, K.C, Z.G2Gf, H2Df, D2Hf, s_tab);
+        const double t = tt[ia];
+        const double d = T1 - t;
+        const double obj = __builtin_fma(Gd, t, d);
+        const uint64_t id = id_oo + (uint64_t)ia;
+
+        // Feasibility (Eq. 4) and bucket: floor(mem * NB / M) is within one of the bucket.
+        const bool feasible = mem <= M;
+        const int j0 = (int)__builtin_fmin(mem * kNB, top);
+        const int jb = j0 + (mem > s_edge[j0] ? 1 : 0) - (mem <= s_edge_lo[j0] ? 1 : 0);
+        const int j = feasible ? min(max(jb, 0), NB - 1) : 0;
+        bool cand = feasible && lex_less(obj, id, w_obj[wave][j], w_id[wave][j]);
         uint64_t ballot = __ballot(cand);
         while (ballot) {
           const int leader = __ffsll((unsigned long long)ballot) - 1;
           if (lane == leader) {
-            if (lex_less(r.obj, id, w_obj[wave][j], w_id[wave][j])) {
-              w_obj[wave][j] = r.obj;
+            if (lex_less(obj, id, w_obj[wave][j], w_id[wave][j])) {
+              w_obj[wave][j] = obj;
               w_id[wave][j] = id;
             }
             cand = false;
           }
           __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
           __builtin_amdgcn_wave_barrier();
-          if (cand) cand = lex_less(r.obj, id, w_obj[wave][j], w_id[wave][j]);
+          if (cand) cand = lex_less(obj, id, w_obj[wave][j], w_id[wave][j]);
           ballot = __ballot(cand);
         }
       }
@@ -413,11 +467,22 @@ __global__ __launch_bounds__(256) void k_eval_ids(EvalArgs a, const uint64_t* __
   const double* r = a.ratio;
   const double* om = a.ratio + a.R;
   const int64_t ke = g.k < g.G ? g.k : g.G;
+  const double* tab = &hw.itab[0][0];
   const PairK P = pair_level(a.m, g.PP, g.k, g.l, a.pairs[g.pair_begin + p], hw);
   const CkptK K = ckpt_level(P, g.l, c, ke);
   const ZeroK Z = zero_level(P, z);
-  const OuterK O = offload_levels(P, K, Z, r[iw], om[iw], r[ig], om[ig], r[io], om[io], hw.iP);
-  const Result res = config_level(K, Z, O, r[ia], om[ia], P.A2, hw.iP, (double)g.G, &hw.itab[0][0]);
+  const WoGoK W = wogo_levels(P, Z, r[iw], om[iw], r[ig], om[ig]);
+  const OoK O = oo_level(P, K, Z, W, r[io], om[io], hw.iP);
+  const double ra = r[ia];
+  const double SO = __builtin_fma(ra, P.A2, om[ia] * K.KA);
+  const double H2Ds = __builtin_fma(ra, K.A, W.HW) * hw.iP;
+  const double D2Hs = __builtin_fma(ra, K.A, W.DG) * hw.iP;
+  struct { double t, d, mem, obj; } res;
+  res.mem = O.Bmax + SO;
+  res.t = interference(K.C, Z.G2Gs, H2Ds, D2Hs, tab);
+  const double T1 = interference(K.C, Z.G2Gf, H2Ds + O.H2Dx, D2Hs + O.D2Hx, tab);
+  res.d = T1 - res.t;
+  res.obj = __builtin_fma((double)g.G, res.t, res.d);
   out[4 * i + 0] = res.t;
   out[4 * i + 1] = res.d;
   out[4 * i + 2] = res.mem;
@@ -431,9 +496,33 @@ int check_launch() {
 
 }  // namespace
 
+template <int R>
+void launch_eval_r(const EvalArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_eval<R>, dim3(a.n_tiles), dim3(kBlock), 0, st, a);
+}
+
 int launch_eval(const EvalArgs& a, void* stream) {
   if (a.n_tiles <= 0) return 0;
-  hipLaunchKernelGGL(k_eval, dim3(a.n_tiles), dim3(kBlock), 0, (hipStream_t)stream, a);
+  hipStream_t st = (hipStream_t)stream;
+  switch (a.R) {
+    case 1: launch_eval_r<1>(a, st); break;
+    case 2: launch_eval_r<2>(a, st); break;
+    case 3: launch_eval_r<3>(a, st); break;
+    case 4: launch_eval_r<4>(a, st); break;
+    case 5: launch_eval_r<5>(a, st); break;
+    case 6: launch_eval_r<6>(a, st); break;
+    case 7: launch_eval_r<7>(a, st); break;
+    case 8: launch_eval_r<8>(a, st); break;
+    case 9: launch_eval_r<9>(a, st); break;
+    case 10: launch_eval_r<10>(a, st); break;
+    case 11: launch_eval_r<11>(a, st); break;
+    case 12: launch_eval_r<12>(a, st); break;
+    case 13: launch_eval_r<13>(a, st); break;
+    case 14: launch_eval_r<14>(a, st); break;
+    case 15: launch_eval_r<15>(a, st); break;
+    case 16: launch_eval_r<16>(a, st); break;
+    default: return (int)hipErrorInvalidValue;
+  }
   return check_launch();
 }
 

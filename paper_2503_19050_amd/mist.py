@@ -223,7 +223,7 @@ class Space:
         b = ctypes.c_int32()
         u = ctypes.c_int32()
         _check(self.L, self.L.mist_launch_info(self.h, ctypes.byref(t), ctypes.byref(b), ctypes.byref(u)))
-        return {"tiles": t.value, "block": b.value, "units_per_tile": u.value}
+        return {"tiles": t.value, "block": b.value, "strips_per_tile": u.value}
 
     # -- results ------------------------------------------------------------------
     def best(self, g0: int = 0, n: int | None = None) -> list[dict]:

@@ -65,7 +65,7 @@ def _create(wl, **over):
     {"h__flops": 0.0}, {"h__mem_bytes": -1.0}, {"h__pcie_bw": float("nan")}, {"h__eta_max": 0.0},
     {"s__n_buckets": 0}, {"s__n_buckets": 65}, {"s__mb": [2, 1]}, {"s__mb": []},
     {"s__ratios": [0.0, 1.5]}, {"s__ratios": [0.5, 0.5]}, {"s__l_rule": 3}, {"s__n_devices": 0},
-    {"s__ratios": [0.0] * 33},
+    {"s__ratios": [j / 16 for j in range(17)]},
 ])
 def test_invalid_descriptors_are_rejected(over):
     rc, msg = _create(W.workload("tiny"), **over)
