@@ -51,6 +51,7 @@ struct mist_space {
   std::vector<DevPair> pairs;
   std::vector<DevTile> tiles;
   std::vector<DevHw> hws;
+  std::vector<int32_t> pk_group;  // group of each pair-constant entry
   DevModel dm;
   uint64_t n_configs = 0;
   int32_t strips_per_tile = 0;
@@ -63,6 +64,8 @@ struct mist_space {
   DevTile* d_tiles = nullptr;
   DevHw* d_hws = nullptr;
   double* d_ratio = nullptr;
+  PairK* d_pk = nullptr;
+  int32_t* d_pk_group = nullptr;
   double* d_part_obj = nullptr;
   uint64_t* d_part_id = nullptr;
   double* d_bucket_obj = nullptr;
@@ -271,6 +274,14 @@ std::string enumerate(mist_space* S) {
   if (S->groups.empty()) return "the space has no configuration";
   if (S->groups.size() > (size_t)INT32_MAX) return "too many groups";
 
+  // Pair-constant entries, group-major.
+  S->pk_group.clear();
+  for (size_t gi = 0; gi < S->groups.size(); ++gi) {
+    S->groups[gi].pk_begin = (int32_t)S->pk_group.size();
+    for (int32_t p = 0; p < S->groups[gi].n_pairs; ++p) S->pk_group.push_back((int32_t)gi);
+    if (S->pk_group.size() > (size_t)INT32_MAX) return "too many pairs";
+  }
+
   // Tiles: contiguous strips of one group, at most strips_per_tile each.
   const uint64_t per_unit_strips = 4ull * (uint64_t)(R * R);
   uint64_t total_strips = 0;
@@ -367,6 +378,9 @@ mist::EvalArgs eval_args(const mist_space* S) {
   a.n_configs = S->n_configs;
   a.part_obj = S->d_part_obj;
   a.part_id = S->d_part_id;
+  a.pk = S->d_pk;
+  a.pk_group = S->d_pk_group;
+  a.n_pk = (int32_t)S->pk_group.size();
   return a;
 }
 
@@ -497,6 +511,11 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
     if (!rc) rc = upload(S, &S->d_tiles, S->tiles, "tiles");
     if (!rc) rc = upload(S, &S->d_hws, S->hws, "hardware tables");
     if (!rc) rc = upload(S, &S->d_ratio, S->ratio_om, "ratios");
+    if (!rc) rc = upload(S, &S->d_pk_group, S->pk_group, "pair groups");
+    if (!rc) {
+      S->d_pk = (PairK*)dev_alloc(S, S->pk_group.size() * sizeof(PairK));
+      if (!S->d_pk) rc = fail(MIST_E_NOMEM, "device allocation failed: pair constants");
+    }
     const size_t nt = S->tiles.size(), ng = S->groups.size();
     if (!rc) {
       S->d_part_obj = (double*)dev_alloc(S, nt * 64 * sizeof(double));
@@ -527,6 +546,9 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
 mist_status mist_eval_space(mist_space* S, void* hip_stream) {
   if (!S) return fail(MIST_E_INVALID, "space is null");
   hipStream_t st = (hipStream_t)hip_stream;
+  const EvalArgs ea = eval_args(S);
+  int rc = launch_pairs(ea, st);
+  if (rc) return fail_hip((hipError_t)rc, "pair kernel launch");
   hipEvent_t* ev = nullptr;
   if (S->timing) {
     while (S->events.size() < S->events_used + 3) {
@@ -540,7 +562,7 @@ mist_status mist_eval_space(mist_space* S, void* hip_stream) {
     const hipError_t e = hipEventRecord(ev[0], st);
     if (e != hipSuccess) return fail_hip(e, "hipEventRecord");
   }
-  int rc = launch_eval(eval_args(S), st);
+  rc = launch_eval(ea, st);
   if (rc) return fail_hip((hipError_t)rc, "evaluation kernel launch");
   if (ev) {
     const hipError_t e = hipEventRecord(ev[1], st);

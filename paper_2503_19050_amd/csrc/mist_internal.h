@@ -21,7 +21,7 @@ struct DevGroup {
   int32_t n_pairs;
   int32_t tile_begin;   // first tile of the group in the tile table
   int32_t n_tiles;
-  int32_t pad;
+  int32_t pk_begin;     // first entry of the group's pairs in the pair-constant table
 };
 
 // One (b, TP) pair of a group, DP = D / (PP * TP).
@@ -61,6 +61,19 @@ struct DevModel {
   int32_t gpt, flash;
 };
 
+// Pair-level constants of one (group, pair): the cost-model quantities that depend on
+// the stage and on (b, TP, DP) only (written by the pair kernel, read per strip).
+struct PairK {
+  int64_t afull, ack;  // activation bytes of a stored / checkpointed layer
+  double Pw, Po;       // stage parameter bytes: fp16 copy, optimizer states
+  double Wb2, Ob2o;    // double-buffered per-layer units: fp16, optimizer states
+  double A2, AF, Xd;   // 2 x layer activations, layer activations, fp32 logits
+  double Fld, Fh3;     // layer forward FLOPs, 3 x LM-head forward FLOPs
+  double r, p2p, ar;   // seconds: one ZeRO AG/RS, pipeline sends, one TP all-reduce
+  double FE;           // 1 / (F * eta(b))
+  double iD;           // 1 / DP
+};
+
 struct EvalArgs {
   DevModel m;
   const DevGroup* groups;
@@ -74,6 +87,9 @@ struct EvalArgs {
   uint64_t n_configs;
   double* part_obj;      // [n_tiles][64]
   uint64_t* part_id;     // [n_tiles][64]
+  PairK* pk;             // [n_pk] pair constants, group-major
+  const int32_t* pk_group;  // [n_pk] group of each entry
+  int32_t n_pk;
 };
 
 struct ReduceArgs {
@@ -90,6 +106,7 @@ struct ReduceArgs {
 };
 
 // Kernel launchers (mist_kernels.hip).
+int launch_pairs(const EvalArgs& a, void* stream);
 int launch_eval(const EvalArgs& a, void* stream);
 int launch_reduce(const ReduceArgs& a, void* stream);
 int launch_eval_ids(const EvalArgs& a, const uint64_t* ids, int64_t n, double* out, void* stream);

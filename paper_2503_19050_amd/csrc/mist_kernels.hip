@@ -26,17 +26,6 @@ __device__ __forceinline__ bool lex_less(double o1, uint64_t i1, double o2, uint
 // fixed at that level: pair (b, TP, DP), recomputed layers c, ZeRO level z, then the
 // weight, gradient, optimizer-state and activation offload ratios.
 // ---------------------------------------------------------------------------------------
-struct PairK {
-  int64_t afull, ack;  // activation bytes of a stored / checkpointed layer
-  double Pw, Po;       // stage parameter bytes: fp16 copy, optimizer states
-  double Wb2, Ob2o;    // double-buffered per-layer units: fp16, optimizer states
-  double A2, AF, Xd;   // 2 x layer activations, layer activations, fp32 logits
-  double Fld, Fh3;     // layer forward FLOPs, 3 x LM-head forward FLOPs
-  double r, p2p, ar;   // seconds: one ZeRO AG/RS, pipeline sends, one TP all-reduce
-  double FE;           // 1 / (F * eta(b))
-  double iD;           // 1 / DP
-};
-
 __device__ __forceinline__ PairK pair_level(const DevModel& m, int64_t PP, int64_t k, int64_t l,
                                             const DevPair& pr, const DevHw& hw) {
   const int64_t h = m.h, s = m.s, V = m.V, f = m.f, bw = m.bw, bo = m.bo;
@@ -227,15 +216,29 @@ __device__ __forceinline__ double interference(double c, double g, double h, dou
   return T + remaining(x);
 }
 
-// First round with a known pattern whose row is in registers, then two looked-up rounds.
-struct Row {
-  double f0, f1, f2, f3, p0, p1, p2, p3;
+// First round with a pattern known in advance (row at e), then two looked-up rounds.
+__device__ __forceinline__ double interference_first(const double* __restrict__ e, double c, double g,
+                                                     double h, double d, const double* __restrict__ tab) {
+  Streams x{c, g, h, d};
+  double T = round_row(x, e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]);
+  T = T + round_lookup(x, tab);
+  T = T + round_lookup(x, tab);
+  return T + remaining(x);
+}
+
+// The first-microbatch streams of a strip: compute and GPU-GPU times (and their scaled
+// values under the strip's first-round row) are fixed, the host streams vary.
+struct FirstRow {
+  double s0, s1, m01;   // C * phi0, G2G * phi1, min of the two
+  double f2, f3, p0, p1, p2, p3;
 };
 
-__device__ __forceinline__ double interference_row(const Row& r, double c, double g, double h,
-                                                   double d, const double* __restrict__ tab) {
-  Streams x{c, g, h, d};
-  double T = round_row(x, r.f0, r.f1, r.f2, r.f3, r.p0, r.p1, r.p2, r.p3);
+__device__ __forceinline__ double interference_strip(const FirstRow& r, double h, double d,
+                                                     const double* __restrict__ tab) {
+  const double s2 = h * r.f2, s3 = d * r.f3;
+  const double ov = __builtin_fmin(r.m01, __builtin_fmin(s2, s3));
+  Streams x{(r.s0 - ov) * r.p0, (r.s1 - ov) * r.p1, (s2 - ov) * r.p2, (s3 - ov) * r.p3};
+  double T = ov;
   T = T + round_lookup(x, tab);
   T = T + round_lookup(x, tab);
   return T + remaining(x);
@@ -254,15 +257,25 @@ __device__ __forceinline__ double interference_row(const Row& r, double c, doubl
 // Every wave keeps a private LDS table of the 64 bucket minima; candidates (rare) are
 // applied one lane at a time; the block merges the tables into the tile's partials.
 // ---------------------------------------------------------------------------------------
+// K0: pair-level constants of every (group, pair).
+__global__ __launch_bounds__(256) void k_pairs(EvalArgs a) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.n_pk) return;
+  const DevGroup g = a.groups[a.pk_group[i]];
+  const int p = i - g.pk_begin;
+  a.pk[i] = pair_level(a.m, g.PP, g.k, g.l, a.pairs[g.pair_begin + p], a.hws[g.hw]);
+}
+
 template <int R>
-__global__ __launch_bounds__(kBlock) void k_eval(EvalArgs a) {
+__global__ __launch_bounds__(kBlock, 4) void k_eval(EvalArgs a) {
   constexpr int R2 = R * R;
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
   __shared__ double s_tab[16 * kTabStride];
   __shared__ double s_edge[MIST_MAX_BUCKETS];
   __shared__ double s_edge_lo[MIST_MAX_BUCKETS];
-  __shared__ double w_obj[kWaves][64];
-  __shared__ uint64_t w_id[kWaves][64];
+  // Per-wave bucket table: [bucket][0] = bits of the minimum objective (a non-negative
+  // double orders like its bit pattern), [bucket][1] = lowest id reaching it.
+  __shared__ unsigned long long w_tab[kWaves][64][2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -279,9 +292,10 @@ __global__ __launch_bounds__(kBlock) void k_eval(EvalArgs a) {
     s_edge[tid] = hw.edge[tid];
     s_edge_lo[tid] = hw.edge_lo[tid];
   }
-  w_obj[wave][lane] = __builtin_huge_val();
-  w_id[wave][lane] = kNone;
+  w_tab[wave][lane][0] = (unsigned long long)__double_as_longlong(__builtin_huge_val());
+  w_tab[wave][lane][1] = kNone;
   __syncthreads();
+  unsigned long long (*tab)[2] = w_tab[wave];
 
   const double iP = hw.iP, M = hw.M, kNB = hw.kNB;
   const double top = (double)(NB - 1);
@@ -290,8 +304,7 @@ __global__ __launch_bounds__(kBlock) void k_eval(EvalArgs a) {
   const double Gd = (double)g.G;
   const bool r0_zero = rr[0] == 0.0;
 
-  int cached_p = -1;
-  PairK P{};
+#pragma unroll 1
   for (int s = tile.strip_begin + tid; s < tile.strip_end; s += kBlock) {
     const int unit = s / SU;
     const int rem = s - unit * SU;
@@ -301,27 +314,41 @@ __global__ __launch_bounds__(kBlock) void k_eval(EvalArgs a) {
     const int ig = rem2 - iw * R;
     const int p = unit / (l + 1);
     const int c = unit - p * (l + 1);
-    if (p != cached_p) {
-      P = pair_level(a.m, g.PP, g.k, l, a.pairs[g.pair_begin + p], hw);
-      cached_p = p;
-    }
+    const PairK& P = a.pk[g.pk_begin + p];
     const CkptK K = ckpt_level(P, l, c, ke);
     const ZeroK Z = zero_level(P, z);
     const double rw = rr[iw], rg = rr[ig];
     const WoGoK W = wogo_levels(P, Z, rw, om[iw], rg, om[ig]);
 
+    // Stable time per activation ratio (it does not depend on the optimizer ratio).  With
+    // a positive activation ratio both host streams run, so the first round's pattern is
+    // compute + both host streams (+ GPU-GPU when it carries traffic).
     double tt[R];
+    const double* es = s_tab + (Z.G2Gs > 0.0 ? 15 : 13) * kTabStride;
 #pragma unroll
     for (int ia = 0; ia < R; ++ia) {
       const double H2Ds = __builtin_fma(rr[ia], K.A, W.HW) * iP;
       const double D2Hs = __builtin_fma(rr[ia], K.A, W.DG) * iP;
-      tt[ia] = interference(K.C, Z.G2Gs, H2Ds, D2Hs, s_tab);
+      if (ia == 0 && r0_zero) tt[ia] = interference(K.C, Z.G2Gs, H2Ds, D2Hs, s_tab);
+      else tt[ia] = interference_first(es, K.C, Z.G2Gs, H2Ds, D2Hs, s_tab);
     }
+    // First microbatch: every configuration of the strip with a non-zero offload ratio
+    // starts with compute, both host streams and (if it carries traffic) GPU-GPU.
     const double* e1 = s_tab + (Z.G2Gf > 0.0 ? 15 : 13) * kTabStride;
-    const Row row{e1[0], e1[1], e1[2], e1[3], e1[4], e1[5], e1[6], e1[7]};
+    FirstRow fr;
+    fr.s0 = K.C * e1[0];
+    fr.s1 = Z.G2Gf * e1[1];
+    fr.m01 = __builtin_fmin(fr.s0, fr.s1);
+    fr.f2 = e1[2];
+    fr.f3 = e1[3];
+    fr.p0 = e1[4];
+    fr.p1 = e1[5];
+    fr.p2 = e1[6];
+    fr.p3 = e1[7];
     const bool zero_strip = r0_zero && rw == 0.0 && rg == 0.0;
     const uint64_t id_strip = g.base + (uint64_t)s * (uint64_t)R2;
 
+#pragma unroll 1
     for (int io = 0; io < R; ++io) {
       const OoK O = oo_level(P, K, Z, W, rr[io], om[io], iP);
       const bool zero_oo = zero_strip && io == 0;
@@ -335,7 +362,7 @@ __global__ __launch_bounds__(kBlock) void k_eval(EvalArgs a) {
         const double D2Hf = __builtin_fma(ra, K.A, W.DG) * iP + O.D2Hx;
         double T1;
         if (ia == 0 && zero_oo) T1 = interference(K.C, Z.G2Gf, H2Df, D2Hf, s_tab);
-        else T1 = interference_row(row, K.C, Z.G2Gf, H2Df, D2Hf, s_tab);
+        else T1 = interference_strip(fr, H2Df, D2Hf, s_tab);
         const double t = tt[ia];
         const double d = T1 - t;
         const double obj = __builtin_fma(Gd, t, d);
@@ -346,34 +373,42 @@ __global__ __launch_bounds__(kBlock) void k_eval(EvalArgs a) {
         const int j0 = (int)__builtin_fmin(mem * kNB, top);
         const int jb = j0 + (mem > s_edge[j0] ? 1 : 0) - (mem <= s_edge_lo[j0] ? 1 : 0);
         const int j = feasible ? min(max(jb, 0), NB - 1) : 0;
-        bool cand = feasible && lex_less(obj, id, w_obj[wave][j], w_id[wave][j]);
-        uint64_t ballot = __ballot(cand);
-        while (ballot) {
-          const int leader = __ffsll((unsigned long long)ballot) - 1;
-          if (lane == leader) {
-            if (lex_less(obj, id, w_obj[wave][j], w_id[wave][j])) {
-              w_obj[wave][j] = obj;
-              w_id[wave][j] = id;
-            }
-            cand = false;
-          }
+
+        // Lexicographic (obj, id) minimum per bucket without a serial loop: the lanes that
+        // beat their bucket's entry lower the objective bits with an LDS atomic minimum;
+        // a lane that sees its bucket's objective drop clears the id, then the lanes whose
+        // objective equals the new minimum lower the id.  A wave's LDS operations complete
+        // in program order, so each step sees the previous one.
+        const unsigned long long key = (unsigned long long)__double_as_longlong(obj);
+        const unsigned long long k_old = tab[j][0];
+        const unsigned long long i_old = tab[j][1];
+        const bool cand = feasible && (key < k_old || (key == k_old && id < i_old));
+        if (__ballot(cand)) {
+          if (cand) atomicMin(&tab[j][0], key);
           __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
           __builtin_amdgcn_wave_barrier();
-          if (cand) cand = lex_less(obj, id, w_obj[wave][j], w_id[wave][j]);
-          ballot = __ballot(cand);
+          const unsigned long long k_new = cand ? tab[j][0] : 0ull;
+          if (cand && k_new < k_old) tab[j][1] = kNone;
+          __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+          __builtin_amdgcn_wave_barrier();
+          if (cand && key == k_new) atomicMin(&tab[j][1], (unsigned long long)id);
+          __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+          __builtin_amdgcn_wave_barrier();
         }
       }
     }
   }
   __syncthreads();
   if (tid < 64) {
-    double bo = w_obj[0][tid];
-    uint64_t bi = w_id[0][tid];
+    double bo = __longlong_as_double((long long)w_tab[0][tid][0]);
+    uint64_t bi = w_tab[0][tid][1];
 #pragma unroll
     for (int w = 1; w < kWaves; ++w) {
-      if (lex_less(w_obj[w][tid], w_id[w][tid], bo, bi)) {
-        bo = w_obj[w][tid];
-        bi = w_id[w][tid];
+      const double o = __longlong_as_double((long long)w_tab[w][tid][0]);
+      const uint64_t i = w_tab[w][tid][1];
+      if (lex_less(o, i, bo, bi)) {
+        bo = o;
+        bi = i;
       }
     }
     a.part_obj[(size_t)blockIdx.x * 64 + tid] = bo;
@@ -523,6 +558,12 @@ int launch_eval(const EvalArgs& a, void* stream) {
     case 16: launch_eval_r<16>(a, st); break;
     default: return (int)hipErrorInvalidValue;
   }
+  return check_launch();
+}
+
+int launch_pairs(const EvalArgs& a, void* stream) {
+  if (a.n_pk <= 0) return 0;
+  hipLaunchKernelGGL(k_pairs, dim3((unsigned)((a.n_pk + 255) / 256)), dim3(256), 0, (hipStream_t)stream, a);
   return check_launch();
 }
 
