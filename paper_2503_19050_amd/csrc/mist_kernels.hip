@@ -142,6 +142,12 @@ __device__ __forceinline__ WoGoK wogo_levels(const PairK& P, const ZeroK& Z, dou
   return W;
 }
 
+// Strip constants that the optimizer-state offload level reads, kept in a per-lane LDS
+// record (registers are the scarce resource of the evaluation kernel).
+struct OoIn {
+  double So, Swg, Obo, Og, DG, DW, Wbuf, Gbuf, Rc, Xd;
+};
+
 // Optimizer-state offload level: everything of a configuration except its activation
 // ratio's terms.
 struct OoK {
@@ -149,15 +155,19 @@ struct OoK {
   double H2Dx, D2Hx;   // seconds: first-microbatch extras
 };
 
-__device__ __forceinline__ OoK oo_level(const PairK& P, const CkptK& K, const ZeroK& Z,
-                                        const WoGoK& W, double ro, double qo, double iP) {
-  const double S = __builtin_fma(qo, Z.So, W.Swg);
-  const double Obuf = __builtin_fma(ro, Z.Obo, W.Og);
-  const double HX = __builtin_fma(ro, Z.So, W.DG);
-  const double DX = __builtin_fma(ro, Z.So, W.DW);
-  const double base = S + W.Wbuf;
-  const double BF = (base + Obuf) + P.Xd;
-  const double BB = ((base + W.Gbuf) + K.Rc) + P.Xd;
+__device__ __forceinline__ OoIn oo_inputs(const PairK& P, const CkptK& K, const ZeroK& Z,
+                                          const WoGoK& W) {
+  return OoIn{Z.So, W.Swg, Z.Obo, W.Og, W.DG, W.DW, W.Wbuf, W.Gbuf, K.Rc, P.Xd};
+}
+
+__device__ __forceinline__ OoK oo_level(const OoIn& I, double ro, double qo, double iP) {
+  const double S = __builtin_fma(qo, I.So, I.Swg);
+  const double Obuf = __builtin_fma(ro, I.Obo, I.Og);
+  const double HX = __builtin_fma(ro, I.So, I.DG);
+  const double DX = __builtin_fma(ro, I.So, I.DW);
+  const double base = S + I.Wbuf;
+  const double BF = (base + Obuf) + I.Xd;
+  const double BB = ((base + I.Gbuf) + I.Rc) + I.Xd;
   OoK O;
   // max(BF + x, BB + x) == max(BF, BB) + x: rounding to nearest is monotone.
   O.Bmax = __builtin_fmax(BF, BB);
@@ -195,10 +205,15 @@ __device__ __forceinline__ double round_row(Streams& x, double f0, double f1, do
   return ov;
 }
 
+// Interference rows in LDS are padded to kLdsRow doubles so that lanes reading different
+// rows spread over more banks.
+constexpr int kLdsRow = 10;
+
+template <int STRIDE>
 __device__ __forceinline__ double round_lookup(Streams& x, const double* __restrict__ tab) {
   const int pat = (x.x0 > 0.0 ? 1 : 0) | (x.x1 > 0.0 ? 2 : 0) | (x.x2 > 0.0 ? 4 : 0) |
                   (x.x3 > 0.0 ? 8 : 0);
-  const double* e = tab + pat * kTabStride;
+  const double* e = tab + pat * STRIDE;
   return round_row(x, e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]);
 }
 
@@ -206,13 +221,14 @@ __device__ __forceinline__ double remaining(const Streams& x) {
   return __builtin_fmax(__builtin_fmax(x.x0, x.x1), __builtin_fmax(x.x2, x.x3));
 }
 
-// Three rounds with per-lane rows.
+// Three rounds with per-lane rows (rows STRIDE doubles apart).
+template <int STRIDE = kLdsRow>
 __device__ __forceinline__ double interference(double c, double g, double h, double d,
                                                const double* __restrict__ tab) {
   Streams x{c, g, h, d};
-  double T = round_lookup(x, tab);
-  T = T + round_lookup(x, tab);
-  T = T + round_lookup(x, tab);
+  double T = round_lookup<STRIDE>(x, tab);
+  T = T + round_lookup<STRIDE>(x, tab);
+  T = T + round_lookup<STRIDE>(x, tab);
   return T + remaining(x);
 }
 
@@ -221,8 +237,8 @@ __device__ __forceinline__ double interference_first(const double* __restrict__ 
                                                      double h, double d, const double* __restrict__ tab) {
   Streams x{c, g, h, d};
   double T = round_row(x, e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]);
-  T = T + round_lookup(x, tab);
-  T = T + round_lookup(x, tab);
+  T = T + round_lookup<kLdsRow>(x, tab);
+  T = T + round_lookup<kLdsRow>(x, tab);
   return T + remaining(x);
 }
 
@@ -239,8 +255,8 @@ __device__ __forceinline__ double interference_strip(const FirstRow& r, double h
   const double ov = __builtin_fmin(r.m01, __builtin_fmin(s2, s3));
   Streams x{(r.s0 - ov) * r.p0, (r.s1 - ov) * r.p1, (s2 - ov) * r.p2, (s3 - ov) * r.p3};
   double T = ov;
-  T = T + round_lookup(x, tab);
-  T = T + round_lookup(x, tab);
+  T = T + round_lookup<kLdsRow>(x, tab);
+  T = T + round_lookup<kLdsRow>(x, tab);
   return T + remaining(x);
 }
 
@@ -266,16 +282,25 @@ __global__ __launch_bounds__(256) void k_pairs(EvalArgs a) {
   a.pk[i] = pair_level(a.m, g.PP, g.k, g.l, a.pairs[g.pair_begin + p], a.hws[g.hw]);
 }
 
+// Waves per SIMD the register allocation aims at: the strip keeps R stable times live, so
+// large ratio counts trade a wave of occupancy for spill-free code.
 template <int R>
-__global__ __launch_bounds__(kBlock, 4) void k_eval(EvalArgs a) {
+constexpr int eval_waves() { return R <= 6 ? 4 : 3; }
+
+template <int R>
+__global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, const double* __restrict__ ratio,
+                                                    const PairK* __restrict__ pk) {
   constexpr int R2 = R * R;
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
-  __shared__ double s_tab[16 * kTabStride];
+  __shared__ double s_tab[16 * kLdsRow];
   __shared__ double s_edge[MIST_MAX_BUCKETS];
   __shared__ double s_edge_lo[MIST_MAX_BUCKETS];
-  // Per-wave bucket table: [bucket][0] = bits of the minimum objective (a non-negative
-  // double orders like its bit pattern), [bucket][1] = lowest id reaching it.
-  __shared__ unsigned long long w_tab[kWaves][64][2];
+  // Per-wave bucket table: bits of the minimum objective (a non-negative double orders like
+  // its bit pattern) and the lowest local id (id - group base, < 2^32) reaching it.
+  __shared__ unsigned long long w_key[kWaves][64];
+  __shared__ unsigned int w_lid[kWaves][64];
+  __shared__ OoIn s_oo[kBlock];       // per-lane strip constants of the optimizer level
+  __shared__ double s_zero[kBlock][2];  // per-lane C and G2G (first microbatch) of the strip
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -284,18 +309,20 @@ __global__ __launch_bounds__(kBlock, 4) void k_eval(EvalArgs a) {
   const DevGroup g = a.groups[tile.group];
   const DevHw& hw = a.hws[g.hw];
   const int NB = a.NB;
-  const double* __restrict__ rr = a.ratio;      // uniform: scalar loads
-  const double* __restrict__ om = a.ratio + R;
+  const double* __restrict__ rr = ratio;        // read-only and uniform: scalar loads
+  const double* __restrict__ om = ratio + R;
 
-  for (int i = tid; i < 16 * kTabStride; i += kBlock) s_tab[i] = (&hw.itab[0][0])[i];
+  for (int i = tid; i < 16 * kTabStride; i += kBlock)
+    s_tab[(i / kTabStride) * kLdsRow + i % kTabStride] = (&hw.itab[0][0])[i];
   if (tid < MIST_MAX_BUCKETS) {
     s_edge[tid] = hw.edge[tid];
     s_edge_lo[tid] = hw.edge_lo[tid];
   }
-  w_tab[wave][lane][0] = (unsigned long long)__double_as_longlong(__builtin_huge_val());
-  w_tab[wave][lane][1] = kNone;
+  w_key[wave][lane] = (unsigned long long)__double_as_longlong(__builtin_huge_val());
+  w_lid[wave][lane] = 0xFFFFFFFFu;
   __syncthreads();
-  unsigned long long (*tab)[2] = w_tab[wave];
+  unsigned long long* key_tab = w_key[wave];
+  unsigned int* lid_tab = w_lid[wave];
 
   const double iP = hw.iP, M = hw.M, kNB = hw.kNB;
   const double top = (double)(NB - 1);
@@ -314,7 +341,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_eval(EvalArgs a) {
     const int ig = rem2 - iw * R;
     const int p = unit / (l + 1);
     const int c = unit - p * (l + 1);
-    const PairK& P = a.pk[g.pk_begin + p];
+    const PairK P = pk[g.pk_begin + p];
     const CkptK K = ckpt_level(P, l, c, ke);
     const ZeroK Z = zero_level(P, z);
     const double rw = rr[iw], rg = rr[ig];
@@ -324,7 +351,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_eval(EvalArgs a) {
     // a positive activation ratio both host streams run, so the first round's pattern is
     // compute + both host streams (+ GPU-GPU when it carries traffic).
     double tt[R];
-    const double* es = s_tab + (Z.G2Gs > 0.0 ? 15 : 13) * kTabStride;
+    const double* es = s_tab + (Z.G2Gs > 0.0 ? 15 : 13) * kLdsRow;
 #pragma unroll
     for (int ia = 0; ia < R; ++ia) {
       const double H2Ds = __builtin_fma(rr[ia], K.A, W.HW) * iP;
@@ -334,7 +361,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_eval(EvalArgs a) {
     }
     // First microbatch: every configuration of the strip with a non-zero offload ratio
     // starts with compute, both host streams and (if it carries traffic) GPU-GPU.
-    const double* e1 = s_tab + (Z.G2Gf > 0.0 ? 15 : 13) * kTabStride;
+    const double* e1 = s_tab + (Z.G2Gf > 0.0 ? 15 : 13) * kLdsRow;
     FirstRow fr;
     fr.s0 = K.C * e1[0];
     fr.s1 = Z.G2Gf * e1[1];
@@ -346,27 +373,31 @@ __global__ __launch_bounds__(kBlock, 4) void k_eval(EvalArgs a) {
     fr.p2 = e1[6];
     fr.p3 = e1[7];
     const bool zero_strip = r0_zero && rw == 0.0 && rg == 0.0;
-    const uint64_t id_strip = g.base + (uint64_t)s * (uint64_t)R2;
+    s_oo[tid] = oo_inputs(P, K, Z, W);
+    s_zero[tid][0] = K.C;
+    s_zero[tid][1] = Z.G2Gf;
+    const double A = K.A, KA = K.KA, A2 = P.A2, HW = W.HW, DG = W.DG;
+    const unsigned int lid_strip = (unsigned int)s * (unsigned int)R2;
 
 #pragma unroll 1
     for (int io = 0; io < R; ++io) {
-      const OoK O = oo_level(P, K, Z, W, rr[io], om[io], iP);
+      const OoK O = oo_level(s_oo[tid], rr[io], om[io], iP);
       const bool zero_oo = zero_strip && io == 0;
-      const uint64_t id_oo = id_strip + (uint64_t)(io * R);
+      const unsigned int lid_oo = lid_strip + (unsigned int)(io * R);
 #pragma unroll
       for (int ia = 0; ia < R; ++ia) {
         const double ra = rr[ia];
-        const double SO = __builtin_fma(ra, P.A2, om[ia] * K.KA);  // stash + offload buffers
+        const double SO = __builtin_fma(ra, A2, om[ia] * KA);  // stash + offload buffers
         const double mem = O.Bmax + SO;
-        const double H2Df = __builtin_fma(ra, K.A, W.HW) * iP + O.H2Dx;
-        const double D2Hf = __builtin_fma(ra, K.A, W.DG) * iP + O.D2Hx;
+        const double H2Df = __builtin_fma(ra, A, HW) * iP + O.H2Dx;
+        const double D2Hf = __builtin_fma(ra, A, DG) * iP + O.D2Hx;
         double T1;
-        if (ia == 0 && zero_oo) T1 = interference(K.C, Z.G2Gf, H2Df, D2Hf, s_tab);
+        if (ia == 0 && zero_oo) T1 = interference(s_zero[tid][0], s_zero[tid][1], H2Df, D2Hf, s_tab);
         else T1 = interference_strip(fr, H2Df, D2Hf, s_tab);
         const double t = tt[ia];
         const double d = T1 - t;
         const double obj = __builtin_fma(Gd, t, d);
-        const uint64_t id = id_oo + (uint64_t)ia;
+        const unsigned int lid = lid_oo + (unsigned int)ia;
 
         // Feasibility (Eq. 4) and bucket: floor(mem * NB / M) is within one of the bucket.
         const bool feasible = mem <= M;
@@ -377,42 +408,39 @@ __global__ __launch_bounds__(kBlock, 4) void k_eval(EvalArgs a) {
         // Lexicographic (obj, id) minimum per bucket without a serial loop: the lanes that
         // beat their bucket's entry lower the objective bits with an LDS atomic minimum;
         // a lane that sees its bucket's objective drop clears the id, then the lanes whose
-        // objective equals the new minimum lower the id.  A wave's LDS operations complete
-        // in program order, so each step sees the previous one.
+        // objective equals the new minimum lower the id.  The LDS operations of a wave
+        // execute in program order and each step addresses the same words as the one
+        // before, so each step sees the previous one's result.
         const unsigned long long key = (unsigned long long)__double_as_longlong(obj);
-        const unsigned long long k_old = tab[j][0];
-        const unsigned long long i_old = tab[j][1];
-        const bool cand = feasible && (key < k_old || (key == k_old && id < i_old));
+        const unsigned long long k_old = key_tab[j];
+        const unsigned int i_old = lid_tab[j];
+        const bool cand = feasible && (key < k_old || (key == k_old && lid < i_old));
+        // Keep the scheduler from interleaving configurations (register pressure).
+        __builtin_amdgcn_wave_barrier();
         if (__ballot(cand)) {
-          if (cand) atomicMin(&tab[j][0], key);
-          __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-          __builtin_amdgcn_wave_barrier();
-          const unsigned long long k_new = cand ? tab[j][0] : 0ull;
-          if (cand && k_new < k_old) tab[j][1] = kNone;
-          __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-          __builtin_amdgcn_wave_barrier();
-          if (cand && key == k_new) atomicMin(&tab[j][1], (unsigned long long)id);
-          __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-          __builtin_amdgcn_wave_barrier();
+          if (cand) atomicMin(&key_tab[j], key);
+          const unsigned long long k_new = cand ? key_tab[j] : 0ull;
+          if (cand && k_new < k_old) lid_tab[j] = 0xFFFFFFFFu;
+          if (cand && key == k_new) atomicMin(&lid_tab[j], lid);
         }
       }
     }
   }
   __syncthreads();
   if (tid < 64) {
-    double bo = __longlong_as_double((long long)w_tab[0][tid][0]);
-    uint64_t bi = w_tab[0][tid][1];
+    double bo = __longlong_as_double((long long)w_key[0][tid]);
+    unsigned int bi = w_lid[0][tid];
 #pragma unroll
     for (int w = 1; w < kWaves; ++w) {
-      const double o = __longlong_as_double((long long)w_tab[w][tid][0]);
-      const uint64_t i = w_tab[w][tid][1];
-      if (lex_less(o, i, bo, bi)) {
+      const double o = __longlong_as_double((long long)w_key[w][tid]);
+      const unsigned int i = w_lid[w][tid];
+      if (o < bo || (o == bo && i < bi)) {
         bo = o;
         bi = i;
       }
     }
     a.part_obj[(size_t)blockIdx.x * 64 + tid] = bo;
-    a.part_id[(size_t)blockIdx.x * 64 + tid] = bi;
+    a.part_id[(size_t)blockIdx.x * 64 + tid] = bi == 0xFFFFFFFFu ? kNone : g.base + (uint64_t)bi;
   }
 }
 
@@ -507,15 +535,15 @@ __global__ __launch_bounds__(256) void k_eval_ids(EvalArgs a, const uint64_t* __
   const CkptK K = ckpt_level(P, g.l, c, ke);
   const ZeroK Z = zero_level(P, z);
   const WoGoK W = wogo_levels(P, Z, r[iw], om[iw], r[ig], om[ig]);
-  const OoK O = oo_level(P, K, Z, W, r[io], om[io], hw.iP);
+  const OoK O = oo_level(oo_inputs(P, K, Z, W), r[io], om[io], hw.iP);
   const double ra = r[ia];
   const double SO = __builtin_fma(ra, P.A2, om[ia] * K.KA);
   const double H2Ds = __builtin_fma(ra, K.A, W.HW) * hw.iP;
   const double D2Hs = __builtin_fma(ra, K.A, W.DG) * hw.iP;
   struct { double t, d, mem, obj; } res;
   res.mem = O.Bmax + SO;
-  res.t = interference(K.C, Z.G2Gs, H2Ds, D2Hs, tab);
-  const double T1 = interference(K.C, Z.G2Gf, H2Ds + O.H2Dx, D2Hs + O.D2Hx, tab);
+  res.t = interference<kTabStride>(K.C, Z.G2Gs, H2Ds, D2Hs, tab);
+  const double T1 = interference<kTabStride>(K.C, Z.G2Gf, H2Ds + O.H2Dx, D2Hs + O.D2Hx, tab);
   res.d = T1 - res.t;
   res.obj = __builtin_fma((double)g.G, res.t, res.d);
   out[4 * i + 0] = res.t;
@@ -533,7 +561,7 @@ int check_launch() {
 
 template <int R>
 void launch_eval_r(const EvalArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_eval<R>, dim3(a.n_tiles), dim3(kBlock), 0, st, a);
+  hipLaunchKernelGGL(k_eval<R>, dim3(a.n_tiles), dim3(kBlock), 0, st, a, a.ratio, (const PairK*)a.pk);
 }
 
 int launch_eval(const EvalArgs& a, void* stream) {
