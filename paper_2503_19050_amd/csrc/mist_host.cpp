@@ -31,8 +31,8 @@ mist_status fail_hip(hipError_t e, const char* what) {
 }
 
 constexpr int64_t kExact = (int64_t)1 << 53;  // integers below this convert to double exactly
-constexpr int64_t kTargetTiles = 8192;        // evaluation blocks to aim for
-constexpr int64_t kStripAlign = kBlock;       // strips per tile: a multiple of the block
+constexpr int64_t kTargetTiles = 65536;       // wave work items to aim for
+constexpr int64_t kStripAlign = kWaveTile;    // strips per tile: a multiple of the wave
 
 int popcount4(int v) { return (v & 1) + ((v >> 1) & 1) + ((v >> 2) & 1) + ((v >> 3) & 1); }
 
@@ -66,6 +66,8 @@ struct mist_space {
   double* d_ratio = nullptr;
   PairK* d_pk = nullptr;
   int32_t* d_pk_group = nullptr;
+  int32_t* d_work = nullptr;
+  int32_t eval_grid = 0;
   double* d_part_obj = nullptr;
   uint64_t* d_part_id = nullptr;
   double* d_bucket_obj = nullptr;
@@ -320,7 +322,10 @@ std::string enumerate(mist_space* S) {
     d.iP = 1.0 / h.pcie_bw;
     d.iL = 1.0 / h.link_bw;
     d.M = h.mem_bytes;
-    d.kNB = (double)S->NB / h.mem_bytes;
+    // floor(mem * kNB) is min{j : mem <= E_j} or one below it (the margin 2^-40 exceeds
+    // every rounding error involved and is far below a bucket width), so one comparison
+    // with E_j settles the bucket.
+    d.kNB = ((double)S->NB / h.mem_bytes) * (1.0 - 0x1p-40);
     for (int j = 0; j < MIST_MAX_MB; ++j) d.ieta[j] = 0.0;
     for (size_t j = 0; j < S->mb.size(); ++j) {
       const double bs = (double)((int64_t)S->mb[j] * m.seq);
@@ -330,7 +335,6 @@ std::string enumerate(mist_space* S) {
     for (int j = 0; j < MIST_MAX_BUCKETS; ++j)
       d.edge[j] = j < S->NB ? (h.mem_bytes * (double)(j + 1)) / (double)S->NB : inf;
     d.edge[S->NB - 1] = h.mem_bytes;
-    for (int j = 0; j < MIST_MAX_BUCKETS; ++j) d.edge_lo[j] = j == 0 ? -inf : d.edge[j - 1];
     for (int mask = 0; mask < 16; ++mask)
       for (int j = 0; j < 4; ++j) {
         const bool update = popcount4(mask) >= 2;
@@ -381,6 +385,7 @@ mist::EvalArgs eval_args(const mist_space* S) {
   a.pk = S->d_pk;
   a.pk_group = S->d_pk_group;
   a.n_pk = (int32_t)S->pk_group.size();
+  a.work = S->d_work;
   return a;
 }
 
@@ -514,7 +519,19 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
     if (!rc) rc = upload(S, &S->d_pk_group, S->pk_group, "pair groups");
     if (!rc) {
       S->d_pk = (PairK*)dev_alloc(S, S->pk_group.size() * sizeof(PairK));
-      if (!S->d_pk) rc = fail(MIST_E_NOMEM, "device allocation failed: pair constants");
+      S->d_work = (int32_t*)dev_alloc(S, sizeof(int32_t));
+      if (!S->d_pk || !S->d_work) rc = fail(MIST_E_NOMEM, "device allocation failed: pair constants");
+    }
+    if (!rc) {
+      // Persistent evaluation grid: as many blocks as fit on the device at once.
+      int dev = 0, cus = 0;
+      hipError_t e = hipGetDevice(&dev);
+      if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+      if (e != hipSuccess) rc = fail_hip(e, "device attributes");
+      const int per_cu = eval_blocks_per_cu(S->R);
+      const int64_t want = (int64_t)cus * (per_cu > 0 ? per_cu : 1);
+      const int64_t waves_needed = (int64_t)(S->tiles.size() + kWaves - 1) / kWaves;
+      S->eval_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>(want, waves_needed));
     }
     const size_t nt = S->tiles.size(), ng = S->groups.size();
     if (!rc) {
@@ -562,7 +579,7 @@ mist_status mist_eval_space(mist_space* S, void* hip_stream) {
     const hipError_t e = hipEventRecord(ev[0], st);
     if (e != hipSuccess) return fail_hip(e, "hipEventRecord");
   }
-  rc = launch_eval(ea, st);
+  rc = launch_eval(ea, S->eval_grid, st);
   if (rc) return fail_hip((hipError_t)rc, "evaluation kernel launch");
   if (ev) {
     const hipError_t e = hipEventRecord(ev[1], st);
@@ -734,7 +751,7 @@ mist_status mist_read_timing(mist_space* S, double* eval_ms, double* reduce_ms, 
 mist_status mist_launch_info(const mist_space* S, int64_t* n_tiles, int32_t* block, int32_t* strips_per_tile) {
   if (!S) return fail(MIST_E_INVALID, "space is null");
   if (n_tiles) *n_tiles = (int64_t)S->tiles.size();
-  if (block) *block = kBlock;
+  if (block) *block = kWaveTile;
   if (strips_per_tile) *strips_per_tile = S->strips_per_tile;
   return MIST_OK;
 }

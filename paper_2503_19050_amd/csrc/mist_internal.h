@@ -9,6 +9,7 @@ namespace mist {
 
 constexpr int kBlock = 256;           // threads per evaluation block
 constexpr int kWaves = kBlock / 64;   // wave64
+constexpr int kWaveTile = 64;         // threads per tile: each wave works on its own tiles
 constexpr int kReduceBlock = 256;     // group-reduction block: one wave per group
 constexpr int kTabStride = 8;         // interference table row: phi[4], psi[4]
 
@@ -30,7 +31,7 @@ struct DevPair {
   double inv_dp;          // 1 / DP, host division
 };
 
-// A block's work: strips [strip_begin, strip_end) of one group.  A strip is one
+// A wave's work item: strips [strip_begin, strip_end) of one group.  A strip is one
 // (pair, recomputed layers, ZeRO level, weight ratio, gradient ratio) combination and
 // holds the R^2 configurations of its (optimizer ratio, activation ratio) digits; strip s
 // of a group covers local ids [s * R^2, (s + 1) * R^2).
@@ -45,10 +46,9 @@ struct DevTile {
 struct DevHw {
   double iF, iP, iL;         // 1 / FLOP/s, 1 / PCIe, 1 / link
   double M;                  // memory budget
-  double kNB;                // NB / M (bucket estimate, corrected against the edges)
+  double kNB;                // NB / M * (1 - 2^-40): floor(mem * kNB) is the bucket or one below
   double ieta[MIST_MAX_MB];  // 1 / eta(b) per microbatch index
   double edge[MIST_MAX_BUCKETS];     // E_j; +inf past NB
-  double edge_lo[MIST_MAX_BUCKETS];  // E_{j-1}; -inf for j = 0
   // Row per co-running pattern (bit j = stream j runs): phi[4] then psi[4].  Patterns of
   // two or more streams: members carry phi and psi = 1/phi, other streams phi = +inf and
   // psi = 1 (their 0 or NaN time scales to NaN, which min/max skip).  Patterns of at most
@@ -83,6 +83,7 @@ struct EvalArgs {
   const double* ratio;   // r[0..R), then om[0..R) = 1 - r
   int32_t R, NB;
   int32_t n_tiles;
+  int32_t* work;         // tile counter of the persistent evaluation kernel (reset by K0)
   int64_t n_groups;
   uint64_t n_configs;
   double* part_obj;      // [n_tiles][64]
@@ -107,7 +108,8 @@ struct ReduceArgs {
 
 // Kernel launchers (mist_kernels.hip).
 int launch_pairs(const EvalArgs& a, void* stream);
-int launch_eval(const EvalArgs& a, void* stream);
+int launch_eval(const EvalArgs& a, int blocks, void* stream);
+int eval_blocks_per_cu(int R);
 int launch_reduce(const ReduceArgs& a, void* stream);
 int launch_eval_ids(const EvalArgs& a, const uint64_t* ids, int64_t n, double* out, void* stream);
 

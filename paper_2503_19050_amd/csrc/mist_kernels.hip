@@ -260,26 +260,43 @@ __device__ __forceinline__ double interference_strip(const FirstRow& r, double h
   return T + remaining(x);
 }
 
+// K0: pair-level constants of every (group, pair).
+__global__ __launch_bounds__(256) void k_pairs(EvalArgs a) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) *a.work = 0;  // the evaluation kernel's tile counter (it runs after this kernel)
+  if (i >= a.n_pk) return;
+  const DevGroup g = a.groups[a.pk_group[i]];
+  const int p = i - g.pk_begin;
+  a.pk[i] = pair_level(a.m, g.PP, g.k, g.l, a.pairs[g.pair_begin + p], a.hws[g.hw]);
+}
+
 // ---------------------------------------------------------------------------------------
-// K1.  One block per tile (a range of strips of one group); each thread walks strips with
-// the block's stride.  A strip fixes (pair, c, z, wo, go) and holds the R x R
-// (optimizer ratio, activation ratio) configurations:
+// K1.  Persistent: every wave claims tiles (a range of strips of one group) from a device
+// counter until none is left, and each lane walks the tile's strips with stride 64.  A
+// strip fixes (pair, c, z, wo, go) and holds the R x R (optimizer ratio, activation ratio)
+// configurations:
 //   - the stable time t does not depend on the optimizer ratio, so it is computed once per
 //     activation ratio and reused across the optimizer ratios;
 //   - the first microbatch's streams start in the same pattern for every configuration of
 //     the strip (compute, GPU-GPU iff that stream carries traffic, and both host streams
 //     iff any offload ratio is non-zero), except the one configuration whose four ratios
 //     are all zero, which takes the looked-up path.
-// Every wave keeps a private LDS table of the 64 bucket minima; candidates (rare) are
-// applied one lane at a time; the block merges the tables into the tile's partials.
+// Each wave keeps an LDS table of the 64 bucket minima of its current tile and writes it
+// as the tile's partials.
 // ---------------------------------------------------------------------------------------
-// K0: pair-level constants of every (group, pair).
-__global__ __launch_bounds__(256) void k_pairs(EvalArgs a) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= a.n_pk) return;
-  const DevGroup g = a.groups[a.pk_group[i]];
-  const int p = i - g.pk_begin;
-  a.pk[i] = pair_level(a.m, g.PP, g.k, g.l, a.pairs[g.pair_begin + p], a.hws[g.hw]);
+struct BucketEntry {
+  unsigned long long key;  // bits of the minimum objective (a non-negative double orders like
+                           // its bit pattern)
+  unsigned int lid;        // lowest local id (id - group base, < 2^32) reaching it
+  unsigned int pad;
+};
+
+// Orders this wave's LDS accesses for the compiler: a lane may read a word another lane of
+// the same wave wrote (the hardware executes a wave's LDS operations in order), so no load
+// may be moved across this point or answered from the lane's own earlier store.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
 }
 
 // Waves per SIMD the register allocation aims at: the strip keeps R stable times live, so
@@ -289,158 +306,152 @@ constexpr int eval_waves() { return R <= 6 ? 4 : 3; }
 
 template <int R>
 __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, const double* __restrict__ ratio,
-                                                    const PairK* __restrict__ pk) {
+                                                                 const PairK* __restrict__ pk) {
   constexpr int R2 = R * R;
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
-  __shared__ double s_tab[16 * kLdsRow];
-  __shared__ double s_edge[MIST_MAX_BUCKETS];
-  __shared__ double s_edge_lo[MIST_MAX_BUCKETS];
-  // Per-wave bucket table: bits of the minimum objective (a non-negative double orders like
-  // its bit pattern) and the lowest local id (id - group base, < 2^32) reaching it.
-  __shared__ unsigned long long w_key[kWaves][64];
-  __shared__ unsigned int w_lid[kWaves][64];
-  __shared__ OoIn s_oo[kBlock];       // per-lane strip constants of the optimizer level
+  __shared__ double s_tab[kWaves][16 * kLdsRow];
+  __shared__ double s_edge[kWaves][MIST_MAX_BUCKETS];
+  __shared__ BucketEntry s_bucket[kWaves][64];
+  __shared__ OoIn s_oo[kBlock];         // per-lane strip constants of the optimizer level
   __shared__ double s_zero[kBlock][2];  // per-lane C and G2G (first microbatch) of the strip
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const DevTile tile = a.tiles[blockIdx.x];
-  const DevGroup g = a.groups[tile.group];
-  const DevHw& hw = a.hws[g.hw];
   const int NB = a.NB;
-  const double* __restrict__ rr = ratio;        // read-only and uniform: scalar loads
+  const double* __restrict__ rr = ratio;  // read-only and uniform: scalar loads
   const double* __restrict__ om = ratio + R;
-
-  for (int i = tid; i < 16 * kTabStride; i += kBlock)
-    s_tab[(i / kTabStride) * kLdsRow + i % kTabStride] = (&hw.itab[0][0])[i];
-  if (tid < MIST_MAX_BUCKETS) {
-    s_edge[tid] = hw.edge[tid];
-    s_edge_lo[tid] = hw.edge_lo[tid];
-  }
-  w_key[wave][lane] = (unsigned long long)__double_as_longlong(__builtin_huge_val());
-  w_lid[wave][lane] = 0xFFFFFFFFu;
-  __syncthreads();
-  unsigned long long* key_tab = w_key[wave];
-  unsigned int* lid_tab = w_lid[wave];
-
-  const double iP = hw.iP, M = hw.M, kNB = hw.kNB;
-  const double top = (double)(NB - 1);
-  const int l = g.l;
-  const int64_t ke = g.k < g.G ? g.k : g.G;
-  const double Gd = (double)g.G;
   const bool r0_zero = rr[0] == 0.0;
+  double* tab = s_tab[wave];
+  double* edge = s_edge[wave];
+  BucketEntry* bucket = s_bucket[wave];
+  const unsigned long long kEmpty = (unsigned long long)__double_as_longlong(__builtin_huge_val());
 
-#pragma unroll 1
-  for (int s = tile.strip_begin + tid; s < tile.strip_end; s += kBlock) {
-    const int unit = s / SU;
-    const int rem = s - unit * SU;
-    const int z = rem / R2;
-    const int rem2 = rem - z * R2;
-    const int iw = rem2 / R;
-    const int ig = rem2 - iw * R;
-    const int p = unit / (l + 1);
-    const int c = unit - p * (l + 1);
-    const PairK P = pk[g.pk_begin + p];
-    const CkptK K = ckpt_level(P, l, c, ke);
-    const ZeroK Z = zero_level(P, z);
-    const double rw = rr[iw], rg = rr[ig];
-    const WoGoK W = wogo_levels(P, Z, rw, om[iw], rg, om[ig]);
-
-    // Stable time per activation ratio (it does not depend on the optimizer ratio).  With
-    // a positive activation ratio both host streams run, so the first round's pattern is
-    // compute + both host streams (+ GPU-GPU when it carries traffic).
-    double tt[R];
-    const double* es = s_tab + (Z.G2Gs > 0.0 ? 15 : 13) * kLdsRow;
-#pragma unroll
-    for (int ia = 0; ia < R; ++ia) {
-      const double H2Ds = __builtin_fma(rr[ia], K.A, W.HW) * iP;
-      const double D2Hs = __builtin_fma(rr[ia], K.A, W.DG) * iP;
-      if (ia == 0 && r0_zero) tt[ia] = interference(K.C, Z.G2Gs, H2Ds, D2Hs, s_tab);
-      else tt[ia] = interference_first(es, K.C, Z.G2Gs, H2Ds, D2Hs, s_tab);
+  int loaded_hw = -1;
+  for (;;) {
+    int t = 0;
+    if (lane == 0) t = atomicAdd(a.work, 1);
+    t = __builtin_amdgcn_readfirstlane(__shfl(t, 0, 64));
+    if (t >= a.n_tiles) break;
+    const DevTile tile = a.tiles[t];
+    const DevGroup g = a.groups[tile.group];
+    const DevHw& hw = a.hws[g.hw];
+    if (g.hw != loaded_hw) {  // the wave's LDS copy of the hardware tables
+      for (int i = lane; i < 16 * kTabStride; i += 64)
+        tab[(i / kTabStride) * kLdsRow + i % kTabStride] = (&hw.itab[0][0])[i];
+      edge[lane] = hw.edge[lane];
+      loaded_hw = g.hw;
     }
-    // First microbatch: every configuration of the strip with a non-zero offload ratio
-    // starts with compute, both host streams and (if it carries traffic) GPU-GPU.
-    const double* e1 = s_tab + (Z.G2Gf > 0.0 ? 15 : 13) * kLdsRow;
-    FirstRow fr;
-    fr.s0 = K.C * e1[0];
-    fr.s1 = Z.G2Gf * e1[1];
-    fr.m01 = __builtin_fmin(fr.s0, fr.s1);
-    fr.f2 = e1[2];
-    fr.f3 = e1[3];
-    fr.p0 = e1[4];
-    fr.p1 = e1[5];
-    fr.p2 = e1[6];
-    fr.p3 = e1[7];
-    const bool zero_strip = r0_zero && rw == 0.0 && rg == 0.0;
-    s_oo[tid] = oo_inputs(P, K, Z, W);
-    s_zero[tid][0] = K.C;
-    s_zero[tid][1] = Z.G2Gf;
-    const double A = K.A, KA = K.KA, A2 = P.A2, HW = W.HW, DG = W.DG;
-    const unsigned int lid_strip = (unsigned int)s * (unsigned int)R2;
+    bucket[lane].key = kEmpty;
+    bucket[lane].lid = 0xFFFFFFFFu;
+    wave_sync();
+
+    const double iP = hw.iP, M = hw.M, kNB = hw.kNB;
+    const double top = (double)(NB - 1);
+    const int l = g.l;
+    const int64_t ke = g.k < g.G ? g.k : g.G;
+    const double Gd = (double)g.G;
 
 #pragma unroll 1
-    for (int io = 0; io < R; ++io) {
-      const OoK O = oo_level(s_oo[tid], rr[io], om[io], iP);
-      const bool zero_oo = zero_strip && io == 0;
-      const unsigned int lid_oo = lid_strip + (unsigned int)(io * R);
+    for (int s = tile.strip_begin + lane; s < tile.strip_end; s += 64) {
+      const int unit = s / SU;
+      const int rem = s - unit * SU;
+      const int z = rem / R2;
+      const int rem2 = rem - z * R2;
+      const int iw = rem2 / R;
+      const int ig = rem2 - iw * R;
+      const int p = unit / (l + 1);
+      const int c = unit - p * (l + 1);
+      const PairK P = pk[g.pk_begin + p];
+      const CkptK K = ckpt_level(P, l, c, ke);
+      const ZeroK Z = zero_level(P, z);
+      const double rw = rr[iw], rg = rr[ig];
+      const WoGoK W = wogo_levels(P, Z, rw, om[iw], rg, om[ig]);
+
+      // Stable time per activation ratio (it does not depend on the optimizer ratio).  With
+      // a positive activation ratio both host streams run, so the first round's pattern is
+      // compute + both host streams (+ GPU-GPU when it carries traffic).
+      double tt[R];
+      const double* es = tab + (Z.G2Gs > 0.0 ? 15 : 13) * kLdsRow;
 #pragma unroll
       for (int ia = 0; ia < R; ++ia) {
-        const double ra = rr[ia];
-        const double SO = __builtin_fma(ra, A2, om[ia] * KA);  // stash + offload buffers
-        const double mem = O.Bmax + SO;
-        const double H2Df = __builtin_fma(ra, A, HW) * iP + O.H2Dx;
-        const double D2Hf = __builtin_fma(ra, A, DG) * iP + O.D2Hx;
-        double T1;
-        if (ia == 0 && zero_oo) T1 = interference(s_zero[tid][0], s_zero[tid][1], H2Df, D2Hf, s_tab);
-        else T1 = interference_strip(fr, H2Df, D2Hf, s_tab);
-        const double t = tt[ia];
-        const double d = T1 - t;
-        const double obj = __builtin_fma(Gd, t, d);
-        const unsigned int lid = lid_oo + (unsigned int)ia;
+        const double H2Ds = __builtin_fma(rr[ia], K.A, W.HW) * iP;
+        const double D2Hs = __builtin_fma(rr[ia], K.A, W.DG) * iP;
+        if (ia == 0 && r0_zero) tt[ia] = interference(K.C, Z.G2Gs, H2Ds, D2Hs, tab);
+        else tt[ia] = interference_first(es, K.C, Z.G2Gs, H2Ds, D2Hs, tab);
+      }
+      // First microbatch: every configuration of the strip with a non-zero offload ratio
+      // starts with compute, both host streams and (if it carries traffic) GPU-GPU.
+      const double* e1 = tab + (Z.G2Gf > 0.0 ? 15 : 13) * kLdsRow;
+      FirstRow fr;
+      fr.s0 = K.C * e1[0];
+      fr.s1 = Z.G2Gf * e1[1];
+      fr.m01 = __builtin_fmin(fr.s0, fr.s1);
+      fr.f2 = e1[2];
+      fr.f3 = e1[3];
+      fr.p0 = e1[4];
+      fr.p1 = e1[5];
+      fr.p2 = e1[6];
+      fr.p3 = e1[7];
+      const bool zero_strip = r0_zero && rw == 0.0 && rg == 0.0;
+      s_oo[tid] = oo_inputs(P, K, Z, W);
+      s_zero[tid][0] = K.C;
+      s_zero[tid][1] = Z.G2Gf;
+      const double A = K.A, KA = K.KA, A2 = P.A2, HW = W.HW, DG = W.DG;
+      const unsigned int lid_strip = (unsigned int)s * (unsigned int)R2;
 
-        // Feasibility (Eq. 4) and bucket: floor(mem * NB / M) is within one of the bucket.
-        const bool feasible = mem <= M;
-        const int j0 = (int)__builtin_fmin(mem * kNB, top);
-        const int jb = j0 + (mem > s_edge[j0] ? 1 : 0) - (mem <= s_edge_lo[j0] ? 1 : 0);
-        const int j = feasible ? min(max(jb, 0), NB - 1) : 0;
+#pragma unroll 1
+      for (int io = 0; io < R; ++io) {
+        const OoK O = oo_level(s_oo[tid], rr[io], om[io], iP);
+        const bool zero_oo = zero_strip && io == 0;
+        const unsigned int lid_oo = lid_strip + (unsigned int)(io * R);
+#pragma unroll
+        for (int ia = 0; ia < R; ++ia) {
+          const double ra = rr[ia];
+          const double SO = __builtin_fma(ra, A2, om[ia] * KA);  // stash + offload buffers
+          const double mem = O.Bmax + SO;
+          const double H2Df = __builtin_fma(ra, A, HW) * iP + O.H2Dx;
+          const double D2Hf = __builtin_fma(ra, A, DG) * iP + O.D2Hx;
+          double T1;
+          if (ia == 0 && zero_oo) T1 = interference(s_zero[tid][0], s_zero[tid][1], H2Df, D2Hf, tab);
+          else T1 = interference_strip(fr, H2Df, D2Hf, tab);
+          const double tv = tt[ia];
+          const double d = T1 - tv;
+          const double obj = __builtin_fma(Gd, tv, d);
+          const unsigned int lid = lid_oo + (unsigned int)ia;
 
-        // Lexicographic (obj, id) minimum per bucket without a serial loop: the lanes that
-        // beat their bucket's entry lower the objective bits with an LDS atomic minimum;
-        // a lane that sees its bucket's objective drop clears the id, then the lanes whose
-        // objective equals the new minimum lower the id.  The LDS operations of a wave
-        // execute in program order and each step addresses the same words as the one
-        // before, so each step sees the previous one's result.
-        const unsigned long long key = (unsigned long long)__double_as_longlong(obj);
-        const unsigned long long k_old = key_tab[j];
-        const unsigned int i_old = lid_tab[j];
-        const bool cand = feasible && (key < k_old || (key == k_old && lid < i_old));
-        // Keep the scheduler from interleaving configurations (register pressure).
-        __builtin_amdgcn_wave_barrier();
-        if (__ballot(cand)) {
-          if (cand) atomicMin(&key_tab[j], key);
-          const unsigned long long k_new = cand ? key_tab[j] : 0ull;
-          if (cand && k_new < k_old) lid_tab[j] = 0xFFFFFFFFu;
-          if (cand && key == k_new) atomicMin(&lid_tab[j], lid);
+          // Feasibility (Eq. 4) and bucket j = min{j : mem <= E_j}: floor(mem * kNB) is j
+          // or j - 1 (kNB carries a 2^-40 margin), so one comparison with E settles it.
+          const bool feasible = mem <= M;
+          const int j0 = (int)__builtin_fmin(mem * kNB, top);
+          const int jb = min(j0 + (mem > edge[j0] ? 1 : 0), NB - 1);
+          const int j = feasible ? jb : 0;
+
+          // Lexicographic (obj, id) minimum per bucket without a serial loop: the lanes that
+          // beat their bucket's entry lower the objective bits with an LDS atomic minimum;
+          // a lane that sees its bucket's objective drop clears the id, then the lanes whose
+          // objective equals the new minimum lower the id.  The LDS operations of a wave
+          // execute in program order and each step addresses the same words as the one
+          // before, so each step sees the previous one's result.
+          const unsigned long long key = (unsigned long long)__double_as_longlong(obj);
+          wave_sync();  // read the entry after every earlier update of the wave
+          const unsigned long long k_old = bucket[j].key;
+          const unsigned int i_old = bucket[j].lid;
+          const bool cand = feasible && (key < k_old || (key == k_old && lid < i_old));
+          if (__ballot(cand)) {
+            if (cand) atomicMin(&bucket[j].key, key);
+            const unsigned long long k_new = cand ? bucket[j].key : 0ull;
+            if (cand && k_new < k_old) bucket[j].lid = 0xFFFFFFFFu;
+            if (cand && key == k_new) atomicMin(&bucket[j].lid, lid);
+          }
         }
       }
     }
-  }
-  __syncthreads();
-  if (tid < 64) {
-    double bo = __longlong_as_double((long long)w_key[0][tid]);
-    unsigned int bi = w_lid[0][tid];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) {
-      const double o = __longlong_as_double((long long)w_key[w][tid]);
-      const unsigned int i = w_lid[w][tid];
-      if (o < bo || (o == bo && i < bi)) {
-        bo = o;
-        bi = i;
-      }
-    }
-    a.part_obj[(size_t)blockIdx.x * 64 + tid] = bo;
-    a.part_id[(size_t)blockIdx.x * 64 + tid] = bi == 0xFFFFFFFFu ? kNone : g.base + (uint64_t)bi;
+    // The tile's partials: lane j = bucket j.
+    wave_sync();
+    const unsigned int bl = bucket[lane].lid;
+    a.part_obj[(size_t)t * 64 + lane] = __longlong_as_double((long long)bucket[lane].key);
+    a.part_id[(size_t)t * 64 + lane] = bl == 0xFFFFFFFFu ? kNone : g.base + (uint64_t)bl;
   }
 }
 
@@ -557,34 +568,47 @@ int check_launch() {
   return e == hipSuccess ? 0 : (int)e;
 }
 
-}  // namespace
-
 template <int R>
-void launch_eval_r(const EvalArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_eval<R>, dim3(a.n_tiles), dim3(kBlock), 0, st, a, a.ratio, (const PairK*)a.pk);
+void launch_eval_r(const EvalArgs& a, int blocks, hipStream_t st) {
+  hipLaunchKernelGGL(k_eval<R>, dim3(blocks), dim3(kBlock), 0, st, a, a.ratio, (const PairK*)a.pk);
 }
 
-int launch_eval(const EvalArgs& a, void* stream) {
+template <int R>
+int blocks_per_cu_r() {
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_eval<R>, kBlock, 0) != hipSuccess) return 1;
+  return n;
+}
+
+#define MIST_FOR_EACH_R(X) \
+  X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16)
+
+}  // namespace
+
+int eval_blocks_per_cu(int R) {
+  switch (R) {
+#define MIST_CASE(n) \
+  case n:            \
+    return blocks_per_cu_r<n>();
+    MIST_FOR_EACH_R(MIST_CASE)
+#undef MIST_CASE
+    default:
+      return 1;
+  }
+}
+
+int launch_eval(const EvalArgs& a, int blocks, void* stream) {
   if (a.n_tiles <= 0) return 0;
   hipStream_t st = (hipStream_t)stream;
   switch (a.R) {
-    case 1: launch_eval_r<1>(a, st); break;
-    case 2: launch_eval_r<2>(a, st); break;
-    case 3: launch_eval_r<3>(a, st); break;
-    case 4: launch_eval_r<4>(a, st); break;
-    case 5: launch_eval_r<5>(a, st); break;
-    case 6: launch_eval_r<6>(a, st); break;
-    case 7: launch_eval_r<7>(a, st); break;
-    case 8: launch_eval_r<8>(a, st); break;
-    case 9: launch_eval_r<9>(a, st); break;
-    case 10: launch_eval_r<10>(a, st); break;
-    case 11: launch_eval_r<11>(a, st); break;
-    case 12: launch_eval_r<12>(a, st); break;
-    case 13: launch_eval_r<13>(a, st); break;
-    case 14: launch_eval_r<14>(a, st); break;
-    case 15: launch_eval_r<15>(a, st); break;
-    case 16: launch_eval_r<16>(a, st); break;
-    default: return (int)hipErrorInvalidValue;
+#define MIST_CASE(n)                 \
+  case n:                            \
+    launch_eval_r<n>(a, blocks, st); \
+    break;
+    MIST_FOR_EACH_R(MIST_CASE)
+#undef MIST_CASE
+    default:
+      return (int)hipErrorInvalidValue;
   }
   return check_launch();
 }
