@@ -31,7 +31,10 @@ mist_status fail_hip(hipError_t e, const char* what) {
 }
 
 constexpr int64_t kExact = (int64_t)1 << 53;  // integers below this convert to double exactly
-constexpr int64_t kTargetTiles = 65536;       // wave work items to aim for
+constexpr int64_t kStaticStrips = 512;        // strips per resident wave up to which a space is
+                                              // cut into one tile per wave
+constexpr int64_t kMinTileConfigs = 8192;     // configurations per tile of a larger space, at least
+constexpr int64_t kMaxTiles = 131072;         // and tiles per space, at most
 constexpr int64_t kStripAlign = kWaveTile;    // strips per tile: a multiple of the wave
 
 int popcount4(int v) { return (v & 1) + ((v >> 1) & 1) + ((v >> 2) & 1) + ((v >> 3) & 1); }
@@ -284,33 +287,12 @@ std::string enumerate(mist_space* S) {
     if (S->pk_group.size() > (size_t)INT32_MAX) return "too many pairs";
   }
 
-  // Tiles: contiguous strips of one group, at most strips_per_tile each.
+  // Strips per group (a strip is one (pair, c, z, wo, go) combination with its R x R
+  // configurations); tiles are cut once the device's resident wave count is known.
   const uint64_t per_unit_strips = 4ull * (uint64_t)(R * R);
-  uint64_t total_strips = 0;
   for (const DevGroup& g : S->groups) {
     const uint64_t st = (uint64_t)g.n_pairs * (uint64_t)(g.l + 1) * per_unit_strips;
     if (st > (uint64_t)INT32_MAX) return "group too large";
-    total_strips += st;
-  }
-  uint64_t spt = (total_strips + kTargetTiles - 1) / kTargetTiles;
-  spt = (spt + kStripAlign - 1) / kStripAlign * kStripAlign;
-  if (spt < (uint64_t)kStripAlign) spt = kStripAlign;
-  if (spt > (uint64_t)INT32_MAX / 2) spt = (uint64_t)INT32_MAX / 2 / kStripAlign * kStripAlign;
-  S->strips_per_tile = (int32_t)spt;
-  S->tiles.clear();
-  for (size_t gi = 0; gi < S->groups.size(); ++gi) {
-    DevGroup& g = S->groups[gi];
-    const int64_t strips = (int64_t)g.n_pairs * (g.l + 1) * (int64_t)per_unit_strips;
-    g.tile_begin = (int32_t)S->tiles.size();
-    for (int64_t u = 0; u < strips; u += (int64_t)spt) {
-      DevTile t{};
-      t.group = (int32_t)gi;
-      t.strip_begin = (int32_t)u;
-      t.strip_end = (int32_t)std::min<int64_t>(strips, u + (int64_t)spt);
-      S->tiles.push_back(t);
-    }
-    g.n_tiles = (int32_t)S->tiles.size() - g.tile_begin;
-    if (S->tiles.size() > (size_t)INT32_MAX) return "too many tiles";
   }
 
   // Per-hardware tables (host divisions, each correctly rounded).
@@ -479,6 +461,52 @@ mist_status fill_results(mist_space* S, const uint64_t* ids, const double* objs,
 
 }  // namespace
 
+namespace {
+
+// Tiles: contiguous strips of one group, at most strips_per_tile each (a multiple of the wave
+// width).  Every wave of the persistent evaluation grid takes tile number (its global wave
+// index) first and claims further tiles from the device counter.  A space of at most
+// kStaticStrips strips per resident wave is cut into about one tile per resident wave, so that
+// no claim is made.  A larger one is cut into tiles of at least kMinTileConfigs configurations
+// (a claim is a device-wide atomic whose latency a wave waits out, and claims on one counter
+// serialize) and at most kMaxTiles tiles (a wave that finishes last holds the kernel for up to
+// one tile).
+std::string build_tiles(mist_space* S, int64_t resident_waves) {
+  const uint64_t per_unit_strips = 4ull * (uint64_t)(S->R * S->R);
+  uint64_t total_strips = 0;
+  for (const DevGroup& g : S->groups) total_strips += (uint64_t)g.n_pairs * (uint64_t)(g.l + 1) * per_unit_strips;
+  const uint64_t W = (uint64_t)std::max<int64_t>(1, resident_waves);
+  const uint64_t R2 = (uint64_t)(S->R * S->R);
+  uint64_t spt;
+  if (total_strips <= W * (uint64_t)kStaticStrips)
+    spt = (total_strips + W - 1) / W;
+  else
+    spt = std::max<uint64_t>(((uint64_t)kMinTileConfigs + R2 - 1) / R2,
+                             (total_strips + (uint64_t)kMaxTiles - 1) / (uint64_t)kMaxTiles);
+  spt = (spt + kStripAlign - 1) / kStripAlign * kStripAlign;
+  if (spt < (uint64_t)kStripAlign) spt = kStripAlign;
+  if (spt > (uint64_t)INT32_MAX / 2) spt = (uint64_t)INT32_MAX / 2 / kStripAlign * kStripAlign;
+  S->strips_per_tile = (int32_t)spt;
+  S->tiles.clear();
+  for (size_t gi = 0; gi < S->groups.size(); ++gi) {
+    DevGroup& g = S->groups[gi];
+    const int64_t strips = (int64_t)g.n_pairs * (g.l + 1) * (int64_t)per_unit_strips;
+    g.tile_begin = (int32_t)S->tiles.size();
+    for (int64_t u = 0; u < strips; u += (int64_t)spt) {
+      DevTile t{};
+      t.group = (int32_t)gi;
+      t.strip_begin = (int32_t)u;
+      t.strip_end = (int32_t)std::min<int64_t>(strips, u + (int64_t)spt);
+      S->tiles.push_back(t);
+    }
+    g.n_tiles = (int32_t)S->tiles.size() - g.tile_begin;
+    if (S->tiles.size() > (size_t)INT32_MAX / 2) return "too many tiles";  // + waves fits int
+  }
+  return "";
+}
+
+}  // namespace
+
 extern "C" {
 
 mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n_hw,
@@ -511,6 +539,24 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
       return fail(MIST_E_INVALID, err);
     }
     mist_status rc = MIST_OK;
+    // Persistent evaluation grid: as many blocks as fit on the device at once.
+    int64_t resident_blocks = 1;
+    {
+      int dev = 0, cus = 0;
+      hipError_t e = hipGetDevice(&dev);
+      if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+      if (e != hipSuccess) rc = fail_hip(e, "device attributes");
+      const int per_cu = eval_blocks_per_cu(S->R);
+      resident_blocks = std::max<int64_t>(1, (int64_t)cus * (per_cu > 0 ? per_cu : 1));
+    }
+    if (!rc) {
+      const std::string terr = build_tiles(S, resident_blocks * kWaves);
+      if (!terr.empty()) rc = fail(MIST_E_INVALID, terr);
+    }
+    if (!rc) {
+      const int64_t waves_needed = (int64_t)(S->tiles.size() + kWaves - 1) / kWaves;
+      S->eval_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>(resident_blocks, waves_needed));
+    }
     if (!rc) rc = upload(S, &S->d_groups, S->groups, "groups");
     if (!rc) rc = upload(S, &S->d_pairs, S->pairs, "pairs");
     if (!rc) rc = upload(S, &S->d_tiles, S->tiles, "tiles");
@@ -521,17 +567,6 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
       S->d_pk = (PairK*)dev_alloc(S, S->pk_group.size() * sizeof(PairK));
       S->d_work = (int32_t*)dev_alloc(S, sizeof(int32_t));
       if (!S->d_pk || !S->d_work) rc = fail(MIST_E_NOMEM, "device allocation failed: pair constants");
-    }
-    if (!rc) {
-      // Persistent evaluation grid: as many blocks as fit on the device at once.
-      int dev = 0, cus = 0;
-      hipError_t e = hipGetDevice(&dev);
-      if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-      if (e != hipSuccess) rc = fail_hip(e, "device attributes");
-      const int per_cu = eval_blocks_per_cu(S->R);
-      const int64_t want = (int64_t)cus * (per_cu > 0 ? per_cu : 1);
-      const int64_t waves_needed = (int64_t)(S->tiles.size() + kWaves - 1) / kWaves;
-      S->eval_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>(want, waves_needed));
     }
     const size_t nt = S->tiles.size(), ng = S->groups.size();
     if (!rc) {

@@ -211,9 +211,10 @@ constexpr int kLdsRow = 10;
 
 template <int STRIDE>
 __device__ __forceinline__ double round_lookup(Streams& x, const double* __restrict__ tab) {
-  const int pat = (x.x0 > 0.0 ? 1 : 0) | (x.x1 > 0.0 ? 2 : 0) | (x.x2 > 0.0 ? 4 : 0) |
-                  (x.x3 > 0.0 ? 8 : 0);
-  const double* e = tab + pat * STRIDE;
+  // Row of the non-zero pattern (bit i for stream i), as a pre-scaled offset.
+  const int off = (x.x0 > 0.0 ? STRIDE : 0) + (x.x1 > 0.0 ? 2 * STRIDE : 0) +
+                  (x.x2 > 0.0 ? 4 * STRIDE : 0) + (x.x3 > 0.0 ? 8 * STRIDE : 0);
+  const double* e = tab + off;
   return round_row(x, e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]);
 }
 
@@ -271,8 +272,9 @@ __global__ __launch_bounds__(256) void k_pairs(EvalArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------
-// K1.  Persistent: every wave claims tiles (a range of strips of one group) from a device
-// counter until none is left, and each lane walks the tile's strips with stride 64.  A
+// K1.  Persistent: every wave takes one tile (a range of strips of one group) by its index
+// in the grid and claims further tiles from a device counter until none is left; each lane
+// walks the tile's strips with stride 64.  A
 // strip fixes (pair, c, z, wo, go) and holds the R x R (optimizer ratio, activation ratio)
 // configurations:
 //   - the stable time t does not depend on the optimizer ratio, so it is computed once per
@@ -302,7 +304,7 @@ __device__ __forceinline__ void wave_sync() {
 // Waves per SIMD the register allocation aims at: the strip keeps R stable times live, so
 // large ratio counts trade a wave of occupancy for spill-free code.
 template <int R>
-constexpr int eval_waves() { return R <= 6 ? 4 : 3; }
+constexpr int eval_waves() { return R <= 4 ? 4 : 3; }
 
 template <int R>
 __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, const double* __restrict__ ratio,
@@ -311,7 +313,7 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
   __shared__ double s_tab[kWaves][16 * kLdsRow];
   __shared__ double s_edge[kWaves][MIST_MAX_BUCKETS];
-  __shared__ BucketEntry s_bucket[kWaves][64];
+  __shared__ BucketEntry s_bucket[kWaves][65];  // entries NB..64: sinks of infeasible configurations
   __shared__ OoIn s_oo[kBlock];         // per-lane strip constants of the optimizer level
   __shared__ double s_zero[kBlock][2];  // per-lane C and G2G (first microbatch) of the strip
 
@@ -327,12 +329,13 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
   BucketEntry* bucket = s_bucket[wave];
   const unsigned long long kEmpty = (unsigned long long)__double_as_longlong(__builtin_huge_val());
 
+  // Tile schedule: wave w of the grid takes tile w, then tiles n_waves + c for the claim
+  // numbers c it draws from the device counter (reset to 0 by K0), until they run out.  When
+  // the grid has at least as many waves as there are tiles no claim is made.
+  const int n_waves = (int)gridDim.x * kWaves;
+  const bool claims = a.n_tiles > n_waves;
   int loaded_hw = -1;
-  for (;;) {
-    int t = 0;
-    if (lane == 0) t = atomicAdd(a.work, 1);
-    t = __builtin_amdgcn_readfirstlane(__shfl(t, 0, 64));
-    if (t >= a.n_tiles) break;
+  for (int t = (int)blockIdx.x * kWaves + wave; t < a.n_tiles;) {
     const DevTile tile = a.tiles[t];
     const DevGroup g = a.groups[tile.group];
     const DevHw& hw = a.hws[g.hw];
@@ -342,12 +345,18 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
       edge[lane] = hw.edge[lane];
       loaded_hw = g.hw;
     }
-    bucket[lane].key = kEmpty;
-    bucket[lane].lid = 0xFFFFFFFFu;
+    // Buckets 0..NB-1 start empty.  Entries NB..64 are sinks: they hold key 0 and local id
+    // 0, which no configuration beats, so an infeasible configuration sent to one never
+    // takes part.
+    bucket[lane].key = lane < NB ? kEmpty : 0ull;
+    bucket[lane].lid = lane < NB ? 0xFFFFFFFFu : 0u;
+    if (lane == 0) {
+      bucket[64].key = 0ull;
+      bucket[64].lid = 0u;
+    }
     wave_sync();
 
-    const double iP = hw.iP, M = hw.M, kNB = hw.kNB;
-    const double top = (double)(NB - 1);
+    const double iP = hw.iP, kNB = hw.kNB;
     const int l = g.l;
     const int64_t ke = g.k < g.G ? g.k : g.G;
     const double Gd = (double)g.G;
@@ -420,12 +429,12 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
           const double obj = __builtin_fma(Gd, tv, d);
           const unsigned int lid = lid_oo + (unsigned int)ia;
 
-          // Feasibility (Eq. 4) and bucket j = min{j : mem <= E_j}: floor(mem * kNB) is j
-          // or j - 1 (kNB carries a 2^-40 margin), so one comparison with E settles it.
-          const bool feasible = mem <= M;
-          const int j0 = (int)__builtin_fmin(mem * kNB, top);
-          const int jb = min(j0 + (mem > edge[j0] ? 1 : 0), NB - 1);
-          const int j = feasible ? jb : 0;
+          // Bucket j = min{j : mem <= E_j}: floor(mem * kNB) is j or j - 1 (kNB carries a
+          // 2^-40 margin), so one comparison with E settles it.  An infeasible configuration
+          // (Eq. 4: mem > M = E_{NB-1}) has floor(mem * kNB) >= NB - 1 and lands on a sink:
+          // past NB - 1 the edges are +inf.
+          const int j0 = (int)__builtin_fmin(mem * kNB, 63.0);
+          BucketEntry* const be = bucket + j0 + (mem > edge[j0] ? 1 : 0);
 
           // Lexicographic (obj, id) minimum per bucket without a serial loop: the lanes that
           // beat their bucket's entry lower the objective bits with an LDS atomic minimum;
@@ -435,14 +444,14 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
           // before, so each step sees the previous one's result.
           const unsigned long long key = (unsigned long long)__double_as_longlong(obj);
           wave_sync();  // read the entry after every earlier update of the wave
-          const unsigned long long k_old = bucket[j].key;
-          const unsigned int i_old = bucket[j].lid;
-          const bool cand = feasible && (key < k_old || (key == k_old && lid < i_old));
-          if (__ballot(cand)) {
-            if (cand) atomicMin(&bucket[j].key, key);
-            const unsigned long long k_new = cand ? bucket[j].key : 0ull;
-            if (cand && k_new < k_old) bucket[j].lid = 0xFFFFFFFFu;
-            if (cand && key == k_new) atomicMin(&bucket[j].lid, lid);
+          const unsigned long long k_old = be->key;
+          const unsigned int i_old = be->lid;
+          const bool cand = (key < k_old) | ((key == k_old) & (lid < i_old));
+          if (__builtin_amdgcn_ballot_w64(cand)) {
+            if (cand) atomicMin(&be->key, key);
+            const unsigned long long k_new = cand ? be->key : 0ull;
+            if (cand && k_new < k_old) be->lid = 0xFFFFFFFFu;
+            if (cand && key == k_new) atomicMin(&be->lid, lid);
           }
         }
       }
@@ -452,6 +461,10 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
     const unsigned int bl = bucket[lane].lid;
     a.part_obj[(size_t)t * 64 + lane] = __longlong_as_double((long long)bucket[lane].key);
     a.part_id[(size_t)t * 64 + lane] = bl == 0xFFFFFFFFu ? kNone : g.base + (uint64_t)bl;
+    if (!claims) break;
+    int c = 0;
+    if (lane == 0) c = atomicAdd(a.work, 1);
+    t = n_waves + __builtin_amdgcn_readfirstlane(__shfl(c, 0, 64));
   }
 }
 
