@@ -465,43 +465,62 @@ namespace {
 
 // Tiles: contiguous strips of one group, at most strips_per_tile each (a multiple of the wave
 // width).  Every wave of the persistent evaluation grid takes tile number (its global wave
-// index) first and claims further tiles from the device counter.  A space of at most
-// kStaticStrips strips per resident wave is cut into about one tile per resident wave, so that
-// no claim is made.  A larger one is cut into tiles of at least kMinTileConfigs configurations
-// (a claim is a device-wide atomic whose latency a wave waits out, and claims on one counter
-// serialize) and at most kMaxTiles tiles (a wave that finishes last holds the kernel for up to
-// one tile).
+// index) first and claims further tiles from the device counter, in tile order.  A space of
+// at most kStaticStrips strips per resident wave is cut into about one tile per resident wave,
+// so that no claim is made.  A larger one is cut into tiles of at least kMinTileConfigs
+// configurations (claims on one counter serialize) and at most kMaxTiles tiles; the strips of
+// a group past its last full-size tile go into tiles a quarter of that size, placed after all
+// full-size tiles, so that the waves that finish last mostly wait for a small tile.
 std::string build_tiles(mist_space* S, int64_t resident_waves) {
   const uint64_t per_unit_strips = 4ull * (uint64_t)(S->R * S->R);
   uint64_t total_strips = 0;
   for (const DevGroup& g : S->groups) total_strips += (uint64_t)g.n_pairs * (uint64_t)(g.l + 1) * per_unit_strips;
   const uint64_t W = (uint64_t)std::max<int64_t>(1, resident_waves);
   const uint64_t R2 = (uint64_t)(S->R * S->R);
+  const auto align = [](uint64_t v) {
+    v = (v + kStripAlign - 1) / kStripAlign * kStripAlign;
+    if (v < (uint64_t)kStripAlign) v = kStripAlign;
+    if (v > (uint64_t)INT32_MAX / 2) v = (uint64_t)INT32_MAX / 2 / kStripAlign * kStripAlign;
+    return v;
+  };
+  const bool single = total_strips <= W * (uint64_t)kStaticStrips;
   uint64_t spt;
-  if (total_strips <= W * (uint64_t)kStaticStrips)
-    spt = (total_strips + W - 1) / W;
+  if (single)
+    spt = align((total_strips + W - 1) / W);
   else
-    spt = std::max<uint64_t>(((uint64_t)kMinTileConfigs + R2 - 1) / R2,
-                             (total_strips + (uint64_t)kMaxTiles - 1) / (uint64_t)kMaxTiles);
-  spt = (spt + kStripAlign - 1) / kStripAlign * kStripAlign;
-  if (spt < (uint64_t)kStripAlign) spt = kStripAlign;
-  if (spt > (uint64_t)INT32_MAX / 2) spt = (uint64_t)INT32_MAX / 2 / kStripAlign * kStripAlign;
+    spt = align(std::max<uint64_t>(((uint64_t)kMinTileConfigs + R2 - 1) / R2,
+                                   (total_strips + (uint64_t)kMaxTiles - 1) / (uint64_t)kMaxTiles));
+  const uint64_t spt_tail = single ? spt : align(spt / 4);
   S->strips_per_tile = (int32_t)spt;
   S->tiles.clear();
+  std::vector<DevTile> tail;
   for (size_t gi = 0; gi < S->groups.size(); ++gi) {
     DevGroup& g = S->groups[gi];
     const int64_t strips = (int64_t)g.n_pairs * (g.l + 1) * (int64_t)per_unit_strips;
+    const int64_t split = single ? strips : strips / (int64_t)spt * (int64_t)spt;
     g.tile_begin = (int32_t)S->tiles.size();
-    for (int64_t u = 0; u < strips; u += (int64_t)spt) {
+    for (int64_t u = 0; u < split; u += (int64_t)spt) {
       DevTile t{};
       t.group = (int32_t)gi;
       t.strip_begin = (int32_t)u;
-      t.strip_end = (int32_t)std::min<int64_t>(strips, u + (int64_t)spt);
+      t.strip_end = (int32_t)std::min<int64_t>(split, u + (int64_t)spt);
       S->tiles.push_back(t);
     }
     g.n_tiles = (int32_t)S->tiles.size() - g.tile_begin;
-    if (S->tiles.size() > (size_t)INT32_MAX / 2) return "too many tiles";  // + waves fits int
+    g.tail_begin = (int32_t)tail.size();  // offset into the small tiles until they are appended
+    for (int64_t u = split; u < strips; u += (int64_t)spt_tail) {
+      DevTile t{};
+      t.group = (int32_t)gi;
+      t.strip_begin = (int32_t)u;
+      t.strip_end = (int32_t)std::min<int64_t>(strips, u + (int64_t)spt_tail);
+      tail.push_back(t);
+    }
+    g.n_tail = (int32_t)tail.size() - g.tail_begin;
+    if (S->tiles.size() + tail.size() > (size_t)INT32_MAX / 2) return "too many tiles";  // + waves fits int
   }
+  const int32_t full = (int32_t)S->tiles.size();
+  for (DevGroup& g : S->groups) g.tail_begin += full;
+  S->tiles.insert(S->tiles.end(), tail.begin(), tail.end());
   return "";
 }
 

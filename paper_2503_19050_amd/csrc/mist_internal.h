@@ -20,9 +20,11 @@ struct DevGroup {
   int32_t G, PP, k, l;
   int32_t pair_begin;   // first (b, TP) pair in the pair table
   int32_t n_pairs;
-  int32_t tile_begin;   // first tile of the group in the tile table
+  int32_t tile_begin;   // first of the group's full-size tiles in the tile table
   int32_t n_tiles;
   int32_t pk_begin;     // first entry of the group's pairs in the pair-constant table
+  int32_t tail_begin;   // first of the group's small tiles (after every group's full-size ones)
+  int32_t n_tail;
 };
 
 // One (b, TP) pair of a group, DP = D / (PP * TP).

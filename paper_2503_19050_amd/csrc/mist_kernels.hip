@@ -470,8 +470,8 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
 
 // ---------------------------------------------------------------------------------------
 // K2: one wave per group; lane j owns bucket j.  Lexicographic minimum over the group's
-// tiles in tile order, then the group's best by a butterfly over the 64 lanes and the
-// staircase by an exclusive prefix minimum over the buckets.
+// tiles (its full-size ones, then its small ones), then the group's best by a butterfly
+// over the 64 lanes and the staircase by an exclusive prefix minimum over the buckets.
 // ---------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kReduceBlock) void k_reduce(ReduceArgs a) {
   const int lane = threadIdx.x & 63;
@@ -482,6 +482,14 @@ __global__ __launch_bounds__(kReduceBlock) void k_reduce(ReduceArgs a) {
   uint64_t id = kNone;
   if (lane < a.NB) {
     for (int t = grp.tile_begin; t < grp.tile_begin + grp.n_tiles; ++t) {
+      const double o = a.part_obj[(size_t)t * 64 + lane];
+      const uint64_t i = a.part_id[(size_t)t * 64 + lane];
+      if (lex_less(o, i, obj, id)) {
+        obj = o;
+        id = i;
+      }
+    }
+    for (int t = grp.tail_begin; t < grp.tail_begin + grp.n_tail; ++t) {
       const double o = a.part_obj[(size_t)t * 64 + lane];
       const uint64_t i = a.part_id[(size_t)t * 64 + lane];
       if (lex_less(o, i, obj, id)) {
