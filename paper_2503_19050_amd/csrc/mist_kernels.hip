@@ -301,16 +301,22 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
-// Waves per SIMD the register allocation aims at: the strip keeps R stable times live, so
-// large ratio counts trade a wave of occupancy for spill-free code.
+// Activation ratios per block of the strip loop: a block keeps its stable times and the
+// per-ratio terms of its configurations in registers across the optimizer ratios.
 template <int R>
-constexpr int eval_waves() { return R <= 4 ? 4 : 3; }
+constexpr int ia_block() { return R <= 6 ? R : (R + 2) / 3; }
+
+// Waves per SIMD the register allocation aims at (measured per block size: five or six
+// ratios in one block fit three waves; blocks of up to four ratios fit four).
+template <int R>
+constexpr int eval_waves() { return R <= 4 ? 4 : (R <= 6 ? 3 : 4); }
 
 template <int R>
 __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, const double* __restrict__ ratio,
                                                                  const PairK* __restrict__ pk) {
   constexpr int R2 = R * R;
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
+  constexpr int IB = ia_block<R>();
   __shared__ double s_tab[kWaves][16 * kLdsRow];
   __shared__ double s_edge[kWaves][MIST_MAX_BUCKETS];
   __shared__ BucketEntry s_bucket[kWaves][65];  // entries NB..64: sinks of infeasible configurations
@@ -377,18 +383,6 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
       const double rw = rr[iw], rg = rr[ig];
       const WoGoK W = wogo_levels(P, Z, rw, om[iw], rg, om[ig]);
 
-      // Stable time per activation ratio (it does not depend on the optimizer ratio).  With
-      // a positive activation ratio both host streams run, so the first round's pattern is
-      // compute + both host streams (+ GPU-GPU when it carries traffic).
-      double tt[R];
-      const double* es = tab + (Z.G2Gs > 0.0 ? 15 : 13) * kLdsRow;
-#pragma unroll
-      for (int ia = 0; ia < R; ++ia) {
-        const double H2Ds = __builtin_fma(rr[ia], K.A, W.HW) * iP;
-        const double D2Hs = __builtin_fma(rr[ia], K.A, W.DG) * iP;
-        if (ia == 0 && r0_zero) tt[ia] = interference(K.C, Z.G2Gs, H2Ds, D2Hs, tab);
-        else tt[ia] = interference_first(es, K.C, Z.G2Gs, H2Ds, D2Hs, tab);
-      }
       // First microbatch: every configuration of the strip with a non-zero offload ratio
       // starts with compute, both host streams and (if it carries traffic) GPU-GPU.
       const double* e1 = tab + (Z.G2Gf > 0.0 ? 15 : 13) * kLdsRow;
@@ -408,50 +402,74 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
       s_zero[tid][1] = Z.G2Gf;
       const double A = K.A, KA = K.KA, A2 = P.A2, HW = W.HW, DG = W.DG;
       const unsigned int lid_strip = (unsigned int)s * (unsigned int)R2;
+      // With a positive activation ratio both host streams run, so the stable microbatch's
+      // first round has the pattern compute + both host streams (+ GPU-GPU when it carries
+      // traffic).
+      const double* es = tab + (Z.G2Gs > 0.0 ? 15 : 13) * kLdsRow;
+
+      // Activation ratios in blocks of IB: the values a block keeps across the optimizer
+      // ratios fit the registers, at the price of one more optimizer-level evaluation per
+      // block.
+#pragma unroll
+      for (int ib = 0; ib < R; ib += IB) {
+        // Stable time per activation ratio (it does not depend on the optimizer ratio).
+        double tt[IB];
+#pragma unroll
+        for (int c = 0; c < IB; ++c) {
+          const int ia = ib + c;
+          if (ia >= R) break;
+          const double H2Ds = __builtin_fma(rr[ia], K.A, W.HW) * iP;
+          const double D2Hs = __builtin_fma(rr[ia], K.A, W.DG) * iP;
+          if (ia == 0 && r0_zero) tt[c] = interference(K.C, Z.G2Gs, H2Ds, D2Hs, tab);
+          else tt[c] = interference_first(es, K.C, Z.G2Gs, H2Ds, D2Hs, tab);
+        }
 
 #pragma unroll 1
-      for (int io = 0; io < R; ++io) {
-        const OoK O = oo_level(s_oo[tid], rr[io], om[io], iP);
-        const bool zero_oo = zero_strip && io == 0;
-        const unsigned int lid_oo = lid_strip + (unsigned int)(io * R);
+        for (int io = 0; io < R; ++io) {
+          const OoK O = oo_level(s_oo[tid], rr[io], om[io], iP);
+          const bool zero_oo = zero_strip && io == 0;
+          const unsigned int lid_oo = lid_strip + (unsigned int)(io * R);
 #pragma unroll
-        for (int ia = 0; ia < R; ++ia) {
-          const double ra = rr[ia];
-          const double SO = __builtin_fma(ra, A2, om[ia] * KA);  // stash + offload buffers
-          const double mem = O.Bmax + SO;
-          const double H2Df = __builtin_fma(ra, A, HW) * iP + O.H2Dx;
-          const double D2Hf = __builtin_fma(ra, A, DG) * iP + O.D2Hx;
-          double T1;
-          if (ia == 0 && zero_oo) T1 = interference(s_zero[tid][0], s_zero[tid][1], H2Df, D2Hf, tab);
-          else T1 = interference_strip(fr, H2Df, D2Hf, tab);
-          const double tv = tt[ia];
-          const double d = T1 - tv;
-          const double obj = __builtin_fma(Gd, tv, d);
-          const unsigned int lid = lid_oo + (unsigned int)ia;
+          for (int c = 0; c < IB; ++c) {
+            const int ia = ib + c;
+            if (ia >= R) break;
+            const double ra = rr[ia];
+            const double SO = __builtin_fma(ra, A2, om[ia] * KA);  // stash + offload buffers
+            const double mem = O.Bmax + SO;
+            const double H2Df = __builtin_fma(ra, A, HW) * iP + O.H2Dx;
+            const double D2Hf = __builtin_fma(ra, A, DG) * iP + O.D2Hx;
+            double T1;
+            if (ia == 0 && zero_oo) T1 = interference(s_zero[tid][0], s_zero[tid][1], H2Df, D2Hf, tab);
+            else T1 = interference_strip(fr, H2Df, D2Hf, tab);
+            const double tv = tt[c];
+            const double d = T1 - tv;
+            const double obj = __builtin_fma(Gd, tv, d);
+            const unsigned int lid = lid_oo + (unsigned int)ia;
 
-          // Bucket j = min{j : mem <= E_j}: floor(mem * kNB) is j or j - 1 (kNB carries a
-          // 2^-40 margin), so one comparison with E settles it.  An infeasible configuration
-          // (Eq. 4: mem > M = E_{NB-1}) has floor(mem * kNB) >= NB - 1 and lands on a sink:
-          // past NB - 1 the edges are +inf.
-          const int j0 = (int)__builtin_fmin(mem * kNB, 63.0);
-          BucketEntry* const be = bucket + j0 + (mem > edge[j0] ? 1 : 0);
+            // Bucket j = min{j : mem <= E_j}: floor(mem * kNB) is j or j - 1 (kNB carries a
+            // 2^-40 margin), so one comparison with E settles it.  An infeasible
+            // configuration (Eq. 4: mem > M = E_{NB-1}) has floor(mem * kNB) >= NB - 1 and
+            // lands on a sink: past NB - 1 the edges are +inf.
+            const int j0 = (int)__builtin_fmin(mem * kNB, 63.0);
+            BucketEntry* const be = bucket + j0 + (mem > edge[j0] ? 1 : 0);
 
-          // Lexicographic (obj, id) minimum per bucket without a serial loop: the lanes that
-          // beat their bucket's entry lower the objective bits with an LDS atomic minimum;
-          // a lane that sees its bucket's objective drop clears the id, then the lanes whose
-          // objective equals the new minimum lower the id.  The LDS operations of a wave
-          // execute in program order and each step addresses the same words as the one
-          // before, so each step sees the previous one's result.
-          const unsigned long long key = (unsigned long long)__double_as_longlong(obj);
-          wave_sync();  // read the entry after every earlier update of the wave
-          const unsigned long long k_old = be->key;
-          const unsigned int i_old = be->lid;
-          const bool cand = (key < k_old) | ((key == k_old) & (lid < i_old));
-          if (__builtin_amdgcn_ballot_w64(cand)) {
-            if (cand) atomicMin(&be->key, key);
-            const unsigned long long k_new = cand ? be->key : 0ull;
-            if (cand && k_new < k_old) be->lid = 0xFFFFFFFFu;
-            if (cand && key == k_new) atomicMin(&be->lid, lid);
+            // Lexicographic (obj, id) minimum per bucket without a serial loop: the lanes
+            // that beat their bucket's entry lower the objective bits with an LDS atomic
+            // minimum; a lane that sees its bucket's objective drop clears the id, then the
+            // lanes whose objective equals the new minimum lower the id.  The LDS operations
+            // of a wave execute in program order and each step addresses the same words as
+            // the one before, so each step sees the previous one's result.
+            const unsigned long long key = (unsigned long long)__double_as_longlong(obj);
+            wave_sync();  // read the entry after every earlier update of the wave
+            const unsigned long long k_old = be->key;
+            const unsigned int i_old = be->lid;
+            const bool cand = (key < k_old) | ((key == k_old) & (lid < i_old));
+            if (__builtin_amdgcn_ballot_w64(cand)) {
+              if (cand) atomicMin(&be->key, key);
+              const unsigned long long k_new = cand ? be->key : 0ull;
+              if (cand && k_new < k_old) be->lid = 0xFFFFFFFFu;
+              if (cand && key == k_new) atomicMin(&be->lid, lid);
+            }
           }
         }
       }
