@@ -35,6 +35,7 @@ constexpr int64_t kStaticStrips = 512;        // strips per resident wave up to 
                                               // cut into one tile per wave
 constexpr int64_t kMinTileConfigs = 8192;     // configurations per tile of a larger space, at least
 constexpr int64_t kMaxTiles = 131072;         // and tiles per space, at most
+constexpr int64_t kTailPercent = 10;          // share of each group's strips in small tiles
 constexpr int64_t kStripAlign = kWaveTile;    // strips per tile: a multiple of the wave
 
 int popcount4(int v) { return (v & 1) + ((v >> 1) & 1) + ((v >> 2) & 1) + ((v >> 3) & 1); }
@@ -468,9 +469,10 @@ namespace {
 // index) first and claims further tiles from the device counter, in tile order.  A space of
 // at most kStaticStrips strips per resident wave is cut into about one tile per resident wave,
 // so that no claim is made.  A larger one is cut into tiles of at least kMinTileConfigs
-// configurations (claims on one counter serialize) and at most kMaxTiles tiles; the strips of
-// a group past its last full-size tile go into tiles a quarter of that size, placed after all
-// full-size tiles, so that the waves that finish last mostly wait for a small tile.
+// configurations (claims on one counter serialize) and at most kMaxTiles tiles; the last
+// kTailPercent percent of a group's strips (rounded up to its last full-size tile) go into
+// tiles a quarter of that size, placed after all full-size tiles, so that the waves that
+// finish last wait for a small tile.
 std::string build_tiles(mist_space* S, int64_t resident_waves) {
   const uint64_t per_unit_strips = 4ull * (uint64_t)(S->R * S->R);
   uint64_t total_strips = 0;
@@ -497,7 +499,7 @@ std::string build_tiles(mist_space* S, int64_t resident_waves) {
   for (size_t gi = 0; gi < S->groups.size(); ++gi) {
     DevGroup& g = S->groups[gi];
     const int64_t strips = (int64_t)g.n_pairs * (g.l + 1) * (int64_t)per_unit_strips;
-    const int64_t split = single ? strips : strips / (int64_t)spt * (int64_t)spt;
+    const int64_t split = single ? strips : strips * (100 - kTailPercent) / 100 / (int64_t)spt * (int64_t)spt;
     g.tile_begin = (int32_t)S->tiles.size();
     for (int64_t u = 0; u < split; u += (int64_t)spt) {
       DevTile t{};
@@ -584,7 +586,7 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
     if (!rc) rc = upload(S, &S->d_pk_group, S->pk_group, "pair groups");
     if (!rc) {
       S->d_pk = (PairK*)dev_alloc(S, S->pk_group.size() * sizeof(PairK));
-      S->d_work = (int32_t*)dev_alloc(S, sizeof(int32_t));
+      S->d_work = (int32_t*)dev_alloc(S, sizeof(int32_t) * kClaimCounters * kCounterStride);
       if (!S->d_pk || !S->d_work) rc = fail(MIST_E_NOMEM, "device allocation failed: pair constants");
     }
     const size_t nt = S->tiles.size(), ng = S->groups.size();

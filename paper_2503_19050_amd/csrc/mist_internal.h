@@ -12,6 +12,8 @@ constexpr int kWaves = kBlock / 64;   // wave64
 constexpr int kWaveTile = 64;         // threads per tile: each wave works on its own tiles
 constexpr int kReduceBlock = 256;     // group-reduction block: one wave per group
 constexpr int kTabStride = 8;         // interference table row: phi[4], psi[4]
+constexpr int kClaimCounters = 8;     // tile counters: one per XCD (blocks are dealt in turn)
+constexpr int kCounterStride = 64;    // ints between counters (separate cache lines)
 
 // One candidate stage (group): hardware sample, G, PP, in-flight count k, layers l.
 struct DevGroup {
@@ -85,7 +87,8 @@ struct EvalArgs {
   const double* ratio;   // r[0..R), then om[0..R) = 1 - r
   int32_t R, NB;
   int32_t n_tiles;
-  int32_t* work;         // tile counter of the persistent evaluation kernel (reset by K0)
+  int32_t* work;         // tile counters of the persistent evaluation kernel, kClaimCounters
+                         // of them kCounterStride apart (reset by K0)
   int64_t n_groups;
   uint64_t n_configs;
   double* part_obj;      // [n_tiles][64]

@@ -264,7 +264,8 @@ __device__ __forceinline__ double interference_strip(const FirstRow& r, double h
 // K0: pair-level constants of every (group, pair).
 __global__ __launch_bounds__(256) void k_pairs(EvalArgs a) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i == 0) *a.work = 0;  // the evaluation kernel's tile counter (it runs after this kernel)
+  if (i < kClaimCounters) a.work[i * kCounterStride] = 0;  // the evaluation kernel's tile
+                                                           // counters (it runs after this one)
   if (i >= a.n_pk) return;
   const DevGroup g = a.groups[a.pk_group[i]];
   const int p = i - g.pk_begin;
@@ -306,10 +307,10 @@ __device__ __forceinline__ void wave_sync() {
 template <int R>
 constexpr int ia_block() { return R <= 6 ? R : (R + 2) / 3; }
 
-// Waves per SIMD the register allocation aims at (measured per block size: five or six
-// ratios in one block fit three waves; blocks of up to four ratios fit four).
+// Waves per SIMD the register allocation aims at: four, the most the LDS use of a block
+// allows (a few strip-level values spill; the occupancy is worth more).
 template <int R>
-constexpr int eval_waves() { return R <= 4 ? 4 : (R <= 6 ? 3 : 4); }
+constexpr int eval_waves() { return 4; }
 
 template <int R>
 __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, const double* __restrict__ ratio,
@@ -335,11 +336,15 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
   BucketEntry* bucket = s_bucket[wave];
   const unsigned long long kEmpty = (unsigned long long)__double_as_longlong(__builtin_huge_val());
 
-  // Tile schedule: wave w of the grid takes tile w, then tiles n_waves + c for the claim
-  // numbers c it draws from the device counter (reset to 0 by K0), until they run out.  When
-  // the grid has at least as many waves as there are tiles no claim is made.
+  // Tile schedule: wave w of the grid takes tile w.  Tile n_waves + x + kClaimCounters * c
+  // goes to the claim that draws number c from counter x (counters reset to 0 by K0); a wave
+  // draws from the counter of its block's XCD and moves to the next counter when one runs
+  // out, until all have.  When the grid has at least as many waves as there are tiles no
+  // claim is made.
   const int n_waves = (int)gridDim.x * kWaves;
   const bool claims = a.n_tiles > n_waves;
+  int counter = (int)(blockIdx.x % kClaimCounters);
+  int exhausted = 0;
   int loaded_hw = -1;
   for (int t = (int)blockIdx.x * kWaves + wave; t < a.n_tiles;) {
     const DevTile tile = a.tiles[t];
@@ -480,9 +485,21 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
     a.part_obj[(size_t)t * 64 + lane] = __longlong_as_double((long long)bucket[lane].key);
     a.part_id[(size_t)t * 64 + lane] = bl == 0xFFFFFFFFu ? kNone : g.base + (uint64_t)bl;
     if (!claims) break;
-    int c = 0;
-    if (lane == 0) c = atomicAdd(a.work, 1);
-    t = n_waves + __builtin_amdgcn_readfirstlane(__shfl(c, 0, 64));
+    for (;;) {
+      int c = 0;
+      if (lane == 0) c = atomicAdd(a.work + counter * kCounterStride, 1);
+      c = __builtin_amdgcn_readfirstlane(__shfl(c, 0, 64));
+      const int64_t next = (int64_t)n_waves + counter + (int64_t)kClaimCounters * c;
+      if (next < a.n_tiles) {
+        t = (int)next;
+        break;
+      }
+      if (++exhausted == kClaimCounters) {  // every counter has run out: no tile is left
+        t = a.n_tiles;
+        break;
+      }
+      counter = counter + 1 == kClaimCounters ? 0 : counter + 1;
+    }
   }
 }
 
