@@ -292,7 +292,10 @@ struct BucketEntry {
                            // its bit pattern)
   unsigned int lid;        // lowest local id (id - group base, < 2^32) reaching it
   unsigned int pad;
+  double edge;             // the bucket's upper memory edge E_j (+inf past NB - 1): one
+                           // address serves the edge test and the entry
 };
+static_assert(sizeof(BucketEntry) == 24, "24-byte entries: the entry offset is one multiply-add");
 
 // Orders this wave's LDS accesses for the compiler: a lane may read a word another lane of
 // the same wave wrote (the hardware executes a wave's LDS operations in order), so no load
@@ -319,7 +322,6 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
   constexpr int IB = ia_block<R>();
   __shared__ double s_tab[kWaves][16 * kLdsRow];
-  __shared__ double s_edge[kWaves][MIST_MAX_BUCKETS];
   __shared__ BucketEntry s_bucket[kWaves][65];  // entries NB..64: sinks of infeasible configurations
   __shared__ OoIn s_oo[kBlock];         // per-lane strip constants of the optimizer level
   __shared__ double s_zero[kBlock][2];  // per-lane C and G2G (first microbatch) of the strip
@@ -332,7 +334,6 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
   const double* __restrict__ om = ratio + R;
   const bool r0_zero = rr[0] == 0.0;
   double* tab = s_tab[wave];
-  double* edge = s_edge[wave];
   BucketEntry* bucket = s_bucket[wave];
   const unsigned long long kEmpty = (unsigned long long)__double_as_longlong(__builtin_huge_val());
 
@@ -353,7 +354,7 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
     if (g.hw != loaded_hw) {  // the wave's LDS copy of the hardware tables
       for (int i = lane; i < 16 * kTabStride; i += 64)
         tab[(i / kTabStride) * kLdsRow + i % kTabStride] = (&hw.itab[0][0])[i];
-      edge[lane] = hw.edge[lane];
+      bucket[lane].edge = hw.edge[lane];
       loaded_hw = g.hw;
     }
     // Buckets 0..NB-1 start empty.  Entries NB..64 are sinks: they hold key 0 and local id
@@ -449,14 +450,16 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
             const double tv = tt[c];
             const double d = T1 - tv;
             const double obj = __builtin_fma(Gd, tv, d);
-            const unsigned int lid = lid_oo + (unsigned int)ia;
 
             // Bucket j = min{j : mem <= E_j}: floor(mem * kNB) is j or j - 1 (kNB carries a
             // 2^-40 margin), so one comparison with E settles it.  An infeasible
             // configuration (Eq. 4: mem > M = E_{NB-1}) has floor(mem * kNB) >= NB - 1 and
             // lands on a sink: past NB - 1 the edges are +inf.
             const int j0 = (int)__builtin_fmin(mem * kNB, 63.0);
-            BucketEntry* const be = bucket + j0 + (mem > edge[j0] ? 1 : 0);
+            const unsigned int off0 = __umul24((unsigned int)j0, (unsigned int)sizeof(BucketEntry));
+            char* const b0 = reinterpret_cast<char*>(bucket) + off0;
+            const double e0 = reinterpret_cast<const BucketEntry*>(b0)->edge;
+            BucketEntry* const be = reinterpret_cast<BucketEntry*>(b0 + (mem > e0 ? sizeof(BucketEntry) : 0));
 
             // Lexicographic (obj, id) minimum per bucket without a serial loop: the lanes
             // that beat their bucket's entry lower the objective bits with an LDS atomic
@@ -467,9 +470,12 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
             const unsigned long long key = (unsigned long long)__double_as_longlong(obj);
             wave_sync();  // read the entry after every earlier update of the wave
             const unsigned long long k_old = be->key;
-            const unsigned int i_old = be->lid;
-            const bool cand = (key < k_old) | ((key == k_old) & (lid < i_old));
-            if (__builtin_amdgcn_ballot_w64(cand)) {
+            // A candidate beats the entry: key < k_old, or an equal key with a lower id.  No
+            // lane with key > k_old is one, so the exact test waits for a lane with key <= k_old.
+            if (__builtin_amdgcn_ballot_w64(key <= k_old)) {
+              const unsigned int lid = lid_oo + (unsigned int)ia;
+              const unsigned int i_old = be->lid;
+              const bool cand = (key < k_old) | ((key == k_old) & (lid < i_old));
               if (cand) atomicMin(&be->key, key);
               const unsigned long long k_new = cand ? be->key : 0ull;
               if (cand && k_new < k_old) be->lid = 0xFFFFFFFFu;
