@@ -56,6 +56,7 @@ typedef int32_t mist_status;
 #define MIST_L_BALANCED 1 /* stage layer counts floor(L/PP) and ceil(L/PP) */
 
 #define MIST_MAX_BUCKETS 64
+#define MIST_MAX_ALPHAS 16
 #define MIST_MAX_RATIOS 16
 #define MIST_MAX_MB 16
 #define MIST_NONE UINT64_MAX /* id of an empty bucket or of a group with no feasible config */
@@ -100,6 +101,9 @@ typedef struct mist_space_desc {
   int32_t n_ratios;      /* R, 1..MIST_MAX_RATIOS */
   int32_t n_buckets;     /* NB, 1..MIST_MAX_BUCKETS; bucket edges E_j = M*(j+1)/NB */
   int32_t l_rule;        /* MIST_L_FULL or MIST_L_BALANCED */
+  int32_t n_alphas;      /* 0..MIST_MAX_ALPHAS weight samples of Eq. 4; 0 (or a zeroed tail of
+                            the struct) turns the weight-sampled argmins off */
+  const double* alphas;  /* host: the samples alpha_a in [0, 1] (any order, repeats allowed) */
 } mist_space_desc;
 
 /* Device memory provider, e.g. PyTorch's caching allocator.  alloc returns NULL on
@@ -164,6 +168,15 @@ mist_status mist_get_best(mist_space* S, int64_t g0, int64_t n, mist_result* out
 mist_status mist_get_pareto(mist_space* S, int64_t g, mist_result* out, int32_t cap,
                             int32_t* n_out);
 
+/* Eq. 4 with sampled weights (Sec. 5.3, the intra-stage (t, d) frontier): waits for the last
+ * evaluation and writes, for groups g0..g0+n-1 and each weight sample alpha_a of the space,
+ * the feasible configuration minimising fma(alpha_a*G, t, (1-alpha_a)*d) (alpha_a*G and
+ * 1-alpha_a each rounded once; lowest id among equal values) into host out[i*A + a], A =
+ * n_alphas; obj holds that weighted value (+inf and id MIST_NONE when the group has no
+ * feasible configuration).  Errors: MIST_E_STATE (no samples, or no evaluation yet),
+ * MIST_E_RANGE, MIST_E_DEVICE. */
+mist_status mist_get_alpha(mist_space* S, int64_t g0, int64_t n, mist_result* out);
+
 /* Raw per-bucket table of groups g0..g0+n-1: host ids[n*NB] and objs[n*NB] (MIST_NONE /
  * +inf for empty buckets) and host frontier masks[n] (bit j = bucket j on the staircase);
  * any output pointer may be NULL.  Waits for the last evaluation.  Errors as get_best. */
@@ -196,9 +209,9 @@ mist_status mist_eval_ids(mist_space* S, const uint64_t* ids, int64_t n, double*
 mist_status mist_set_timing(mist_space* S, int32_t on);
 mist_status mist_read_timing(mist_space* S, double* eval_ms, double* reduce_ms, int64_t* n_evals);
 
-/* Launch geometry of the evaluation kernel: tiles (blocks), threads per block, strips per
- * tile (a strip is the R^2 configurations sharing pair, recomputed layers, ZeRO level,
- * weight and gradient ratios). */
+/* Launch geometry of the evaluation kernel: tiles (work items, one wave each), threads per
+ * tile, strips per full-size tile (a strip is the R^2 configurations sharing pair,
+ * recomputed layers, ZeRO level, weight and gradient ratios). */
 mist_status mist_launch_info(const mist_space* S, int64_t* n_tiles, int32_t* block,
                              int32_t* strips_per_tile);
 

@@ -738,6 +738,46 @@ int orc_run(const Model* m, const Hw* hw, int32_t n_hw, const Space* s, int64_t 
   return 0;
 }
 
+// Eq. 4 with sampled weights (Sec. 5.3): for each sample alpha_a, the feasible
+// configuration of the group that minimises alpha_a * G * t + (1 - alpha_a) * d, the
+// lowest id among equal values.  The value is fma(alpha_a * G, t, (1 - alpha_a) * d), with
+// alpha_a * G (per group) and 1 - alpha_a (per sample) each rounded once.  A group with no
+// feasible configuration gets UINT64_MAX and +inf.  Outputs are [g1 - g0][n_alpha].
+int orc_run_alpha(const Model* m, const Hw* hw, int32_t n_hw, const Space* s, const double* alphas,
+                  int32_t n_alpha, int64_t g0, int64_t g1, uint64_t* out_id, double* out_obj) {
+  Ctx X;
+  if (!build_ctx(X, m, hw, n_hw, s)) return -1;
+  if (g0 < 0 || g1 < g0 || g1 > (int64_t)X.groups.size()) return -5;
+  if (n_alpha < 1 || n_alpha > 16) return -1;
+  for (int32_t a = 0; a < n_alpha; ++a)
+    if (!(alphas[a] >= 0.0 && alphas[a] <= 1.0)) return -1;
+  const double inf = std::numeric_limits<double>::infinity();
+  std::vector<double> beta(n_alpha), aG(n_alpha);
+  for (int32_t a = 0; a < n_alpha; ++a) beta[a] = 1.0 - alphas[a];
+  for (int64_t gi = g0; gi < g1; ++gi) {
+    const Group& g = X.groups[gi];
+    const int64_t o = gi - g0;
+    for (int32_t a = 0; a < n_alpha; ++a) {
+      aG[a] = alphas[a] * exact(g.G);
+      out_id[o * n_alpha + a] = UINT64_MAX;
+      out_obj[o * n_alpha + a] = inf;
+    }
+    walk_group<double>(X, g, full_box(X, g), nullptr, [&](int64_t local, double t, double d, double mem, double obj) {
+      check_values(t, d, mem, obj);
+      if (bucket_of(X, g.hw, mem) < 0) return;  // Eq. 4 constraint: mem <= budget
+      const uint64_t id = g.base + (uint64_t)local;
+      for (int32_t a = 0; a < n_alpha; ++a) {
+        const double v = std::fma(aG[a], t, beta[a] * d);
+        if (lex_less(v, id, out_obj[o * n_alpha + a], out_id[o * n_alpha + a])) {
+          out_obj[o * n_alpha + a] = v;
+          out_id[o * n_alpha + a] = id;
+        }
+      }
+    });
+  }
+  return 0;
+}
+
 // FP64 operations of the definition over groups [g0, g1), counted by running
 // the same templates on the counting type.
 int orc_count_flops(const Model* m, const Hw* hw, int32_t n_hw, const Space* s, int64_t g0, int64_t g1,

@@ -63,6 +63,8 @@ def lib() -> ctypes.CDLL:
                                          P(ctypes.c_uint64), P(ctypes.c_double), P(ctypes.c_uint64)]
             L.orc_count_flops.argtypes = args + [ctypes.c_int64, ctypes.c_int64, P(ctypes.c_uint64),
                                                  P(ctypes.c_uint64)]
+            L.orc_run_alpha.argtypes = args + [P(ctypes.c_double), ctypes.c_int32, ctypes.c_int64,
+                                               ctypes.c_int64, P(ctypes.c_uint64), P(ctypes.c_double)]
             L.orc_interference.argtypes = [P(ctypes.c_double), P(ctypes.c_double)]
             L.orc_interference.restype = ctypes.c_double
             _lib = L
@@ -190,6 +192,17 @@ class Oracle:
                                    _up(res["bucket_id"]), _dp(res["bucket_obj"]), _up(res["frontier"])))
         return res
 
+    def run_alpha(self, alphas, g0: int = 0, g1: int | None = None) -> dict:
+        """Per group and weight sample alpha: the feasible configuration minimising
+        alpha*G*t + (1-alpha)*d (Eq. 4), lowest id on ties: {"id", "obj"} of shape [n, A]."""
+        g1 = self.n_groups if g1 is None else g1
+        al = np.ascontiguousarray(alphas, dtype=np.float64)
+        n = g1 - g0
+        res = {"id": np.empty((n, len(al)), dtype=np.uint64), "obj": np.empty((n, len(al)), dtype=np.float64)}
+        self._check(self.L.orc_run_alpha(*self._args(), _dp(al), len(al), g0, g1, _up(res["id"]),
+                                         _dp(res["obj"])))
+        return res
+
     def count_flops(self, g0: int = 0, g1: int | None = None) -> tuple[int, int]:
         g1 = self.n_groups if g1 is None else g1
         f = ctypes.c_uint64()
@@ -219,6 +232,27 @@ def _worker_init(wl):
 def _worker_run(rng):
     g0, g1 = rng
     return g0, _worker_oracle.run(g0, g1)
+
+
+def _worker_run_alpha(job):
+    alphas, g0, g1 = job
+    return g0, _worker_oracle.run_alpha(alphas, g0, g1)
+
+
+def run_alpha_groups(wl: dict, alphas, groups, procs: int = 1) -> dict:
+    """Oracle.run_alpha on the listed group indices; arrays in that order."""
+    groups = [int(g) for g in groups]
+    alphas = [float(a) for a in alphas]
+    if procs <= 1:
+        o = Oracle(wl)
+        parts = [(g, o.run_alpha(alphas, g, g + 1)) for g in groups]
+    else:
+        import multiprocessing as mp
+        ctx = mp.get_context("spawn")
+        with ctx.Pool(procs, initializer=_worker_init, initargs=(wl,)) as pool:
+            parts = pool.map(_worker_run_alpha, [(alphas, g, g + 1) for g in groups], chunksize=1)
+    by = dict(parts)
+    return {k: np.concatenate([by[g][k] for g in groups]) for k in ("id", "obj")}
 
 
 def run_groups(wl: dict, groups, procs: int = 1) -> dict:

@@ -79,6 +79,15 @@ struct mist_space {
   double* d_best_obj = nullptr;
   uint64_t* d_best_id = nullptr;
   uint64_t* d_frontier = nullptr;
+  // weight samples of Eq. 4 (A = 0: off)
+  int32_t A = 0;
+  std::vector<double> alphas, betas;  // alpha_a and 1 - alpha_a
+  double* d_alpha = nullptr;
+  double* d_beta = nullptr;
+  double* d_part_aobj = nullptr;
+  uint64_t* d_part_aid = nullptr;
+  double* d_alpha_obj = nullptr;
+  uint64_t* d_alpha_id = nullptr;
   // state
   bool evaluated = false;
   hipStream_t stream = nullptr;
@@ -166,6 +175,10 @@ std::string validate(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n
       return "ratios must be strictly ascending in [0, 1]";
   if (s->n_buckets < 1 || s->n_buckets > MIST_MAX_BUCKETS) return "n_buckets out of range";
   if (s->l_rule != MIST_L_FULL && s->l_rule != MIST_L_BALANCED) return "unknown l_rule";
+  if (s->n_alphas < 0 || s->n_alphas > MIST_MAX_ALPHAS || (s->n_alphas > 0 && !s->alphas))
+    return "n_alphas out of range";
+  for (int32_t i = 0; i < s->n_alphas; ++i)
+    if (!(s->alphas[i] >= 0.0 && s->alphas[i] <= 1.0)) return "weight samples must lie in [0, 1]";
   return "";
 }
 
@@ -369,6 +382,11 @@ mist::EvalArgs eval_args(const mist_space* S) {
   a.pk_group = S->d_pk_group;
   a.n_pk = (int32_t)S->pk_group.size();
   a.work = S->d_work;
+  a.n_alpha = S->A;
+  a.alpha = S->d_alpha;
+  a.beta = S->d_beta;
+  a.part_aobj = S->d_part_aobj;
+  a.part_aid = S->d_part_aid;
   return a;
 }
 
@@ -550,6 +568,9 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
     S->l_rule = s->l_rule;
     S->ratio_om.assign(s->ratios, s->ratios + s->n_ratios);
     for (int32_t i = 0; i < s->n_ratios; ++i) S->ratio_om.push_back(1.0 - s->ratios[i]);
+    S->A = s->n_alphas;
+    S->alphas.assign(s->alphas, s->alphas + s->n_alphas);
+    for (int32_t i = 0; i < s->n_alphas; ++i) S->betas.push_back(1.0 - s->alphas[i]);
     if (alloc) {
       S->alloc = *alloc;
       S->custom_alloc = true;
@@ -567,7 +588,7 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
       hipError_t e = hipGetDevice(&dev);
       if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
       if (e != hipSuccess) rc = fail_hip(e, "device attributes");
-      const int per_cu = eval_blocks_per_cu(S->R);
+      const int per_cu = eval_blocks_per_cu(S->R, S->A > 0);
       resident_blocks = std::max<int64_t>(1, (int64_t)cus * (per_cu > 0 ? per_cu : 1));
     }
     if (!rc) {
@@ -584,6 +605,8 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
     if (!rc) rc = upload(S, &S->d_hws, S->hws, "hardware tables");
     if (!rc) rc = upload(S, &S->d_ratio, S->ratio_om, "ratios");
     if (!rc) rc = upload(S, &S->d_pk_group, S->pk_group, "pair groups");
+    if (!rc && S->A > 0) rc = upload(S, &S->d_alpha, S->alphas, "weight samples");
+    if (!rc && S->A > 0) rc = upload(S, &S->d_beta, S->betas, "weight samples");
     if (!rc) {
       S->d_pk = (PairK*)dev_alloc(S, S->pk_group.size() * sizeof(PairK));
       S->d_work = (int32_t*)dev_alloc(S, sizeof(int32_t) * kClaimCounters * kCounterStride);
@@ -601,6 +624,15 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
       if (!S->d_part_obj || !S->d_part_id || !S->d_bucket_obj || !S->d_bucket_id || !S->d_best_obj ||
           !S->d_best_id || !S->d_frontier)
         rc = fail(MIST_E_NOMEM, "device allocation failed: results");
+    }
+    if (!rc && S->A > 0) {
+      const size_t A = (size_t)S->A;
+      S->d_part_aobj = (double*)dev_alloc(S, nt * A * sizeof(double));
+      S->d_part_aid = (uint64_t*)dev_alloc(S, nt * A * sizeof(uint64_t));
+      S->d_alpha_obj = (double*)dev_alloc(S, ng * A * sizeof(double));
+      S->d_alpha_id = (uint64_t*)dev_alloc(S, ng * A * sizeof(uint64_t));
+      if (!S->d_part_aobj || !S->d_part_aid || !S->d_alpha_obj || !S->d_alpha_id)
+        rc = fail(MIST_E_NOMEM, "device allocation failed: weight-sample results");
     }
     if (rc) {
       dev_free_all(S);
@@ -652,6 +684,11 @@ mist_status mist_eval_space(mist_space* S, void* hip_stream) {
   r.best_obj = S->d_best_obj;
   r.best_id = S->d_best_id;
   r.frontier = S->d_frontier;
+  r.n_alpha = S->A;
+  r.part_aobj = S->d_part_aobj;
+  r.part_aid = S->d_part_aid;
+  r.alpha_obj = S->d_alpha_obj;
+  r.alpha_id = S->d_alpha_id;
   rc = launch_reduce(r, st);
   if (rc) return fail_hip((hipError_t)rc, "reduction kernel launch");
   if (ev) {
@@ -677,6 +714,56 @@ mist_status mist_get_best(mist_space* S, int64_t g0, int64_t n, mist_result* out
       e = hipMemcpy(objs.data(), S->d_best_obj + g0, n * sizeof(double), hipMemcpyDeviceToHost);
     if (e != hipSuccess) return fail_hip(e, "hipMemcpy best");
     return fill_results(S, ids.data(), objs.data(), n, out);
+  } catch (const std::bad_alloc&) {
+    return fail(MIST_E_NOMEM, "host allocation failed");
+  }
+}
+
+mist_status mist_get_alpha(mist_space* S, int64_t g0, int64_t n, mist_result* out) {
+  if (!S || (!out && n > 0)) return fail(MIST_E_INVALID, "null argument");
+  if (S->A == 0) return fail(MIST_E_STATE, "the space has no weight samples");
+  if (g0 < 0 || n < 0 || g0 + n > (int64_t)S->groups.size()) return fail(MIST_E_RANGE, "group range");
+  mist_status rc = wait_results(S);
+  if (rc) return rc;
+  if (n == 0) return MIST_OK;
+  try {
+    const size_t A = (size_t)S->A, m = (size_t)n * A;
+    std::vector<uint64_t> ids(m);
+    std::vector<double> objs(m);
+    hipError_t e = hipMemcpy(ids.data(), S->d_alpha_id + (size_t)g0 * A, m * sizeof(uint64_t),
+                             hipMemcpyDeviceToHost);
+    if (e == hipSuccess)
+      e = hipMemcpy(objs.data(), S->d_alpha_obj + (size_t)g0 * A, m * sizeof(double), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpy weight-sample results");
+    std::vector<uint64_t> want;
+    for (size_t i = 0; i < m; ++i)
+      if (ids[i] != MIST_NONE) want.push_back(ids[i]);
+    std::vector<double> vals(want.size() * 4);
+    rc = eval_ids_impl(S, want.data(), (int64_t)want.size(), vals.data(), S->stream);
+    if (rc) return rc;
+    size_t w = 0;
+    for (size_t i = 0; i < m; ++i) {
+      mist_result& r = out[i];
+      std::memset(&r, 0, sizeof(r));
+      r.id = ids[i];
+      r.obj = objs[i];
+      if (ids[i] == MIST_NONE) {
+        r.t = r.d = r.mem = std::numeric_limits<double>::infinity();
+        r.bucket = -1;
+        r.cfg.hw = -1;
+        continue;
+      }
+      r.t = vals[4 * w + 0];
+      r.d = vals[4 * w + 1];
+      r.mem = vals[4 * w + 2];
+      ++w;
+      decode_host(S, r.id, &r.cfg);
+      const size_t a = i % A;
+      const double v = std::fma(S->alphas[a] * (double)r.cfg.G, r.t, S->betas[a] * r.d);
+      if (v != r.obj) return fail(MIST_E_DEVICE, "re-evaluated weighted objective differs");
+      r.bucket = bucket_host(S, S->hws[r.cfg.hw], r.mem);
+    }
+    return MIST_OK;
   } catch (const std::bad_alloc&) {
     return fail(MIST_E_NOMEM, "host allocation failed");
   }

@@ -14,6 +14,7 @@ constexpr int kReduceBlock = 256;     // group-reduction block: one wave per gro
 constexpr int kTabStride = 8;         // interference table row: phi[4], psi[4]
 constexpr int kClaimCounters = 8;     // tile counters: one per XCD (blocks are dealt in turn)
 constexpr int kCounterStride = 64;    // ints between counters (separate cache lines)
+constexpr int kMaxAlphas = 16;        // weight samples of the (t, d) frontier
 
 // One candidate stage (group): hardware sample, G, PP, in-flight count k, layers l.
 struct DevGroup {
@@ -96,6 +97,13 @@ struct EvalArgs {
   PairK* pk;             // [n_pk] pair constants, group-major
   const int32_t* pk_group;  // [n_pk] group of each entry
   int32_t n_pk;
+  // Weight samples of Eq. 4 (n_alpha = 0: off): alpha[a] and 1 - alpha[a], and the per-tile
+  // argmin of fma(alpha*G, t, (1-alpha)*d) over feasible configurations.
+  int32_t n_alpha;
+  const double* alpha;   // [n_alpha]
+  const double* beta;    // [n_alpha]
+  double* part_aobj;     // [n_tiles][n_alpha]
+  uint64_t* part_aid;    // [n_tiles][n_alpha]
 };
 
 struct ReduceArgs {
@@ -109,12 +117,17 @@ struct ReduceArgs {
   double* best_obj;      // [n_groups]
   uint64_t* best_id;     // [n_groups]
   uint64_t* frontier;    // [n_groups]
+  int32_t n_alpha;
+  const double* part_aobj;
+  const uint64_t* part_aid;
+  double* alpha_obj;     // [n_groups][n_alpha]
+  uint64_t* alpha_id;    // [n_groups][n_alpha]
 };
 
 // Kernel launchers (mist_kernels.hip).
 int launch_pairs(const EvalArgs& a, void* stream);
 int launch_eval(const EvalArgs& a, int blocks, void* stream);
-int eval_blocks_per_cu(int R);
+int eval_blocks_per_cu(int R, bool alpha);
 int launch_reduce(const ReduceArgs& a, void* stream);
 int launch_eval_ids(const EvalArgs& a, const uint64_t* ids, int64_t n, double* out, void* stream);
 

@@ -297,6 +297,22 @@ struct BucketEntry {
 };
 static_assert(sizeof(BucketEntry) == 24, "24-byte entries: the entry offset is one multiply-add");
 
+// Weight-sampled argmin (Eq. 4 with sampled alpha) of the wave's current tile: the value
+// (a double, for the fast comparison), its order key (for the LDS atomic minimum; weighted
+// values may be negative) and the lowest local id reaching it.
+struct AlphaEntry {
+  double val;
+  unsigned long long key;
+  unsigned int lid;
+  unsigned int pad;
+};
+
+// A 64-bit key that orders like the double (neither -0 nor NaN occurs as a key).
+__device__ __forceinline__ unsigned long long order_key(double v) {
+  const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+  return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
+}
+
 // Orders this wave's LDS accesses for the compiler: a lane may read a word another lane of
 // the same wave wrote (the hardware executes a wave's LDS operations in order), so no load
 // may be moved across this point or answered from the lane's own earlier store.
@@ -315,7 +331,8 @@ constexpr int ia_block() { return R <= 6 ? R : (R + 2) / 3; }
 template <int R>
 constexpr int eval_waves() { return 4; }
 
-template <int R>
+// AL: also the weight-sampled argmins of Eq. 4 (a.n_alpha samples).
+template <int R, bool AL>
 __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, const double* __restrict__ ratio,
                                                                  const PairK* __restrict__ pk) {
   constexpr int R2 = R * R;
@@ -325,6 +342,8 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
   __shared__ BucketEntry s_bucket[kWaves][65];  // entries NB..64: sinks of infeasible configurations
   __shared__ OoIn s_oo[kBlock];         // per-lane strip constants of the optimizer level
   __shared__ double s_zero[kBlock][2];  // per-lane C and G2G (first microbatch) of the strip
+  __shared__ double2 s_ab[AL ? kWaves : 1][kMaxAlphas];      // alpha * G, 1 - alpha
+  __shared__ AlphaEntry s_aent[AL ? kWaves : 1][kMaxAlphas];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -366,12 +385,20 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
       bucket[64].key = 0ull;
       bucket[64].lid = 0u;
     }
+    const double Gd = (double)g.G;
+    if constexpr (AL) {
+      if (lane < a.n_alpha) {
+        s_ab[wave][lane] = make_double2(a.alpha[lane] * Gd, a.beta[lane]);
+        s_aent[wave][lane].val = __builtin_huge_val();
+        s_aent[wave][lane].key = order_key(__builtin_huge_val());
+        s_aent[wave][lane].lid = 0xFFFFFFFFu;
+      }
+    }
     wave_sync();
 
-    const double iP = hw.iP, kNB = hw.kNB;
+    const double iP = hw.iP, kNB = hw.kNB, M = hw.M;
     const int l = g.l;
     const int64_t ke = g.k < g.G ? g.k : g.G;
-    const double Gd = (double)g.G;
 
 #pragma unroll 1
     for (int s = tile.strip_begin + lane; s < tile.strip_end; s += 64) {
@@ -481,6 +508,36 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
               if (cand && k_new < k_old) be->lid = 0xFFFFFFFFu;
               if (cand && key == k_new) atomicMin(&be->lid, lid);
             }
+
+            if constexpr (AL) {
+              // Eq. 4 for every weight sample, feasible configurations only: an infeasible
+              // one carries a NaN delta, so each of its weighted values is NaN and compares
+              // false.  All lanes address the sample's single entry; the same three-step
+              // LDS sequence keeps the lexicographic minimum.
+              const double dn = mem <= M ? d : __builtin_nan("");
+#pragma unroll 1
+              for (int q = 0; q < a.n_alpha; ++q) {
+                const double2 ab = s_ab[wave][q];
+                const double v = __builtin_fma(ab.x, tv, ab.y * dn);
+                AlphaEntry* const e = &s_aent[wave][q];
+                wave_sync();
+                const double cur = e->val;
+                if (__builtin_amdgcn_ballot_w64(v <= cur)) {
+                  const unsigned int lid = lid_oo + (unsigned int)ia;
+                  const unsigned long long ak = order_key(v);
+                  const unsigned long long ak_old = e->key;
+                  const unsigned int ai_old = e->lid;
+                  const bool cand = (v <= cur) & ((ak < ak_old) | ((ak == ak_old) & (lid < ai_old)));
+                  if (cand) atomicMin(&e->key, ak);
+                  const unsigned long long ak_new = cand ? e->key : 0ull;
+                  if (cand && ak_new < ak_old) e->lid = 0xFFFFFFFFu;
+                  if (cand && ak == ak_new) {
+                    atomicMin(&e->lid, lid);
+                    e->val = v;
+                  }
+                }
+              }
+            }
           }
         }
       }
@@ -490,6 +547,13 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
     const unsigned int bl = bucket[lane].lid;
     a.part_obj[(size_t)t * 64 + lane] = __longlong_as_double((long long)bucket[lane].key);
     a.part_id[(size_t)t * 64 + lane] = bl == 0xFFFFFFFFu ? kNone : g.base + (uint64_t)bl;
+    if constexpr (AL) {
+      if (lane < a.n_alpha) {
+        const AlphaEntry e = s_aent[wave][lane];
+        a.part_aobj[(size_t)t * a.n_alpha + lane] = e.val;
+        a.part_aid[(size_t)t * a.n_alpha + lane] = e.lid == 0xFFFFFFFFu ? kNone : g.base + (uint64_t)e.lid;
+      }
+    }
     if (!claims) break;
     for (;;) {
       int c = 0;
@@ -568,6 +632,28 @@ __global__ __launch_bounds__(kReduceBlock) void k_reduce(ReduceArgs a) {
     a.best_id[g] = bi;
     a.frontier[g] = mask;
   }
+  if (lane < a.n_alpha) {  // lane a: weight sample a
+    double ao = __builtin_huge_val();
+    uint64_t ai = kNone;
+    for (int t = grp.tile_begin; t < grp.tile_begin + grp.n_tiles; ++t) {
+      const double o = a.part_aobj[(size_t)t * a.n_alpha + lane];
+      const uint64_t i = a.part_aid[(size_t)t * a.n_alpha + lane];
+      if (lex_less(o, i, ao, ai)) {
+        ao = o;
+        ai = i;
+      }
+    }
+    for (int t = grp.tail_begin; t < grp.tail_begin + grp.n_tail; ++t) {
+      const double o = a.part_aobj[(size_t)t * a.n_alpha + lane];
+      const uint64_t i = a.part_aid[(size_t)t * a.n_alpha + lane];
+      if (lex_less(o, i, ao, ai)) {
+        ao = o;
+        ai = i;
+      }
+    }
+    a.alpha_obj[g * a.n_alpha + lane] = ao;
+    a.alpha_id[g * a.n_alpha + lane] = ai;
+  }
 }
 
 // ---------------------------------------------------------------------------------------
@@ -632,14 +718,18 @@ int check_launch() {
 
 template <int R>
 void launch_eval_r(const EvalArgs& a, int blocks, hipStream_t st) {
-  hipLaunchKernelGGL(k_eval<R>, dim3(blocks), dim3(kBlock), 0, st, a, a.ratio, (const PairK*)a.pk);
+  if (a.n_alpha > 0)
+    hipLaunchKernelGGL((k_eval<R, true>), dim3(blocks), dim3(kBlock), 0, st, a, a.ratio, (const PairK*)a.pk);
+  else
+    hipLaunchKernelGGL((k_eval<R, false>), dim3(blocks), dim3(kBlock), 0, st, a, a.ratio, (const PairK*)a.pk);
 }
 
 template <int R>
-int blocks_per_cu_r() {
+int blocks_per_cu_r(bool alpha) {
   int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_eval<R>, kBlock, 0) != hipSuccess) return 1;
-  return n;
+  const hipError_t e = alpha ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_eval<R, true>, kBlock, 0)
+                             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_eval<R, false>, kBlock, 0);
+  return e == hipSuccess ? n : 1;
 }
 
 #define MIST_FOR_EACH_R(X) \
@@ -647,11 +737,11 @@ int blocks_per_cu_r() {
 
 }  // namespace
 
-int eval_blocks_per_cu(int R) {
+int eval_blocks_per_cu(int R, bool alpha) {
   switch (R) {
 #define MIST_CASE(n) \
   case n:            \
-    return blocks_per_cu_r<n>();
+    return blocks_per_cu_r<n>(alpha);
     MIST_FOR_EACH_R(MIST_CASE)
 #undef MIST_CASE
     default:

@@ -21,7 +21,8 @@ MIST_NONE = 0xFFFFFFFFFFFFFFFF
 NONE = np.uint64(MIST_NONE)
 
 EXPORTS = [
-    "mist_space_create", "mist_eval_space", "mist_get_best", "mist_get_pareto", "mist_get_buckets",
+    "mist_space_create", "mist_eval_space", "mist_get_best", "mist_get_pareto", "mist_get_alpha",
+    "mist_get_buckets",
     "mist_space_info", "mist_get_group_key", "mist_decode", "mist_eval_ids", "mist_set_timing",
     "mist_read_timing", "mist_launch_info", "mist_space_destroy", "mist_last_error",
 ]
@@ -50,7 +51,8 @@ class SpaceDesc(ctypes.Structure):
     _fields_ = [("n_devices", ctypes.c_int64), ("global_batch", ctypes.c_int64),
                 ("mb", ctypes.POINTER(ctypes.c_int32)), ("n_mb", ctypes.c_int32),
                 ("ratios", ctypes.POINTER(ctypes.c_double)), ("n_ratios", ctypes.c_int32),
-                ("n_buckets", ctypes.c_int32), ("l_rule", ctypes.c_int32)]
+                ("n_buckets", ctypes.c_int32), ("l_rule", ctypes.c_int32),
+                ("n_alphas", ctypes.c_int32), ("alphas", ctypes.POINTER(ctypes.c_double))]
 
 
 ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p)
@@ -99,6 +101,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         L.mist_eval_space.argtypes = [vp, vp]
         L.mist_get_best.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, P(Result)]
         L.mist_get_pareto.argtypes = [vp, ctypes.c_int64, P(Result), ctypes.c_int32, P(ctypes.c_int32)]
+        L.mist_get_alpha.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, P(Result)]
         L.mist_get_buckets.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, P(ctypes.c_uint64),
                                        P(ctypes.c_double), P(ctypes.c_uint64)]
         L.mist_space_info.argtypes = [vp, P(ctypes.c_uint64), P(ctypes.c_int64), P(ctypes.c_int32)]
@@ -159,10 +162,13 @@ class Space:
                     self._hw[i].phi[m][j] = float(h["phi"][m][j])
         self._mb = np.ascontiguousarray(space["mb"], dtype=np.int32)
         self._ratios = np.ascontiguousarray(space["ratios"], dtype=np.float64)
+        self._alphas = np.ascontiguousarray(space.get("alphas", []), dtype=np.float64)
+        self.n_alphas = len(self._alphas)
         self._space = SpaceDesc(space["n_devices"], space["global_batch"],
                                 self._mb.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), len(self._mb),
                                 self._ratios.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
-                                len(self._ratios), space["n_buckets"], space["l_rule"])
+                                len(self._ratios), space["n_buckets"], space["l_rule"], self.n_alphas,
+                                self._alphas.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
         self._alloc = None
         if allocator == "torch":
             self._alloc = self._torch_allocator()
@@ -237,6 +243,15 @@ class Space:
         cnt = ctypes.c_int32()
         _check(self.L, self.L.mist_get_pareto(self.h, g, out, 64, ctypes.byref(cnt)))
         return [_struct_to_dict(out[i]) for i in range(cnt.value)]
+
+    def alpha(self, g0: int = 0, n: int | None = None) -> list[list[dict]]:
+        """Per group g0..g0+n-1 and weight sample a: the feasible configuration minimising
+        alpha_a*G*t + (1-alpha_a)*d (Eq. 4); obj holds that weighted value."""
+        n = self.n_groups - g0 if n is None else n
+        A = self.n_alphas
+        out = (Result * max(n * A, 1))()
+        _check(self.L, self.L.mist_get_alpha(self.h, g0, n, out))
+        return [[_struct_to_dict(out[i * A + a]) for a in range(A)] for i in range(n)]
 
     def buckets(self, g0: int = 0, n: int | None = None):
         """(ids[n, NB], objs[n, NB], frontier masks[n]) of groups g0..g0+n-1."""

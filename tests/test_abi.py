@@ -52,9 +52,12 @@ def _create(wl, **over):
                 hw[i].phi[a][j] = float(h["phi"][a][j])
     mb = np.ascontiguousarray(s["mb"], dtype=np.int32)
     r = np.ascontiguousarray(s["ratios"], dtype=np.float64)
+    al = np.ascontiguousarray(s.get("alphas", []), dtype=np.float64)
+    n_al = s.get("n_alphas", len(al))
     space = mist.SpaceDesc(s["n_devices"], s["global_batch"], mb.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                            len(mb), r.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), len(r),
-                           s["n_buckets"], s["l_rule"])
+                           s["n_buckets"], s["l_rule"], n_al,
+                           al.ctypes.data_as(ctypes.POINTER(ctypes.c_double)) if len(al) else None)
     h = ctypes.c_void_p()
     rc = L.mist_space_create(ctypes.byref(model), hw, len(hws), ctypes.byref(space), None, ctypes.byref(h))
     return rc, L.mist_last_error().decode()
@@ -66,6 +69,8 @@ def _create(wl, **over):
     {"s__n_buckets": 0}, {"s__n_buckets": 65}, {"s__mb": [2, 1]}, {"s__mb": []},
     {"s__ratios": [0.0, 1.5]}, {"s__ratios": [0.5, 0.5]}, {"s__l_rule": 3}, {"s__n_devices": 0},
     {"s__ratios": [j / 16 for j in range(17)]},
+    {"s__alphas": [0.5, 1.5]}, {"s__alphas": [-0.25]}, {"s__alphas": [float("nan")]},
+    {"s__alphas": [0.5] * 17}, {"s__n_alphas": 2}, {"s__n_alphas": -1},
 ])
 def test_invalid_descriptors_are_rejected(over):
     rc, msg = _create(W.workload("tiny"), **over)

@@ -18,7 +18,8 @@ import pytest
 from oracle import oracle as O
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-PINS = ["tests/test_oracle_pins.py", "tests/test_oracle_terms.py", "tests/test_oracle_reduce.py"]
+PINS = ["tests/test_oracle_pins.py", "tests/test_oracle_terms.py", "tests/test_oracle_reduce.py",
+        "tests/test_oracle_alpha.py"]
 
 MUTANTS = {
     "forward peak drops the optimizer-step unit": (
@@ -56,6 +57,15 @@ MUTANTS = {
         "const R BB = ((base + Gbuf) + Rc) + Xd;", "const R BB = ((base + Gbuf) + Rc);"),
     "efficiency of the wrong microbatch": (
         "R(X.inv_eta[g.hw][pr.mb_index])", "R(X.inv_eta[g.hw][0])"),
+    "weight sample applied to the delta instead of the time": (
+        "for (int32_t a = 0; a < n_alpha; ++a) beta[a] = 1.0 - alphas[a];",
+        "for (int32_t a = 0; a < n_alpha; ++a) beta[a] = alphas[a];"),
+    "weight-sampled argmin ignores the memory budget": (
+        "      if (bucket_of(X, g.hw, mem) < 0) return;  // Eq. 4 constraint: mem <= budget\n      const uint64_t id = g.base + (uint64_t)local;\n      for (int32_t a",
+        "      const uint64_t id = g.base + (uint64_t)local;\n      for (int32_t a"),
+    "weight-sampled argmin keeps the last of equal values": (
+        "        if (lex_less(v, id, out_obj[o * n_alpha + a], out_id[o * n_alpha + a])) {",
+        "        if (!(out_obj[o * n_alpha + a] < v)) {"),
     "pipeline sends counted once for middle stages": (
         "(int64_t)((k > 1) + (k < PP))", "(int64_t)((k > 1) || (k < PP))"),
 }
