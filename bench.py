@@ -4,7 +4,8 @@ vector roofline fraction of the evaluation kernel.
 
 One step = one mist_eval_space over the whole space of the workload (default c2: GPT
 L32 h2560, 273,952,500 configurations, 4,527 groups), inputs resident on the GPU.
-Prints one JSON line.  The CPU baseline is the plain oracle timed on this host over a
+Prints one JSON line; its "alpha_frontier" field times the same space with weight samples of
+Eq. 4 added (the per-group (t, d) argmins).  The CPU baseline is the plain oracle timed on this host over a
 bounded, seeded sample of the same workload's groups.
 """
 
@@ -90,6 +91,9 @@ def main() -> int:
     ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--alphas", type=int, default=8,
+                    help="after the headline run, also time the space with this many weight samples of "
+                         "Eq. 4 (alpha = k/(n-1)); 0 skips it")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="after the timed region, copy a buffer of this many MiB on the device "
                          "(a plain copy kernel of known size, to scale the HBM byte counters)")
@@ -161,6 +165,32 @@ def main() -> int:
                     "unit": "TFLOP/s", "frac": achieved / FP64_VECTOR_PEAK_TFLOPS, "traffic": traffic,
                     "kernel": "k_eval", "flops_per_config": fpc}
 
+    alpha = None
+    if args.alphas > 0:
+        A = args.alphas
+        wa = dict(wl)
+        wa["space"] = dict(wl["space"], alphas=[k / (A - 1) if A > 1 else 0.5 for k in range(A)])
+        SA = mist.from_workload(wa)
+        for _ in range(args.warmup):
+            SA.eval()
+        torch.cuda.synchronize()
+        SA.set_timing(True)
+        start.record()
+        for _ in range(args.steps):
+            SA.eval()
+        end.record()
+        torch.cuda.synchronize()
+        a_total = start.elapsed_time(end)
+        a_k1, a_k2, a_n = SA.read_timing()
+        SA.set_timing(False)
+        a_fpc = None if fpc is None else fpc + 3.0 * A   # + per sample: (1-alpha)*d and one fma
+        a_k1_avg = a_k1 / a_n
+        alpha = {"n_alphas": A, "value": S.n_configs / (a_total / args.steps / 1e3), "unit": "configs/s",
+                 "ms_per_step": a_total / args.steps, "eval_kernel_ms": a_k1_avg, "reduce_kernel_ms": a_k2 / a_n,
+                 "flops_per_config": a_fpc,
+                 "frac": None if a_fpc is None else a_fpc * S.n_configs / (a_k1_avg / 1e3) / 1e12 / FP64_VECTOR_PEAK_TFLOPS}
+        SA.close()
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline: oracle for about %.0f s" % args.cpu_seconds)
@@ -177,7 +207,7 @@ def main() -> int:
         "extract_best_ms": extract_ms, "feasible_groups": feasible,
         "device": {"name": props.name, "cus": props.multi_processor_count,
                    "arch": getattr(props, "gcnArchName", "")},
-        "roofline": roofline, "cpu_baseline": cpu,
+        "roofline": roofline, "cpu_baseline": cpu, "alpha_frontier": alpha,
     }
     S.close()
     print(json.dumps(rec))

@@ -515,6 +515,18 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
               // false.  All lanes address the sample's single entry; the same three-step
               // LDS sequence keeps the lexicographic minimum.
               const double dn = mem <= M ? d : __builtin_nan("");
+              // First every sample against the entries as they stand (no lane can beat an
+              // entry it does not beat now: entries only decrease), in straight-line code;
+              // the exact sequence only when some lane of the wave may win.
+              wave_sync();
+              bool any = false;
+#pragma unroll
+              for (int q = 0; q < kMaxAlphas; ++q) {
+                if (q >= a.n_alpha) break;
+                const double2 ab = s_ab[wave][q];
+                any = any | (__builtin_fma(ab.x, tv, ab.y * dn) <= s_aent[wave][q].val);
+              }
+              if (!__builtin_amdgcn_ballot_w64(any)) continue;
 #pragma unroll 1
               for (int q = 0; q < a.n_alpha; ++q) {
                 const double2 ab = s_ab[wave][q];
