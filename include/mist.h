@@ -57,6 +57,7 @@ typedef int32_t mist_status;
 
 #define MIST_MAX_BUCKETS 64
 #define MIST_MAX_ALPHAS 16
+#define MIST_MAX_STAGES 64
 #define MIST_MAX_RATIOS 16
 #define MIST_MAX_MB 16
 #define MIST_NONE UINT64_MAX /* id of an empty bucket or of a group with no feasible config */
@@ -135,6 +136,29 @@ typedef struct mist_result {
   mist_config cfg;
 } mist_result;
 
+/* One intra-stage candidate for the inter-stage planner: a configuration of group
+ * (G, PP, k, l) of one hardware sample with its stable time t and first-microbatch delta d
+ * (seconds). */
+typedef struct mist_stage_point {
+  int32_t G, PP, k, l;
+  uint64_t id;
+  double t, d;
+} mist_stage_point;
+
+typedef struct mist_stage_plan {
+  int32_t l, k;   /* layers of the stage; microbatches in flight (PP - i + 1 for stage i) */
+  uint64_t id;    /* the stage's configuration */
+  double t, d;
+} mist_stage_plan;
+
+/* A pipeline plan (Sec. 5.3, Eq. 1-3) for one hardware sample. */
+typedef struct mist_plan {
+  int32_t found;  /* 0 when no plan exists (then F = +inf) */
+  int32_t hw, G, PP;
+  double F;       /* Eq. 2: (G-1)*max t_i + sum t_i + max_i (d_i - sum_{j<i} t_j), in stage order */
+  mist_stage_plan stage[MIST_MAX_STAGES];  /* stages 1..PP */
+} mist_plan;
+
 typedef struct mist_group_key {
   int32_t hw, G, PP, k, l, n_pairs;
   uint64_t base;  /* id of the group's first configuration */
@@ -176,6 +200,22 @@ mist_status mist_get_pareto(mist_space* S, int64_t g, mist_result* out, int32_t 
  * feasible configuration).  Errors: MIST_E_STATE (no samples, or no evaluation yet),
  * MIST_E_RANGE, MIST_E_DEVICE. */
 mist_status mist_get_alpha(mist_space* S, int64_t g0, int64_t n, mist_result* out);
+
+/* Inter-stage planner (Sec. 5.3, Eq. 1-3), host only: among the candidate points pts[0..n-1]
+ * of one hardware sample, chooses G, PP, the layer counts l_1..l_PP (summing to n_layers; stage
+ * i draws from the points of group (G, PP, k = PP - i + 1, l_i)) and one point per stage so
+ * that Eq. 2 is minimal, exactly (a dominance-pruned dynamic program over stages).  pp = 0
+ * allows every PP, otherwise only plans with PP = pp (<= MIST_MAX_STAGES; points of larger PP
+ * are ignored).  Writes *out (found = 0 when no plan exists).  Errors: MIST_E_INVALID. */
+mist_status mist_plan_points(const mist_stage_point* pts, int64_t n, int32_t n_layers, int32_t pp,
+                             mist_plan* out);
+
+/* The planner on an evaluated space: every group of hardware sample hw contributes its best
+ * configuration and, when the space has weight samples, the configuration each sample selects
+ * (its points of the (t, d) frontier, Eq. 3-4); waits for the last evaluation, re-evaluates the
+ * points' t and d on the device and calls mist_plan_points with the model's layer count.
+ * Errors: MIST_E_STATE (no evaluation yet), MIST_E_RANGE (hw), MIST_E_DEVICE, MIST_E_NOMEM. */
+mist_status mist_plan_pipeline(mist_space* S, int32_t hw, int32_t pp, mist_plan* out);
 
 /* Raw per-bucket table of groups g0..g0+n-1: host ids[n*NB] and objs[n*NB] (MIST_NONE /
  * +inf for empty buckets) and host frontier masks[n] (bit j = bucket j on the staircase);

@@ -769,6 +769,53 @@ mist_status mist_get_alpha(mist_space* S, int64_t g0, int64_t n, mist_result* ou
   }
 }
 
+mist_status mist_plan_pipeline(mist_space* S, int32_t hw, int32_t pp, mist_plan* out) {
+  if (!S || !out) return fail(MIST_E_INVALID, "null argument");
+  if (hw < 0 || hw >= (int32_t)S->hw.size()) return fail(MIST_E_RANGE, "hardware sample out of range");
+  if (pp < 0 || pp > MIST_MAX_STAGES) return fail(MIST_E_INVALID, "pp out of range");
+  mist_status rc = wait_results(S);
+  if (rc) return rc;
+  try {
+    const size_t A = (size_t)S->A, ng = S->groups.size();
+    std::vector<uint64_t> best(ng), alpha(ng * A);
+    hipError_t e = hipMemcpy(best.data(), S->d_best_id, ng * sizeof(uint64_t), hipMemcpyDeviceToHost);
+    if (e == hipSuccess && A)
+      e = hipMemcpy(alpha.data(), S->d_alpha_id, ng * A * sizeof(uint64_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpy frontier points");
+    std::vector<mist_stage_point> pts;
+    std::vector<uint64_t> ids;
+    for (size_t g = 0; g < ng; ++g) {
+      if (S->groups[g].hw != hw || (pp != 0 && S->groups[g].PP != pp)) continue;
+      std::vector<uint64_t> mine(1 + A);
+      mine[0] = best[g];
+      for (size_t a = 0; a < A; ++a) mine[1 + a] = alpha[g * A + a];
+      std::sort(mine.begin(), mine.end());
+      mine.erase(std::unique(mine.begin(), mine.end()), mine.end());
+      const DevGroup& G = S->groups[g];
+      for (uint64_t id : mine) {
+        if (id == MIST_NONE) continue;
+        mist_stage_point p{};
+        p.G = G.G; p.PP = G.PP; p.k = G.k; p.l = G.l; p.id = id;
+        pts.push_back(p);
+        ids.push_back(id);
+      }
+    }
+    std::vector<double> vals(ids.size() * 4);
+    rc = eval_ids_impl(S, ids.data(), (int64_t)ids.size(), vals.data(), S->stream);
+    if (rc) return rc;
+    for (size_t i = 0; i < pts.size(); ++i) {
+      pts[i].t = vals[4 * i + 0];
+      pts[i].d = vals[4 * i + 1];
+    }
+    rc = mist_plan_points(pts.data(), (int64_t)pts.size(), S->model.n_layers, pp, out);
+    if (rc) return rc;
+    out->hw = hw;
+    return MIST_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(MIST_E_NOMEM, "host allocation failed");
+  }
+}
+
 mist_status mist_get_buckets(mist_space* S, int64_t g0, int64_t n, uint64_t* ids, double* objs,
                              uint64_t* masks) {
   if (!S) return fail(MIST_E_INVALID, "space is null");
@@ -911,3 +958,7 @@ mist_status mist_space_destroy(mist_space* S) {
 const char* mist_last_error(void) { return g_error.c_str(); }
 
 }  // extern "C"
+
+namespace mist {
+__attribute__((visibility("hidden"))) mist_status plan_fail(mist_status code, const std::string& msg) { return fail(code, msg); }
+}  // namespace mist

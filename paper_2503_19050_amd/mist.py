@@ -25,6 +25,7 @@ EXPORTS = [
     "mist_get_buckets",
     "mist_space_info", "mist_get_group_key", "mist_decode", "mist_eval_ids", "mist_set_timing",
     "mist_read_timing", "mist_launch_info", "mist_space_destroy", "mist_last_error",
+    "mist_plan_points", "mist_plan_pipeline",
 ]
 
 
@@ -53,6 +54,31 @@ class SpaceDesc(ctypes.Structure):
                 ("ratios", ctypes.POINTER(ctypes.c_double)), ("n_ratios", ctypes.c_int32),
                 ("n_buckets", ctypes.c_int32), ("l_rule", ctypes.c_int32),
                 ("n_alphas", ctypes.c_int32), ("alphas", ctypes.POINTER(ctypes.c_double))]
+
+
+MAX_STAGES = 64
+
+
+class StagePoint(ctypes.Structure):
+    _fields_ = [("G", ctypes.c_int32), ("PP", ctypes.c_int32), ("k", ctypes.c_int32), ("l", ctypes.c_int32),
+                ("id", ctypes.c_uint64), ("t", ctypes.c_double), ("d", ctypes.c_double)]
+
+
+class StagePlan(ctypes.Structure):
+    _fields_ = [("l", ctypes.c_int32), ("k", ctypes.c_int32), ("id", ctypes.c_uint64),
+                ("t", ctypes.c_double), ("d", ctypes.c_double)]
+
+
+class Plan(ctypes.Structure):
+    _fields_ = [("found", ctypes.c_int32), ("hw", ctypes.c_int32), ("G", ctypes.c_int32), ("PP", ctypes.c_int32),
+                ("F", ctypes.c_double), ("stage", StagePlan * MAX_STAGES)]
+
+
+def _plan_dict(p: Plan) -> dict | None:
+    if not p.found:
+        return None
+    return {"hw": p.hw, "G": p.G, "PP": p.PP, "F": p.F,
+            "stages": [_struct_to_dict(p.stage[i]) for i in range(p.PP)]}
 
 
 ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p)
@@ -112,6 +138,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         L.mist_read_timing.argtypes = [vp, P(ctypes.c_double), P(ctypes.c_double), P(ctypes.c_int64)]
         L.mist_launch_info.argtypes = [vp, P(ctypes.c_int64), P(ctypes.c_int32), P(ctypes.c_int32)]
         L.mist_space_destroy.argtypes = [vp]
+        L.mist_plan_points.argtypes = [P(StagePoint), ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P(Plan)]
+        L.mist_plan_pipeline.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, P(Plan)]
         L.mist_last_error.restype = ctypes.c_char_p
         for name in EXPORTS:
             if name != "mist_last_error":
@@ -244,6 +272,13 @@ class Space:
         _check(self.L, self.L.mist_get_pareto(self.h, g, out, 64, ctypes.byref(cnt)))
         return [_struct_to_dict(out[i]) for i in range(cnt.value)]
 
+    def plan(self, hw: int = 0, pp: int = 0) -> dict | None:
+        """The inter-stage plan (Eq. 1-3) of hardware sample hw from this space's frontier
+        points; pp = 0 allows every stage count.  None when no plan exists."""
+        out = Plan()
+        _check(self.L, self.L.mist_plan_pipeline(self.h, hw, pp, ctypes.byref(out)))
+        return _plan_dict(out)
+
     def alpha(self, g0: int = 0, n: int | None = None) -> list[list[dict]]:
         """Per group g0..g0+n-1 and weight sample a: the feasible configuration minimising
         alpha_a*G*t + (1-alpha_a)*d (Eq. 4); obj holds that weighted value."""
@@ -304,3 +339,16 @@ class Space:
 
 def from_workload(wl: dict, allocator: str | None = "torch") -> Space:
     return Space(wl["model"], wl["hws"], wl["space"], allocator=allocator)
+
+
+def plan_points(points, n_layers: int, pp: int = 0) -> dict | None:
+    """The host planner on explicit candidate points: an iterable of dicts with keys G, PP, k,
+    l, id, t, d.  None when no plan exists."""
+    L = load()
+    pts = list(points)
+    arr = (StagePoint * max(len(pts), 1))()
+    for i, p in enumerate(pts):
+        arr[i] = StagePoint(p["G"], p["PP"], p["k"], p["l"], p["id"], p["t"], p["d"])
+    out = Plan()
+    _check(L, L.mist_plan_points(arr, len(pts), n_layers, pp, ctypes.byref(out)))
+    return _plan_dict(out)
