@@ -3,8 +3,9 @@
 Bar: identical argmin ids, bucket tables and frontier bits, and every cost value within
 1e-12 relative (the kernels follow the same IEEE operation sequence, so the values are
 compared bit for bit).  Full-size workloads c3-c5 run in the benchmark's launch
-configuration; the oracle then recomputes a sample of whole groups and a sample of
-single configurations.
+configuration; every group is compared with the oracle's stored whole-space run (one digest
+per group), and the oracle recomputes a sample of whole groups and single configurations in
+full.
 """
 
 import os
@@ -19,6 +20,7 @@ from paper_2503_19050_amd import workloads as W
 pytestmark = pytest.mark.gpu
 
 PROCS = max(1, min(16, os.cpu_count() or 1))
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 
 def say(*a):
@@ -106,6 +108,29 @@ def test_full_size_sampled_parity(name, torch_cuda):
     ref = O.run_groups(wl, groups, procs=PROCS)
     _compare_groups(S, ref, groups)
     _compare_ids(S, o, _sample_ids(o, rng, 3000))
+    S.close()
+
+
+@pytest.mark.parametrize("name", ["c3", "c4"])
+def test_full_parity_large(name, torch_cuda):
+    """Every group of the full-size workloads against the oracle's whole-space run, stored as
+    one digest per group by tests/golden/make_full_oracle.py (which calls only the oracle)."""
+    sys.path.insert(0, GOLDEN)
+    from digest import group_digests
+    gold = np.load(os.path.join(GOLDEN, "full_%s.npz" % name))
+    wl = W.workload(name)
+    S = _space(wl, torch_cuda)
+    assert (S.n_configs, S.n_groups, S.n_buckets) == (int(gold["n_configs"]), int(gold["n_groups"]),
+                                                      int(gold["n_buckets"]))
+    _eval(S, torch_cuda)
+    ids, objs, masks = S.buckets(0, S.n_groups)
+    best = S.best(0, S.n_groups)
+    bid = np.array([b["id"] for b in best], dtype=np.uint64)
+    bobj = np.array([b["obj"] for b in best], dtype=np.float64)
+    got = group_digests(ids, objs, masks, bid, bobj)
+    bad = np.flatnonzero(got != gold["digest"])
+    assert bad.size == 0, "%d of %d groups differ from the oracle, first %s" % (bad.size, S.n_groups, bad[:8])
+    say(name, "all", S.n_groups, "groups match the oracle's whole-space run")
     S.close()
 
 
