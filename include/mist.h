@@ -217,6 +217,21 @@ mist_status mist_plan_points(const mist_stage_point* pts, int64_t n, int32_t n_l
  * Errors: MIST_E_STATE (no evaluation yet), MIST_E_RANGE (hw), MIST_E_DEVICE, MIST_E_NOMEM. */
 mist_status mist_plan_pipeline(mist_space* S, int32_t hw, int32_t pp, mist_plan* out);
 
+/* Exact time-vs-memory frontier of every group (the staircase without memory buckets): after
+ * mist_eval_space, finds for each group the feasible configurations whose obj is strictly
+ * below that of every configuration before them in (mem, obj, id) order.  A candidate pass
+ * keeps only configurations that beat every lower bucket's minimum and are not dominated by
+ * their bucket's winner; they are sorted by memory per group and scanned.  Waits for the
+ * evaluation and once more for the candidate count, then enqueues the rest on hip_stream.
+ * Errors: MIST_E_STATE (no evaluation yet), MIST_E_RANGE (2^32 candidates or more),
+ * MIST_E_NOMEM, MIST_E_DEVICE. */
+mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream);
+
+/* The exact frontier of group g in increasing memory (strictly decreasing obj) into host
+ * out[0..*n_out-1]; returns MIST_E_RANGE with *n_out set when cap is too small.  Waits for
+ * mist_eval_pareto_exact.  Errors: MIST_E_STATE, MIST_E_RANGE, MIST_E_DEVICE. */
+mist_status mist_get_pareto_exact(mist_space* S, int64_t g, mist_result* out, int64_t cap, int64_t* n_out);
+
 /* Raw per-bucket table of groups g0..g0+n-1: host ids[n*NB] and objs[n*NB] (MIST_NONE /
  * +inf for empty buckets) and host frontier masks[n] (bit j = bucket j on the staircase);
  * any output pointer may be NULL.  Waits for the last evaluation.  Errors as get_best. */

@@ -33,6 +33,7 @@
 // counting build (R = Counted) reports the FP64 operations of the definition
 // per configuration: add, sub and mul count 1, fma counts 2, min/max/compare 0.
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstdio>
@@ -776,6 +777,42 @@ int orc_run_alpha(const Model* m, const Hw* hw, int32_t n_hw, const Space* s, co
     });
   }
   return 0;
+}
+
+// Exact time-vs-memory frontier of group g (the staircase without memory buckets): the
+// feasible configurations ordered by (mem, obj, id); one is on the frontier when its obj is
+// strictly below the obj of every configuration before it.  Writes up to cap points in that
+// order (increasing mem, strictly decreasing obj) and the count to *n_out; returns -5 when
+// cap is too small (with *n_out set to the count).
+int orc_pareto_exact(const Model* m, const Hw* hw, int32_t n_hw, const Space* s, int64_t g_index,
+                     uint64_t* out_id, double* out_obj, double* out_mem, int64_t cap, int64_t* n_out) {
+  Ctx X;
+  if (!build_ctx(X, m, hw, n_hw, s)) return -1;
+  if (g_index < 0 || g_index >= (int64_t)X.groups.size()) return -5;
+  const Group& g = X.groups[g_index];
+  struct P { double mem, obj; uint64_t id; };
+  std::vector<P> all;
+  walk_group<double>(X, g, full_box(X, g), nullptr, [&](int64_t local, double t, double d, double mem, double obj) {
+    check_values(t, d, mem, obj);
+    if (bucket_of(X, g.hw, mem) < 0) return;  // Eq. 4 constraint: mem <= budget
+    all.push_back(P{mem, obj, g.base + (uint64_t)local});
+  });
+  std::sort(all.begin(), all.end(), [](const P& a, const P& b) {
+    if (a.mem != b.mem) return a.mem < b.mem;
+    if (a.obj != b.obj) return a.obj < b.obj;
+    return a.id < b.id;
+  });
+  int64_t n = 0;
+  double run = std::numeric_limits<double>::infinity();
+  for (const P& p : all) {
+    if (p.obj < run) {
+      if (n < cap) { out_id[n] = p.id; out_obj[n] = p.obj; out_mem[n] = p.mem; }
+      ++n;
+    }
+    run = min2(run, p.obj);
+  }
+  *n_out = n;
+  return n > cap ? -5 : 0;
 }
 
 // FP64 operations of the definition over groups [g0, g1), counted by running

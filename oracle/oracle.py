@@ -65,6 +65,8 @@ def lib() -> ctypes.CDLL:
                                                  P(ctypes.c_uint64)]
             L.orc_run_alpha.argtypes = args + [P(ctypes.c_double), ctypes.c_int32, ctypes.c_int64,
                                                ctypes.c_int64, P(ctypes.c_uint64), P(ctypes.c_double)]
+            L.orc_pareto_exact.argtypes = args + [ctypes.c_int64, P(ctypes.c_uint64), P(ctypes.c_double),
+                                                  P(ctypes.c_double), ctypes.c_int64, P(ctypes.c_int64)]
             L.orc_interference.argtypes = [P(ctypes.c_double), P(ctypes.c_double)]
             L.orc_interference.restype = ctypes.c_double
             _lib = L
@@ -202,6 +204,21 @@ class Oracle:
         self._check(self.L.orc_run_alpha(*self._args(), _dp(al), len(al), g0, g1, _up(res["id"]),
                                          _dp(res["obj"])))
         return res
+
+    def pareto_exact(self, g: int) -> dict:
+        """Exact (non-bucketed) time-vs-memory frontier of group g: {"id", "obj", "mem"} in
+        increasing memory, strictly decreasing objective."""
+        cap = 4096
+        while True:
+            res = {"id": np.empty(cap, dtype=np.uint64), "obj": np.empty(cap), "mem": np.empty(cap)}
+            n = ctypes.c_int64()
+            rc = self.L.orc_pareto_exact(*self._args(), g, _up(res["id"]), _dp(res["obj"]), _dp(res["mem"]),
+                                         cap, ctypes.byref(n))
+            if rc == -5 and n.value > cap:
+                cap = n.value
+                continue
+            self._check(rc)
+            return {k: v[:n.value] for k, v in res.items()}
 
     def count_flops(self, g0: int = 0, g1: int | None = None) -> tuple[int, int]:
         g1 = self.n_groups if g1 is None else g1

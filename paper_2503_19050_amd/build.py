@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmist.so")
 SOURCES = [os.path.join(CSRC, "mist_host.cpp"), os.path.join(CSRC, "mist_plan.cpp"),
-           os.path.join(CSRC, "mist_kernels.hip")]
+           os.path.join(CSRC, "mist_kernels.hip"), os.path.join(CSRC, "mist_exact.hip")]
 HEADERS = [os.path.join(CSRC, "mist_internal.h"), os.path.join(INCLUDE, "mist.h")]
 
 ARCH = "gfx950"

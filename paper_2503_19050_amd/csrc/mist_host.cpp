@@ -88,6 +88,25 @@ struct mist_space {
   uint64_t* d_part_aid = nullptr;
   double* d_alpha_obj = nullptr;
   uint64_t* d_alpha_id = nullptr;
+  int32_t cus = 0;
+  // exact frontier (mist_eval_pareto_exact)
+  bool exact_done = false;
+  hipStream_t exact_stream = nullptr;
+  FiltEntry* d_filt = nullptr;
+  int32_t* d_cnt_tile = nullptr;
+  int64_t* d_tile_off = nullptr;
+  int64_t* d_seg = nullptr;
+  int64_t* d_front_cnt = nullptr;
+  std::vector<int32_t> h_cnt;
+  std::vector<int64_t> h_tile_off, h_seg;
+  int64_t cand_cap = 0, n_cand = 0;
+  uint64_t *d_cand_key = nullptr, *d_cand_id = nullptr, *d_key_sorted = nullptr;
+  double* d_cand_obj = nullptr;
+  uint32_t *d_idx_in = nullptr, *d_idx_out = nullptr;
+  uint64_t *d_front_key = nullptr, *d_front_id = nullptr;
+  double* d_front_obj = nullptr;
+  void* d_sort_temp = nullptr;
+  size_t sort_temp_bytes = 0;
   // state
   bool evaluated = false;
   hipStream_t stream = nullptr;
@@ -108,6 +127,17 @@ void* dev_alloc(mist_space* S, size_t bytes) {
   }
   if (p) S->dev_buffers.push_back(p);
   return p;
+}
+
+void dev_free_one(mist_space* S, void* p) {
+  if (!p) return;
+  for (size_t i = 0; i < S->dev_buffers.size(); ++i)
+    if (S->dev_buffers[i] == p) {
+      S->dev_buffers.erase(S->dev_buffers.begin() + (long)i);
+      break;
+    }
+  if (S->custom_alloc) S->alloc.free(p, S->alloc.ctx);
+  else (void)hipFree(p);
 }
 
 void dev_free_all(mist_space* S) {
@@ -588,8 +618,9 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
       hipError_t e = hipGetDevice(&dev);
       if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
       if (e != hipSuccess) rc = fail_hip(e, "device attributes");
-      const int per_cu = eval_blocks_per_cu(S->R, S->A > 0);
+      const int per_cu = eval_blocks_per_cu(S->R, S->A > 0 ? kModeAlpha : kModeBuckets);
       resident_blocks = std::max<int64_t>(1, (int64_t)cus * (per_cu > 0 ? per_cu : 1));
+      S->cus = cus;
     }
     if (!rc) {
       const std::string terr = build_tiles(S, resident_blocks * kWaves);
@@ -667,7 +698,7 @@ mist_status mist_eval_space(mist_space* S, void* hip_stream) {
     const hipError_t e = hipEventRecord(ev[0], st);
     if (e != hipSuccess) return fail_hip(e, "hipEventRecord");
   }
-  rc = launch_eval(ea, S->eval_grid, st);
+  rc = launch_eval(ea, S->eval_grid, S->A > 0 ? kModeAlpha : kModeBuckets, st);
   if (rc) return fail_hip((hipError_t)rc, "evaluation kernel launch");
   if (ev) {
     const hipError_t e = hipEventRecord(ev[1], st);
@@ -697,7 +728,153 @@ mist_status mist_eval_space(mist_space* S, void* hip_stream) {
   }
   S->evaluated = true;
   S->stream = st;
+  S->exact_done = false;
   return MIST_OK;
+}
+
+// Grid of the persistent evaluation kernel in a given variant.
+static int32_t mode_grid(const mist_space* S, int mode) {
+  const int per_cu = eval_blocks_per_cu(S->R, mode);
+  const int64_t resident = std::max<int64_t>(1, (int64_t)S->cus * (per_cu > 0 ? per_cu : 1));
+  const int64_t waves_needed = (int64_t)(S->tiles.size() + kWaves - 1) / kWaves;
+  return (int32_t)std::max<int64_t>(1, std::min<int64_t>(resident, waves_needed));
+}
+
+mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
+  if (!S) return fail(MIST_E_INVALID, "space is null");
+  mist_status rc = wait_results(S);
+  if (rc) return rc;
+  try {
+    hipStream_t st = (hipStream_t)hip_stream;
+    const size_t nt = S->tiles.size(), ng = S->groups.size();
+    if (!S->d_filt) {
+      S->d_filt = (FiltEntry*)dev_alloc(S, ng * 64 * sizeof(FiltEntry));
+      S->d_cnt_tile = (int32_t*)dev_alloc(S, nt * sizeof(int32_t));
+      S->d_tile_off = (int64_t*)dev_alloc(S, nt * sizeof(int64_t));
+      S->d_seg = (int64_t*)dev_alloc(S, (ng + 1) * sizeof(int64_t));
+      S->d_front_cnt = (int64_t*)dev_alloc(S, ng * sizeof(int64_t));
+      if (!S->d_filt || !S->d_cnt_tile || !S->d_tile_off || !S->d_seg || !S->d_front_cnt)
+        return fail(MIST_E_NOMEM, "device allocation failed: exact frontier");
+    }
+    EvalArgs ea = eval_args(S);
+    ea.filt = S->d_filt;
+    ea.cnt_tile = S->d_cnt_tile;
+    ea.tile_off = S->d_tile_off;
+    int k = launch_filter(ea, S->d_bucket_obj, S->d_bucket_id, S->d_filt, st);
+    if (!k) k = launch_pairs(ea, st);  // also resets the tile counters
+    if (!k) k = launch_eval(ea, mode_grid(S, kModeCount), kModeCount, st);
+    if (k) return fail_hip((hipError_t)k, "exact frontier: count");
+    S->h_cnt.resize(nt);
+    hipError_t e = hipMemcpyAsync(S->h_cnt.data(), S->d_cnt_tile, nt * sizeof(int32_t), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return fail_hip(e, "exact frontier: counts");
+    // Candidate slots in group order: a group's full-size tiles, then its small ones.
+    S->h_tile_off.assign(nt, 0);
+    S->h_seg.assign(ng + 1, 0);
+    int64_t off = 0;
+    for (size_t g = 0; g < ng; ++g) {
+      const DevGroup& G = S->groups[g];
+      S->h_seg[g] = off;
+      for (int32_t t = G.tile_begin; t < G.tile_begin + G.n_tiles; ++t) {
+        S->h_tile_off[t] = off;
+        off += S->h_cnt[t];
+      }
+      for (int32_t t = G.tail_begin; t < G.tail_begin + G.n_tail; ++t) {
+        S->h_tile_off[t] = off;
+        off += S->h_cnt[t];
+      }
+    }
+    S->h_seg[ng] = off;
+    if (off >= ((int64_t)1 << 32)) return fail(MIST_E_RANGE, "exact frontier: more than 2^32 candidates");
+    if (off > S->cand_cap) {
+      void* old[] = {S->d_cand_key, S->d_cand_id, S->d_key_sorted, S->d_cand_obj, S->d_idx_in, S->d_idx_out,
+                     S->d_front_key, S->d_front_id, S->d_front_obj};
+      for (void* p : old) dev_free_one(S, p);
+      const size_t n = (size_t)off;
+      S->d_cand_key = (uint64_t*)dev_alloc(S, n * 8);
+      S->d_cand_id = (uint64_t*)dev_alloc(S, n * 8);
+      S->d_key_sorted = (uint64_t*)dev_alloc(S, n * 8);
+      S->d_cand_obj = (double*)dev_alloc(S, n * 8);
+      S->d_idx_in = (uint32_t*)dev_alloc(S, n * 4);
+      S->d_idx_out = (uint32_t*)dev_alloc(S, n * 4);
+      S->d_front_key = (uint64_t*)dev_alloc(S, n * 8);
+      S->d_front_id = (uint64_t*)dev_alloc(S, n * 8);
+      S->d_front_obj = (double*)dev_alloc(S, n * 8);
+      S->cand_cap = off;
+      if (!S->d_cand_key || !S->d_cand_id || !S->d_key_sorted || !S->d_cand_obj || !S->d_idx_in ||
+          !S->d_idx_out || !S->d_front_key || !S->d_front_id || !S->d_front_obj) {
+        S->cand_cap = 0;
+        return fail(MIST_E_NOMEM, "device allocation failed: exact frontier candidates");
+      }
+    }
+    size_t need = 0;
+    k = exact_sort(S->d_cand_key, S->d_key_sorted, S->d_idx_in, S->d_idx_out, off, (int64_t)ng, S->d_seg,
+                   nullptr, &need, st);
+    if (k) return fail_hip((hipError_t)k, "exact frontier: sort storage");
+    if (need > S->sort_temp_bytes) {
+      dev_free_one(S, S->d_sort_temp);
+      S->d_sort_temp = dev_alloc(S, need);
+      S->sort_temp_bytes = S->d_sort_temp ? need : 0;
+      if (!S->d_sort_temp) return fail(MIST_E_NOMEM, "device allocation failed: sort storage");
+    }
+    e = hipMemcpyAsync(S->d_tile_off, S->h_tile_off.data(), nt * sizeof(int64_t), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(S->d_seg, S->h_seg.data(), (ng + 1) * sizeof(int64_t), hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return fail_hip(e, "exact frontier: offsets");
+    ea.cand_key = S->d_cand_key;
+    ea.cand_obj = S->d_cand_obj;
+    ea.cand_id = S->d_cand_id;
+    k = launch_pairs(ea, st);
+    if (!k) k = launch_eval(ea, mode_grid(S, kModeEmit), kModeEmit, st);
+    if (!k) {
+      size_t bytes = S->sort_temp_bytes;
+      k = exact_sort(S->d_cand_key, S->d_key_sorted, S->d_idx_in, S->d_idx_out, off, (int64_t)ng, S->d_seg,
+                     S->d_sort_temp, &bytes, st);
+    }
+    if (!k)
+      k = launch_front_scan(S->d_key_sorted, S->d_idx_out, S->d_cand_obj, S->d_cand_id, S->d_seg, (int64_t)ng,
+                            S->d_front_key, S->d_front_obj, S->d_front_id, S->d_front_cnt, st);
+    if (k) return fail_hip((hipError_t)k, "exact frontier");
+    S->n_cand = off;
+    S->exact_done = true;
+    S->exact_stream = st;
+    return MIST_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(MIST_E_NOMEM, "host allocation failed");
+  }
+}
+
+mist_status mist_get_pareto_exact(mist_space* S, int64_t g, mist_result* out, int64_t cap, int64_t* n_out) {
+  if (!S || !n_out || (!out && cap > 0)) return fail(MIST_E_INVALID, "null argument");
+  if (!S->exact_done) return fail(MIST_E_STATE, "mist_eval_pareto_exact has not been called");
+  if (g < 0 || g >= (int64_t)S->groups.size()) return fail(MIST_E_RANGE, "group out of range");
+  hipError_t e = hipStreamSynchronize(S->exact_stream);
+  if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+  try {
+    int64_t n = 0;
+    e = hipMemcpy(&n, S->d_front_cnt + g, sizeof(int64_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpy frontier count");
+    *n_out = n;
+    if (n > cap) return fail(MIST_E_RANGE, "cap is smaller than the frontier");
+    if (n == 0) return MIST_OK;
+    const size_t b = (size_t)S->h_seg[g];
+    std::vector<uint64_t> keys(n), ids(n);
+    std::vector<double> objs(n);
+    e = hipMemcpy(keys.data(), S->d_front_key + b, n * 8, hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = hipMemcpy(ids.data(), S->d_front_id + b, n * 8, hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = hipMemcpy(objs.data(), S->d_front_obj + b, n * 8, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpy frontier");
+    mist_status rc = fill_results(S, ids.data(), objs.data(), n, out);
+    if (rc) return rc;
+    for (int64_t i = 0; i < n; ++i) {
+      double mem;
+      std::memcpy(&mem, &keys[i], 8);
+      if (mem != out[i].mem) return fail(MIST_E_DEVICE, "re-evaluated memory differs");
+    }
+    return MIST_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(MIST_E_NOMEM, "host allocation failed");
+  }
 }
 
 mist_status mist_get_best(mist_space* S, int64_t g0, int64_t n, mist_result* out) {

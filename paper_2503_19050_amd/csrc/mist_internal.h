@@ -79,6 +79,19 @@ struct PairK {
   double iD;           // 1 / DP
 };
 
+// Candidate filter of the exact frontier, per (group, bucket j): the objective below which a
+// configuration of bucket j can beat every lower bucket (exclusive prefix minimum of the bucket
+// minima), and the objective and memory of bucket j's winner.
+struct FiltEntry {
+  double pm, bobj, bmem;
+};
+
+// Evaluation kernel variants.
+constexpr int kModeBuckets = 0;  // bucket minima (and per-tile partials)
+constexpr int kModeAlpha = 1;    // bucket minima and the weight-sampled argmins
+constexpr int kModeCount = 2;    // exact frontier: count each tile's candidates
+constexpr int kModeEmit = 3;     // exact frontier: write each tile's candidates
+
 struct EvalArgs {
   DevModel m;
   const DevGroup* groups;
@@ -104,6 +117,13 @@ struct EvalArgs {
   const double* beta;    // [n_alpha]
   double* part_aobj;     // [n_tiles][n_alpha]
   uint64_t* part_aid;    // [n_tiles][n_alpha]
+  // Exact frontier (count and emit variants).
+  const FiltEntry* filt;     // [n_groups][64]
+  int32_t* cnt_tile;         // [n_tiles] candidates per tile (count variant)
+  const int64_t* tile_off;   // [n_tiles] first candidate slot of each tile (emit variant)
+  uint64_t* cand_key;        // memory bit patterns (a non-negative double orders like its bits)
+  double* cand_obj;
+  uint64_t* cand_id;
 };
 
 struct ReduceArgs {
@@ -126,8 +146,17 @@ struct ReduceArgs {
 
 // Kernel launchers (mist_kernels.hip).
 int launch_pairs(const EvalArgs& a, void* stream);
-int launch_eval(const EvalArgs& a, int blocks, void* stream);
-int eval_blocks_per_cu(int R, bool alpha);
+int launch_eval(const EvalArgs& a, int blocks, int mode, void* stream);
+int eval_blocks_per_cu(int R, int mode);
+int launch_filter(const EvalArgs& a, const double* bucket_obj, const uint64_t* bucket_id, FiltEntry* filt,
+                  void* stream);
+// Exact frontier, mist_exact.hip: segmented sort of the candidates by memory (group g's
+// candidates are [seg[g], seg[g+1])) and the per-group scan that keeps the staircase.
+int exact_sort(const uint64_t* key_in, uint64_t* key_out, uint32_t* idx_in, uint32_t* idx_out, int64_t n,
+               int64_t n_groups, const int64_t* seg, void* temp, size_t* temp_bytes, void* stream);
+int launch_front_scan(const uint64_t* key_sorted, const uint32_t* idx_sorted, const double* cand_obj,
+                      const uint64_t* cand_id, const int64_t* seg, int64_t n_groups, uint64_t* front_key,
+                      double* front_obj, uint64_t* front_id, int64_t* front_cnt, void* stream);
 int launch_reduce(const ReduceArgs& a, void* stream);
 int launch_eval_ids(const EvalArgs& a, const uint64_t* ids, int64_t n, double* out, void* stream);
 

@@ -331,10 +331,14 @@ constexpr int ia_block() { return R <= 6 ? R : (R + 2) / 3; }
 template <int R>
 constexpr int eval_waves() { return 4; }
 
-// AL: also the weight-sampled argmins of Eq. 4 (a.n_alpha samples).
-template <int R, bool AL>
+// MODE kModeBuckets: bucket minima; kModeAlpha: also the weight-sampled argmins of Eq. 4
+// (a.n_alpha samples); kModeCount / kModeEmit: the exact frontier's candidates, counted or
+// written per tile (the bucket reduction is skipped).
+template <int R, int MODE>
 __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, const double* __restrict__ ratio,
                                                                  const PairK* __restrict__ pk) {
+  constexpr bool AL = MODE == kModeAlpha;
+  constexpr bool EX = MODE == kModeCount || MODE == kModeEmit;
   constexpr int R2 = R * R;
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
   constexpr int IB = ia_block<R>();
@@ -344,6 +348,7 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
   __shared__ double s_zero[kBlock][2];  // per-lane C and G2G (first microbatch) of the strip
   __shared__ double2 s_ab[AL ? kWaves : 1][kMaxAlphas];      // alpha * G, 1 - alpha
   __shared__ AlphaEntry s_aent[AL ? kWaves : 1][kMaxAlphas];
+  __shared__ FiltEntry s_filt[EX ? kWaves : 1][EX ? 64 : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -386,6 +391,15 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
       bucket[64].lid = 0u;
     }
     const double Gd = (double)g.G;
+    int64_t n_cand = 0;  // exact frontier: candidates counted, or the next slot to write
+    int64_t n_end = 0;   // emit: end of the tile's slots (the count pass's total)
+    if constexpr (EX) {
+      s_filt[wave][lane] = a.filt[(size_t)tile.group * 64 + lane];
+      if constexpr (MODE == kModeEmit) {
+        n_cand = a.tile_off[t];
+        n_end = n_cand + a.cnt_tile[t];
+      }
+    }
     if constexpr (AL) {
       if (lane < a.n_alpha) {
         s_ab[wave][lane] = make_double2(a.alpha[lane] * Gd, a.beta[lane]);
@@ -486,6 +500,30 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
             const unsigned int off0 = __umul24((unsigned int)j0, (unsigned int)sizeof(BucketEntry));
             char* const b0 = reinterpret_cast<char*>(bucket) + off0;
             const double e0 = reinterpret_cast<const BucketEntry*>(b0)->edge;
+            if constexpr (EX) {
+              // Exact frontier candidates: feasible, below every lower bucket's minimum, and not
+              // dominated by the bucket's winner (no more memory and no smaller objective, not
+              // both equal).  Every frontier point passes; the scan after the sort decides.
+              const int j = min(j0 + (mem > e0 ? 1 : 0), 63);
+              const FiltEntry f = s_filt[wave][j];
+              const bool cand = (mem <= M) & (obj < f.pm) &
+                                !(((obj > f.bobj) & (mem >= f.bmem)) | ((obj >= f.bobj) & (mem > f.bmem)));
+              const unsigned long long m = __builtin_amdgcn_ballot_w64(cand);
+              if constexpr (MODE == kModeEmit) {
+                if (cand) {
+                  const unsigned int below = __builtin_amdgcn_mbcnt_hi(
+                      (unsigned int)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)m, 0u));
+                  const int64_t slot = n_cand + below;
+                  if (slot < n_end) {  // the count pass evaluated the same operations
+                    a.cand_key[slot] = (unsigned long long)__double_as_longlong(mem);
+                    a.cand_obj[slot] = obj;
+                    a.cand_id[slot] = g.base + (uint64_t)(lid_oo + (unsigned int)ia);
+                  }
+                }
+              }
+              n_cand += __builtin_popcountll(m);
+              continue;
+            }
             BucketEntry* const be = reinterpret_cast<BucketEntry*>(b0 + (mem > e0 ? sizeof(BucketEntry) : 0));
 
             // Lexicographic (obj, id) minimum per bucket without a serial loop: the lanes
@@ -555,10 +593,14 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
       }
     }
     // The tile's partials: lane j = bucket j.
-    wave_sync();
-    const unsigned int bl = bucket[lane].lid;
-    a.part_obj[(size_t)t * 64 + lane] = __longlong_as_double((long long)bucket[lane].key);
-    a.part_id[(size_t)t * 64 + lane] = bl == 0xFFFFFFFFu ? kNone : g.base + (uint64_t)bl;
+    if constexpr (EX) {
+      if (MODE == kModeCount && lane == 0) a.cnt_tile[t] = (int32_t)n_cand;
+    } else {
+      wave_sync();
+      const unsigned int bl = bucket[lane].lid;
+      a.part_obj[(size_t)t * 64 + lane] = __longlong_as_double((long long)bucket[lane].key);
+      a.part_id[(size_t)t * 64 + lane] = bl == 0xFFFFFFFFu ? kNone : g.base + (uint64_t)bl;
+    }
     if constexpr (AL) {
       if (lane < a.n_alpha) {
         const AlphaEntry e = s_aent[wave][lane];
@@ -671,11 +713,13 @@ __global__ __launch_bounds__(kReduceBlock) void k_reduce(ReduceArgs a) {
 // ---------------------------------------------------------------------------------------
 // Per-id evaluation with the same level functions (parity and result extraction).
 // ---------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_eval_ids(EvalArgs a, const uint64_t* __restrict__ ids,
-                                                  int64_t n, double* __restrict__ out) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const uint64_t id = ids[i];
+struct OneVal {
+  double t, d, mem, obj;
+};
+
+// One configuration by id: binary search of the group, mixed-radix decode, and the level
+// functions of the evaluation kernel.
+__device__ OneVal eval_one(const EvalArgs& a, uint64_t id) {
   int64_t lo = 0, hi = a.n_groups;
   while (hi - lo > 1) {
     const int64_t mid = (lo + hi) / 2;
@@ -711,16 +755,48 @@ __global__ __launch_bounds__(256) void k_eval_ids(EvalArgs a, const uint64_t* __
   const double SO = __builtin_fma(ra, P.A2, om[ia] * K.KA);
   const double H2Ds = __builtin_fma(ra, K.A, W.HW) * hw.iP;
   const double D2Hs = __builtin_fma(ra, K.A, W.DG) * hw.iP;
-  struct { double t, d, mem, obj; } res;
+  OneVal res;
   res.mem = O.Bmax + SO;
   res.t = interference<kTabStride>(K.C, Z.G2Gs, H2Ds, D2Hs, tab);
   const double T1 = interference<kTabStride>(K.C, Z.G2Gf, H2Ds + O.H2Dx, D2Hs + O.D2Hx, tab);
   res.d = T1 - res.t;
   res.obj = __builtin_fma((double)g.G, res.t, res.d);
-  out[4 * i + 0] = res.t;
-  out[4 * i + 1] = res.d;
-  out[4 * i + 2] = res.mem;
-  out[4 * i + 3] = res.obj;
+  return res;
+}
+
+__global__ __launch_bounds__(256) void k_eval_ids(EvalArgs a, const uint64_t* __restrict__ ids,
+                                                  int64_t n, double* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const OneVal v = eval_one(a, ids[i]);
+  out[4 * i + 0] = v.t;
+  out[4 * i + 1] = v.d;
+  out[4 * i + 2] = v.mem;
+  out[4 * i + 3] = v.obj;
+}
+
+// Candidate filter of the exact frontier: one wave per group, lane j = bucket j.
+__global__ __launch_bounds__(kReduceBlock) void k_filter(EvalArgs a, const double* __restrict__ bucket_obj,
+                                                         const uint64_t* __restrict__ bucket_id,
+                                                         FiltEntry* __restrict__ filt) {
+  const int lane = threadIdx.x & 63;
+  const int64_t g = (int64_t)blockIdx.x * (kReduceBlock / 64) + (threadIdx.x >> 6);
+  if (g >= a.n_groups) return;
+  const double obj = lane < a.NB ? bucket_obj[g * 64 + lane] : __builtin_huge_val();
+  const uint64_t id = lane < a.NB ? bucket_id[g * 64 + lane] : kNone;
+  double pm = obj;  // inclusive prefix minimum over buckets 0..lane
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const double o = __shfl_up(pm, off, 64);
+    if (lane >= off) pm = __builtin_fmin(pm, o);
+  }
+  double below = __shfl_up(pm, 1, 64);
+  if (lane == 0) below = __builtin_huge_val();
+  FiltEntry f;
+  f.pm = below;
+  f.bobj = obj;
+  f.bmem = id == kNone ? __builtin_huge_val() : eval_one(a, id).mem;
+  filt[g * 64 + lane] = f;
 }
 
 int check_launch() {
@@ -728,20 +804,35 @@ int check_launch() {
   return e == hipSuccess ? 0 : (int)e;
 }
 
-template <int R>
-void launch_eval_r(const EvalArgs& a, int blocks, hipStream_t st) {
-  if (a.n_alpha > 0)
-    hipLaunchKernelGGL((k_eval<R, true>), dim3(blocks), dim3(kBlock), 0, st, a, a.ratio, (const PairK*)a.pk);
-  else
-    hipLaunchKernelGGL((k_eval<R, false>), dim3(blocks), dim3(kBlock), 0, st, a, a.ratio, (const PairK*)a.pk);
+template <int R, int MODE>
+void launch_eval_rm(const EvalArgs& a, int blocks, hipStream_t st) {
+  hipLaunchKernelGGL((k_eval<R, MODE>), dim3(blocks), dim3(kBlock), 0, st, a, a.ratio, (const PairK*)a.pk);
 }
 
 template <int R>
-int blocks_per_cu_r(bool alpha) {
+void launch_eval_r(const EvalArgs& a, int blocks, int mode, hipStream_t st) {
+  switch (mode) {
+    case kModeAlpha: launch_eval_rm<R, kModeAlpha>(a, blocks, st); break;
+    case kModeCount: launch_eval_rm<R, kModeCount>(a, blocks, st); break;
+    case kModeEmit: launch_eval_rm<R, kModeEmit>(a, blocks, st); break;
+    default: launch_eval_rm<R, kModeBuckets>(a, blocks, st); break;
+  }
+}
+
+template <int R, int MODE>
+int blocks_per_cu_rm() {
   int n = 0;
-  const hipError_t e = alpha ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_eval<R, true>, kBlock, 0)
-                             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_eval<R, false>, kBlock, 0);
-  return e == hipSuccess ? n : 1;
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_eval<R, MODE>, kBlock, 0) == hipSuccess ? n : 1;
+}
+
+template <int R>
+int blocks_per_cu_r(int mode) {
+  switch (mode) {
+    case kModeAlpha: return blocks_per_cu_rm<R, kModeAlpha>();
+    case kModeCount: return blocks_per_cu_rm<R, kModeCount>();
+    case kModeEmit: return blocks_per_cu_rm<R, kModeEmit>();
+    default: return blocks_per_cu_rm<R, kModeBuckets>();
+  }
 }
 
 #define MIST_FOR_EACH_R(X) \
@@ -749,11 +840,11 @@ int blocks_per_cu_r(bool alpha) {
 
 }  // namespace
 
-int eval_blocks_per_cu(int R, bool alpha) {
+int eval_blocks_per_cu(int R, int mode) {
   switch (R) {
 #define MIST_CASE(n) \
   case n:            \
-    return blocks_per_cu_r<n>(alpha);
+    return blocks_per_cu_r<n>(mode);
     MIST_FOR_EACH_R(MIST_CASE)
 #undef MIST_CASE
     default:
@@ -761,13 +852,13 @@ int eval_blocks_per_cu(int R, bool alpha) {
   }
 }
 
-int launch_eval(const EvalArgs& a, int blocks, void* stream) {
+int launch_eval(const EvalArgs& a, int blocks, int mode, void* stream) {
   if (a.n_tiles <= 0) return 0;
   hipStream_t st = (hipStream_t)stream;
   switch (a.R) {
-#define MIST_CASE(n)                 \
-  case n:                            \
-    launch_eval_r<n>(a, blocks, st); \
+#define MIST_CASE(n)                       \
+  case n:                                  \
+    launch_eval_r<n>(a, blocks, mode, st); \
     break;
     MIST_FOR_EACH_R(MIST_CASE)
 #undef MIST_CASE
@@ -788,6 +879,16 @@ int launch_reduce(const ReduceArgs& a, void* stream) {
   const int per = kReduceBlock / 64;
   const int64_t blocks = (a.n_groups + per - 1) / per;
   hipLaunchKernelGGL(k_reduce, dim3((unsigned)blocks), dim3(kReduceBlock), 0, (hipStream_t)stream, a);
+  return check_launch();
+}
+
+int launch_filter(const EvalArgs& a, const double* bucket_obj, const uint64_t* bucket_id, FiltEntry* filt,
+                  void* stream) {
+  if (a.n_groups <= 0) return 0;
+  const int per = kReduceBlock / 64;
+  const int64_t blocks = (a.n_groups + per - 1) / per;
+  hipLaunchKernelGGL(k_filter, dim3((unsigned)blocks), dim3(kReduceBlock), 0, (hipStream_t)stream, a, bucket_obj,
+                     bucket_id, filt);
   return check_launch();
 }
 

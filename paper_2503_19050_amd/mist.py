@@ -25,7 +25,7 @@ EXPORTS = [
     "mist_get_buckets",
     "mist_space_info", "mist_get_group_key", "mist_decode", "mist_eval_ids", "mist_set_timing",
     "mist_read_timing", "mist_launch_info", "mist_space_destroy", "mist_last_error",
-    "mist_plan_points", "mist_plan_pipeline",
+    "mist_plan_points", "mist_plan_pipeline", "mist_eval_pareto_exact", "mist_get_pareto_exact",
 ]
 
 
@@ -138,6 +138,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         L.mist_read_timing.argtypes = [vp, P(ctypes.c_double), P(ctypes.c_double), P(ctypes.c_int64)]
         L.mist_launch_info.argtypes = [vp, P(ctypes.c_int64), P(ctypes.c_int32), P(ctypes.c_int32)]
         L.mist_space_destroy.argtypes = [vp]
+        L.mist_eval_pareto_exact.argtypes = [vp, vp]
+        L.mist_get_pareto_exact.argtypes = [vp, ctypes.c_int64, P(Result), ctypes.c_int64, P(ctypes.c_int64)]
         L.mist_plan_points.argtypes = [P(StagePoint), ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P(Plan)]
         L.mist_plan_pipeline.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, P(Plan)]
         L.mist_last_error.restype = ctypes.c_char_p
@@ -271,6 +273,23 @@ class Space:
         cnt = ctypes.c_int32()
         _check(self.L, self.L.mist_get_pareto(self.h, g, out, 64, ctypes.byref(cnt)))
         return [_struct_to_dict(out[i]) for i in range(cnt.value)]
+
+    def eval_pareto_exact(self, stream=None) -> None:
+        """Exact (non-bucketed) time-vs-memory frontier of every group; after eval()."""
+        _check(self.L, self.L.mist_eval_pareto_exact(self.h, _stream_handle(stream)))
+
+    def pareto_exact(self, g: int) -> list[dict]:
+        """Group g's exact frontier in increasing memory (strictly decreasing objective)."""
+        n = ctypes.c_int64()
+        cap = 256
+        while True:
+            out = (Result * cap)()
+            rc = self.L.mist_get_pareto_exact(self.h, g, out, cap, ctypes.byref(n))
+            if rc == -5 and n.value > cap:
+                cap = n.value
+                continue
+            _check(self.L, rc)
+            return [_struct_to_dict(out[i]) for i in range(n.value)]
 
     def plan(self, hw: int = 0, pp: int = 0) -> dict | None:
         """The inter-stage plan (Eq. 1-3) of hardware sample hw from this space's frontier

@@ -1,0 +1,59 @@
+"""GPU exact (non-bucketed) time-vs-memory frontier against the oracle's sort-and-scan, through
+the C ABI: the same ids, objectives and memory, in the same order, for every checked group."""
+
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2503_19050_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "a GPU is required"
+    torch.cuda.init()
+    return torch
+
+
+def _tight():
+    wl = W.workload("tiny")
+    wl["hws"][0]["mem_bytes"] = 3.0e7
+    wl["name"] = "tight"
+    return wl
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny_llama", "tight", "c1", "c2", "c3", "c4", "c5"])
+def test_exact_frontier(name, torch_cuda):
+    from paper_2503_19050_amd import mist
+    wl = _tight() if name == "tight" else W.workload(name)
+    S = mist.from_workload(wl)
+    S.eval()
+    S.eval_pareto_exact()
+    torch_cuda.cuda.synchronize()
+    o = O.Oracle(wl)
+    if name in ("tiny", "tiny_llama", "tight", "c1"):
+        groups = range(o.n_groups)
+    else:
+        rng = np.random.default_rng(4)
+        groups = sorted({0, o.n_groups - 1} | set(int(g) for g in rng.choice(o.n_groups, size=6, replace=False)))
+    best = S.best(0, S.n_groups)
+    total = 0
+    for g in groups:
+        got = S.pareto_exact(g)
+        want = o.pareto_exact(g)
+        assert [r["id"] for r in got] == [int(i) for i in want["id"]], g
+        assert [r["obj"] for r in got] == list(want["obj"]) and [r["mem"] for r in got] == list(want["mem"]), g
+        if got:
+            assert got[-1]["obj"] == best[g]["obj"]
+        total += len(got)
+    say(name, "groups", len(groups), "frontier points", total)
+    S.close()

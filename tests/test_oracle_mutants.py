@@ -19,7 +19,7 @@ from oracle import oracle as O
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PINS = ["tests/test_oracle_pins.py", "tests/test_oracle_terms.py", "tests/test_oracle_reduce.py",
-        "tests/test_oracle_alpha.py"]
+        "tests/test_oracle_alpha.py", "tests/test_oracle_pareto.py"]
 
 MUTANTS = {
     "forward peak drops the optimizer-step unit": (
@@ -66,6 +66,11 @@ MUTANTS = {
     "weight-sampled argmin keeps the last of equal values": (
         "        if (lex_less(v, id, out_obj[o * n_alpha + a], out_id[o * n_alpha + a])) {",
         "        if (!(out_obj[o * n_alpha + a] < v)) {"),
+    "exact frontier keeps equal objectives": (
+        "    if (p.obj < run) {\n      if (n < cap)", "    if (p.obj <= run) {\n      if (n < cap)"),
+    "exact frontier ordered by objective first": (
+        "    if (a.mem != b.mem) return a.mem < b.mem;\n    if (a.obj != b.obj) return a.obj < b.obj;",
+        "    if (a.obj != b.obj) return a.obj < b.obj;\n    if (a.mem != b.mem) return a.mem < b.mem;"),
     "pipeline sends counted once for middle stages": (
         "(int64_t)((k > 1) + (k < PP))", "(int64_t)((k > 1) || (k < PP))"),
 }
