@@ -94,6 +94,9 @@ def main() -> int:
     ap.add_argument("--alphas", type=int, default=8,
                     help="after the headline run, also time the space with this many weight samples of "
                          "Eq. 4 (alpha = k/(n-1)); 0 skips it")
+    ap.add_argument("--exact-runs", type=int, default=10,
+                    help="after the headline run, time this many exact (non-bucketed) frontier passes "
+                         "(mist_eval_pareto_exact) on the evaluated space; 0 skips them")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="after the timed region, copy a buffer of this many MiB on the device "
                          "(a plain copy kernel of known size, to scale the HBM byte counters)")
@@ -165,6 +168,22 @@ def main() -> int:
                     "unit": "TFLOP/s", "frac": achieved / FP64_VECTOR_PEAK_TFLOPS, "traffic": traffic,
                     "kernel": "k_eval", "flops_per_config": fpc}
 
+    exact = None
+    if args.exact_runs > 0:
+        S.eval_pareto_exact()   # first pass allocates the candidate buffers
+        torch.cuda.synchronize()
+        runs = []
+        for _ in range(args.exact_runs):
+            t0 = time.perf_counter()
+            S.eval_pareto_exact()
+            torch.cuda.synchronize()
+            runs.append((time.perf_counter() - t0) * 1e3)
+        runs.sort()
+        exact = {"ms_per_run": runs[len(runs) // 2], "runs": len(runs),
+                 "what": "exact time-vs-memory frontier of every group after the evaluation: candidate filter, "
+                         "count and emit passes of the evaluation kernel, segmented sort by memory, scan; host "
+                         "wall time including its one synchronisation"}
+
     alpha = None
     if args.alphas > 0:
         A = args.alphas
@@ -207,7 +226,7 @@ def main() -> int:
         "extract_best_ms": extract_ms, "feasible_groups": feasible,
         "device": {"name": props.name, "cus": props.multi_processor_count,
                    "arch": getattr(props, "gcnArchName", "")},
-        "roofline": roofline, "cpu_baseline": cpu, "alpha_frontier": alpha,
+        "roofline": roofline, "cpu_baseline": cpu, "alpha_frontier": alpha, "exact_frontier": exact,
     }
     S.close()
     print(json.dumps(rec))
