@@ -57,3 +57,29 @@ def test_exact_frontier(name, torch_cuda):
         total += len(got)
     say(name, "groups", len(groups), "frontier points", total)
     S.close()
+
+
+def test_exact_and_plan_states(torch_cuda):
+    """The exact frontier needs an evaluation first and is read only after its own pass; a
+    space without weight samples still plans from each group's best."""
+    from paper_2503_19050_amd import mist
+    S = mist.from_workload(W.workload("tiny"))
+    with pytest.raises(mist.MistError) as e:
+        S.eval_pareto_exact()
+    assert e.value.status == -4
+    S.eval()
+    with pytest.raises(mist.MistError) as e:
+        S.pareto_exact(0)
+    assert e.value.status == -4
+    S.eval_pareto_exact()
+    assert S.pareto_exact(0)
+    with pytest.raises(mist.MistError):
+        S.pareto_exact(S.n_groups)
+    plan = S.plan(0)
+    assert plan is not None and sum(st["l"] for st in plan["stages"]) == W.workload("tiny")["model"]["n_layers"]
+    with pytest.raises(mist.MistError):
+        S.plan(1)      # no such hardware sample
+    S.eval()           # a new evaluation invalidates the exact frontier
+    with pytest.raises(mist.MistError):
+        S.pareto_exact(0)
+    S.close()
