@@ -261,6 +261,18 @@ __device__ __forceinline__ double interference_strip(const FirstRow& r, double h
   return T + remaining(x);
 }
 
+// Algorithm 1 on (c, g, +0, +0), c > 0: the first round uses the row of pattern 3 (compute and
+// GPU-GPU), after which at most one stream is positive and the other rounds leave the times
+// unchanged and add +0; with g = 0 the only row met has one stream and the time is c.  This
+// equals interference() on the same streams bit for bit.
+__device__ __forceinline__ double interference_zero(double c, double g, const double* __restrict__ tab) {
+  const double* e = tab + 3 * kLdsRow;
+  const double s0 = c * e[0], s1 = g * e[1];
+  const double ov = __builtin_fmin(s0, s1);
+  const double t = ov + __builtin_fmax((s0 - ov) * e[4], (s1 - ov) * e[5]);
+  return g > 0.0 ? t : c;
+}
+
 // K0: pair-level constants of every (group, pair).
 __global__ __launch_bounds__(256) void k_pairs(EvalArgs a) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -283,7 +295,8 @@ __global__ __launch_bounds__(256) void k_pairs(EvalArgs a) {
 //   - the first microbatch's streams start in the same pattern for every configuration of
 //     the strip (compute, GPU-GPU iff that stream carries traffic, and both host streams
 //     iff any offload ratio is non-zero), except the one configuration whose four ratios
-//     are all zero, which takes the looked-up path.
+//     are all zero: its host streams are exactly +0, and its time is computed once per
+//     strip in closed form (interference_zero).
 // Each wave keeps an LDS table of the 64 bucket minima of its current tile and writes it
 // as the tile's partials.
 // ---------------------------------------------------------------------------------------
@@ -345,7 +358,6 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
   __shared__ double s_tab[kWaves][16 * kLdsRow];
   __shared__ BucketEntry s_bucket[kWaves][65];  // entries NB..64: sinks of infeasible configurations
   __shared__ OoIn s_oo[kBlock];         // per-lane strip constants of the optimizer level
-  __shared__ double s_zero[kBlock][2];  // per-lane C and G2G (first microbatch) of the strip
   __shared__ double2 s_ab[AL ? kWaves : 1][kMaxAlphas];      // alpha * G, 1 - alpha
   __shared__ AlphaEntry s_aent[AL ? kWaves : 1][kMaxAlphas];
   __shared__ FiltEntry s_filt[EX ? kWaves : 1][EX ? 64 : 1];
@@ -444,9 +456,9 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
       fr.p2 = e1[6];
       fr.p3 = e1[7];
       const bool zero_strip = r0_zero && rw == 0.0 && rg == 0.0;
+      // First-microbatch time of the strip's all-zero configuration (no host streams).
+      const double T1z = interference_zero(K.C, Z.G2Gf, tab);
       s_oo[tid] = oo_inputs(P, K, Z, W);
-      s_zero[tid][0] = K.C;
-      s_zero[tid][1] = Z.G2Gf;
       const double A = K.A, KA = K.KA, A2 = P.A2, HW = W.HW, DG = W.DG;
       const unsigned int lid_strip = (unsigned int)s * (unsigned int)R2;
       // With a positive activation ratio both host streams run, so the stable microbatch's
@@ -485,9 +497,8 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
             const double mem = O.Bmax + SO;
             const double H2Df = __builtin_fma(ra, A, HW) * iP + O.H2Dx;
             const double D2Hf = __builtin_fma(ra, A, DG) * iP + O.D2Hx;
-            double T1;
-            if (ia == 0 && zero_oo) T1 = interference(s_zero[tid][0], s_zero[tid][1], H2Df, D2Hf, tab);
-            else T1 = interference_strip(fr, H2Df, D2Hf, tab);
+            double T1 = interference_strip(fr, H2Df, D2Hf, tab);
+            if (ia == 0) T1 = zero_oo ? T1z : T1;
             const double tv = tt[c];
             const double d = T1 - tv;
             const double obj = __builtin_fma(Gd, tv, d);
