@@ -111,7 +111,7 @@ def test_full_size_sampled_parity(name, torch_cuda):
     S.close()
 
 
-@pytest.mark.parametrize("name", ["c3", "c4"])
+@pytest.mark.parametrize("name", ["c3", "c4", "c5"])
 def test_full_parity_large(name, torch_cuda):
     """Every group of the full-size workloads against the oracle's whole-space run, stored as
     one digest per group by tests/golden/make_full_oracle.py (which calls only the oracle)."""
