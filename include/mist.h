@@ -85,11 +85,15 @@ typedef struct mist_hw_desc {
   double mem_bytes;  /* memory budget in bytes, > 0 (the Mem_Budget of Eq. 4) */
   double pcie_bw;    /* host<->device bytes/s, > 0 */
   double link_bw;    /* device<->device bytes/s, > 0 */
-  double eta_max;    /* compute efficiency eta(b) = eta_max*b*s/(b*s + n_half) */
+  double eta_max;    /* compute efficiency eta(b) = eta_max*b*s/(b*s + n_half); 0 selects
+                        eta_tab */
   double n_half;
   double phi[16][4]; /* phi[mask][j]: slowdown of stream j (0 compute, 1 GPU-GPU, 2 host->
                         device, 3 device->host) when the streams of mask co-run; >= 1 and
                         finite; entries of absent streams and single-stream masks unused */
+  double eta_tab[MIST_MAX_MB]; /* with eta_max = 0: measured efficiency of the space's i-th
+                        microbatch size (positive, finite), e.g. from mist_measure_eta (the
+                        operator database of Sec. 5.2.1); unused otherwise */
 } mist_hw_desc;
 
 /* The search space of Table 2 for every candidate stage. */
@@ -269,6 +273,101 @@ mist_status mist_read_timing(mist_space* S, double* eval_ms, double* reduce_ms, 
  * recomputed layers, ZeRO level, weight and gradient ratios). */
 mist_status mist_launch_info(const mist_space* S, int64_t* n_tiles, int32_t* block,
                              int32_t* strips_per_tile);
+
+/* ---------------------------------------------------------------------------------------
+ * Calibration of the cost model's constants on the current device.  Mist estimates compute
+ * time from an operator database benchmarked on the target hardware (Sec. 5.2.1) and fits one
+ * slowdown factor per co-running combination and participant from benchmarked co-runs of
+ * computation and communication kernels (Sec. 5.2.2, the fit after Algorithm 1).  The four
+ * streams are those of Algorithm 1: 0 compute, 1 GPU-GPU, 2 host->device, 3 device->host.
+ * --------------------------------------------------------------------------------------- */
+
+#define MIST_CORUN_MAX_UNITS 256
+#define MIST_CORUN_SAMPLES_PER_SHAPE 28 /* members of the 11 combinations of >= 2 streams */
+
+/* One unit of work of each stream. */
+typedef struct mist_corun_shape {
+  int64_t gemm_m, gemm_n, gemm_k; /* compute: one rocBLAS bf16 GEMM D = A^T B (A k x m, B k x n,
+                                     D m x n, column-major, fp32 accumulation), each in 1..2^31-1 */
+  int64_t g2g_bytes;  /* GPU-GPU: one device-to-device copy by a kernel of g2g_blocks workgroups
+                         (on one device this stands in for a collective's kernel: it occupies CUs
+                         and HBM, not a link); a positive multiple of 16 */
+  int64_t h2d_bytes;  /* host->device: one copy from pinned host memory, positive */
+  int64_t d2h_bytes;  /* device->host: one copy into pinned host memory, positive */
+} mist_corun_shape;
+
+typedef struct mist_corun mist_corun;
+
+/* Creates the benchmark's state on the current device: four streams of default priority plus
+ * a control stream, device buffers and pinned host buffers large enough for every field of
+ * *max, a rocBLAS handle and the events.  The operands hold pseudo-random values.  Errors:
+ * MIST_E_INVALID, MIST_E_NOMEM, MIST_E_DEVICE. */
+mist_status mist_corun_create(const mist_corun_shape* max, int32_t g2g_blocks, mist_corun** out);
+
+/* Runs the streams of mask (bit j = stream j) together: every member waits for one common
+ * start, then stream j runs units[j] (1..MIST_CORUN_MAX_UNITS; entries of non-members are
+ * ignored) units of shape *sh back to back with an event before the first and after each, and
+ * host t[j*stride + i] (i = 0..units[j]; stride > every units[j])
+ * receives the events' times in seconds after the common start.  Synchronous.  Errors:
+ * MIST_E_INVALID (mask, units, stride, or a shape field above the creation maximum),
+ * MIST_E_DEVICE. */
+mist_status mist_corun_run(mist_corun* C, int32_t mask, const mist_corun_shape* sh, const int32_t* units,
+                           double* t, int32_t stride);
+
+/* The all-running window of one run, host only: over the members j of mask the window is
+ * [max_j t[j*stride], min_j t[j*stride + units[j]]]; host mean[j] receives the mean duration of
+ * member j's units that lie entirely inside it and count[j] their number (NaN and 0 for
+ * non-members and for members without such a unit).  Inside the window the running streams are
+ * exactly those of mask, the situation a factor phi[mask][j] describes.  Errors:
+ * MIST_E_INVALID (empty mask, units < 1, stride too small, decreasing times). */
+mist_status mist_corun_reduce(int32_t mask, const double* t, int32_t stride, const int32_t* units,
+                              double* mean, int32_t* count);
+
+/* One benchmarked (combination, member, shape): mean unit times alone and inside the window. */
+typedef struct mist_corun_sample {
+  int32_t mask, stream, shape; /* shape: index into the shapes given to mist_corun_measure */
+  int32_t units;               /* co-run units inside the window */
+  double solo_s, corun_s;
+} mist_corun_sample;
+
+/* The co-run benchmark: for each shape k, every stream alone (units[j] = clamp(ceil(target_s /
+ * first-run unit time), 3, MIST_CORUN_MAX_UNITS)), then each of the 11 combinations of two or
+ * more streams with the same unit counts (once more with doubled counts if a member has no
+ * unit inside the window).  Writes MIST_CORUN_SAMPLES_PER_SHAPE samples per shape into host
+ * out, in shape, mask, stream order.  Errors: MIST_E_RANGE (cap too small; *n_out receives the
+ * count), MIST_E_INVALID, MIST_E_STATE (a member still without a unit inside its window),
+ * MIST_E_DEVICE. */
+mist_status mist_corun_measure(mist_corun* C, const mist_corun_shape* shapes, int32_t n_shapes,
+                               double target_s, mist_corun_sample* out, int32_t cap, int32_t* n_out);
+
+/* Frees the benchmark's state.  NULL is accepted. */
+mist_status mist_corun_destroy(mist_corun* C);
+
+/* Fits the slowdown factors to benchmarked co-runs, host only: for every combination of two or
+ * more streams and each member j, phi[mask*4 + j] = max(1, sum corun_s*solo_s / sum solo_s^2)
+ * over its samples (the least-squares factor from solo to co-run unit time; a measured speed-up
+ * is noise, the model's factors are slowdowns); every other entry of host phi[64] is 1.
+ * Errors: MIST_E_INVALID (a sample whose stream is not in its mask or whose times are not
+ * positive and finite, or a member of a combination without samples). */
+mist_status mist_fit_phi(const mist_corun_sample* s, int64_t n, double* phi);
+
+/* Algorithm 1 on one vector of stream times, host only: host x[4] (seconds, >= 0, finite) and
+ * factors host phi[64] (phi[mask*4 + j], finite and >= 1 for the members of combinations of
+ * two or more streams) give the overlapped time in *out, with the evaluation kernel's
+ * arithmetic (psi = 1/phi rounded once; updates while two or more streams are non-zero).
+ * Errors: MIST_E_INVALID. */
+mist_status mist_interference(const double* phi, const double* x, double* out);
+
+/* Operator database of one model on the current device: for each microbatch size mb[i] (n_mb
+ * in 1..MIST_MAX_MB), times the forward GEMMs of one transformer layer at tensor parallelism tp
+ * on mb[i]*seq tokens (query/key/value and output projections, the MLP's up (GPT) or gate+up
+ * (Llama) and down projections; rocBLAS bf16, weights transposed), one warm-up and reps >= 1
+ * timed runs, and writes host eta[i] = their FLOPs / median time / peak_flops and host sec[i] =
+ * the median time.  The attention core is not timed; the cost model applies the same
+ * efficiency to it.  Errors: MIST_E_INVALID (tp must divide heads, hidden and ffn), MIST_E_NOMEM,
+ * MIST_E_DEVICE. */
+mist_status mist_measure_eta(const mist_model_desc* m, const int32_t* mb, int32_t n_mb, int32_t tp,
+                             double peak_flops, int32_t reps, double* eta, double* sec);
 
 /* Frees every buffer of the space (through its allocator).  NULL is accepted. */
 mist_status mist_space_destroy(mist_space* S);

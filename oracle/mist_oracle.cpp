@@ -69,6 +69,8 @@ struct Hw {
   double eta_max;    // asymptotic compute efficiency
   double n_half;     // tokens at which efficiency is half of eta_max
   double phi[16][4]; // slowdown factors, [co-running mask][stream]
+  double eta_tab[16];  // with eta_max == 0: measured compute efficiency of the space's i-th
+                       // microbatch size (the operator database of Sec. 5.2.1)
 };
 
 struct Space {
@@ -196,7 +198,10 @@ bool build_ctx(Ctx& X, const Model* m, const Hw* hw, int32_t n_hw, const Space* 
   }
   for (const Hw& h : X.hw) {
     if (!(h.flops > 0 && h.mem_bytes > 0 && h.pcie_bw > 0 && h.link_bw > 0)) return false;
-    if (!(h.eta_max > 0 && h.n_half >= 0)) return false;
+    if (!(h.eta_max >= 0 && h.n_half >= 0)) return false;
+    if (h.eta_max == 0)
+      for (size_t i = 0; i < X.mb.size(); ++i)
+        if (!(h.eta_tab[i] > 0 && std::isfinite(h.eta_tab[i]))) return false;
     for (int mask = 0; mask < 16; ++mask)
       for (int j = 0; j < 4; ++j)
         if (!(h.phi[mask][j] >= 1.0 && std::isfinite(h.phi[mask][j]))) return false;
@@ -209,9 +214,14 @@ bool build_ctx(Ctx& X, const Model* m, const Hw* hw, int32_t n_hw, const Space* 
     X.inv_P.push_back(1.0 / h.pcie_bw);
     X.inv_L.push_back(1.0 / h.link_bw);
     std::vector<double> ie;
-    for (int32_t b : X.mb) {
+    for (size_t i = 0; i < X.mb.size(); ++i) {
+      if (h.eta_max == 0) {
+        // Measured efficiency of this microbatch size; its inverse.
+        ie.push_back(1.0 / h.eta_tab[i]);
+        continue;
+      }
       // Efficiency eta(b) = eta_max * bs / (bs + n_half); its inverse.
-      const double bs = exact((int64_t)b * m->seq);
+      const double bs = exact((int64_t)X.mb[i] * m->seq);
       const double num = bs + h.n_half;
       const double den = h.eta_max * bs;
       ie.push_back(num / den);

@@ -83,7 +83,7 @@ class _Model(ctypes.Structure):
 class _Hw(ctypes.Structure):
     _fields_ = [("flops", ctypes.c_double), ("mem_bytes", ctypes.c_double), ("pcie_bw", ctypes.c_double),
                 ("link_bw", ctypes.c_double), ("eta_max", ctypes.c_double), ("n_half", ctypes.c_double),
-                ("phi", ctypes.c_double * 64)]
+                ("phi", ctypes.c_double * 64), ("eta_tab", ctypes.c_double * 16)]
 
 
 class _Space(ctypes.Structure):
@@ -129,6 +129,8 @@ class Oracle:
                 setattr(self.hw[i], k, float(h[k]))
             flat = [float(v) for row in h["phi"] for v in row]
             self.hw[i].phi[:] = flat
+            tab = [float(v) for v in h.get("eta_tab", [])]
+            self.hw[i].eta_tab[:len(tab)] = tab
         self.n_hw = len(hws)
         self._mb = np.ascontiguousarray(s["mb"], dtype=np.int32)
         self._ratios = np.ascontiguousarray(s["ratios"], dtype=np.float64)

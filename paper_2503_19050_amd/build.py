@@ -2,9 +2,11 @@
 
 from __future__ import annotations
 
+import concurrent.futures
 import os
 import subprocess
 import sys
+import tempfile
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -12,7 +14,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmist.so")
 SOURCES = [os.path.join(CSRC, "mist_host.cpp"), os.path.join(CSRC, "mist_plan.cpp"),
-           os.path.join(CSRC, "mist_kernels.hip"), os.path.join(CSRC, "mist_exact.hip")]
+           os.path.join(CSRC, "mist_calib.cpp"), os.path.join(CSRC, "mist_kernels.hip"),
+           os.path.join(CSRC, "mist_exact.hip"), os.path.join(CSRC, "mist_corun.hip")]
+LIBS = ["-lrocblas"]  # the calibration's GEMMs
 HEADERS = [os.path.join(CSRC, "mist_internal.h"), os.path.join(INCLUDE, "mist.h")]
 
 ARCH = "gfx950"
@@ -28,13 +32,29 @@ FLAGS = [
 ]
 
 
-def build(out: str = LIB, extra: list[str] | None = None, verbose: bool = False) -> str:
-    """Compiles the library; always rebuilds."""
+def build(out: str = LIB, extra: list[str] | None = None, verbose: bool = False,
+          sources: list[str] | None = None, include: list[str] | None = None) -> str:
+    """Compiles the library (every source in its own hipcc process, in parallel) and links it;
+    always rebuilds."""
     tmp = out + ".tmp%d" % os.getpid()
-    cmd = ["hipcc", *FLAGS, *(extra or []), "-I", INCLUDE, "-I", CSRC, *SOURCES, "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), file=sys.stderr)
-    subprocess.run(cmd, check=True)
+    srcs = sources or SOURCES
+    inc = [a for d in (include or [CSRC]) + [INCLUDE] for a in ("-I", d)]
+    with tempfile.TemporaryDirectory(prefix="mist_build_") as objdir:
+        def compile_one(i_src):
+            i, src = i_src
+            obj = os.path.join(objdir, "%d_%s.o" % (i, os.path.basename(src)))
+            cmd = ["hipcc", *FLAGS, *(extra or []), *inc, "-c", src, "-o", obj]
+            cmd.remove("-shared")
+            if verbose:
+                print(" ".join(cmd), file=sys.stderr)
+            subprocess.run(cmd, check=True)
+            return obj
+        with concurrent.futures.ThreadPoolExecutor(max_workers=len(srcs)) as ex:
+            objs = list(ex.map(compile_one, enumerate(srcs)))
+        cmd = ["hipcc", *FLAGS, *(extra or []), *objs, *LIBS, "-o", tmp]
+        if verbose:
+            print(" ".join(cmd), file=sys.stderr)
+        subprocess.run(cmd, check=True)
     os.replace(tmp, out)
     return out
 

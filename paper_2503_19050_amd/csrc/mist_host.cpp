@@ -186,8 +186,12 @@ std::string validate(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n
     const double v[4] = {h.flops, h.mem_bytes, h.pcie_bw, h.link_bw};
     for (double x : v)
       if (!(x > 0.0) || !std::isfinite(x)) return "hardware rates and memory must be positive and finite";
-    if (!(h.eta_max > 0.0) || !std::isfinite(h.eta_max) || !(h.n_half >= 0.0) || !std::isfinite(h.n_half))
-      return "eta_max must be positive and n_half non-negative";
+    if (!(h.eta_max >= 0.0) || !std::isfinite(h.eta_max) || !(h.n_half >= 0.0) || !std::isfinite(h.n_half))
+      return "eta_max and n_half must be non-negative and finite";
+    if (h.eta_max == 0.0 && s && s->mb && s->n_mb >= 1 && s->n_mb <= MIST_MAX_MB)
+      for (int32_t j = 0; j < s->n_mb; ++j)
+        if (!(h.eta_tab[j] > 0.0) || !std::isfinite(h.eta_tab[j]))
+          return "with eta_max = 0 every eta_tab entry of the microbatch list must be positive and finite";
     for (int mask = 0; mask < 16; ++mask) {
       if (popcount4(mask) < 2) continue;
       for (int j = 0; j < 4; ++j)
@@ -354,6 +358,10 @@ std::string enumerate(mist_space* S) {
     d.kNB = ((double)S->NB / h.mem_bytes) * (1.0 - 0x1p-40);
     for (int j = 0; j < MIST_MAX_MB; ++j) d.ieta[j] = 0.0;
     for (size_t j = 0; j < S->mb.size(); ++j) {
+      if (h.eta_max == 0.0) {  // measured efficiency of this microbatch size
+        d.ieta[j] = 1.0 / h.eta_tab[j];
+        continue;
+      }
       const double bs = (double)((int64_t)S->mb[j] * m.seq);
       d.ieta[j] = (bs + h.n_half) / (h.eta_max * bs);
     }
@@ -1138,5 +1146,5 @@ const char* mist_last_error(void) { return g_error.c_str(); }
 }  // extern "C"
 
 namespace mist {
-__attribute__((visibility("hidden"))) mist_status plan_fail(mist_status code, const std::string& msg) { return fail(code, msg); }
+__attribute__((visibility("hidden"))) mist_status lib_fail(mist_status code, const std::string& msg) { return fail(code, msg); }
 }  // namespace mist

@@ -26,7 +26,7 @@
 #include "mist.h"
 
 namespace mist {
-__attribute__((visibility("hidden"))) mist_status plan_fail(mist_status code, const std::string& msg);  // sets the thread's error
+__attribute__((visibility("hidden"))) mist_status lib_fail(mist_status code, const std::string& msg);  // sets the thread's error
 }
 
 namespace {
@@ -84,9 +84,9 @@ double plan_value(int32_t G, const std::vector<double>& t, const std::vector<dou
 
 extern "C" mist_status mist_plan_points(const mist_stage_point* pts, int64_t n, int32_t n_layers, int32_t pp,
                                         mist_plan* out) {
-  using mist::plan_fail;
-  if (!out || (!pts && n > 0)) return plan_fail(MIST_E_INVALID, "null argument");
-  if (n < 0 || n_layers < 1 || pp < 0 || pp > MIST_MAX_STAGES) return plan_fail(MIST_E_INVALID, "argument out of range");
+  using mist::lib_fail;
+  if (!out || (!pts && n > 0)) return lib_fail(MIST_E_INVALID, "null argument");
+  if (n < 0 || n_layers < 1 || pp < 0 || pp > MIST_MAX_STAGES) return lib_fail(MIST_E_INVALID, "argument out of range");
   try {
     std::memset(out, 0, sizeof(*out));
     out->F = std::numeric_limits<double>::infinity();
@@ -95,7 +95,7 @@ extern "C" mist_status mist_plan_points(const mist_stage_point* pts, int64_t n, 
     for (int64_t i = 0; i < n; ++i) {
       const mist_stage_point& p = pts[i];
       if (p.PP < 1 || p.k < 1 || p.k > p.PP || p.l < 1 || p.G < 1 || !std::isfinite(p.t) || !std::isfinite(p.d))
-        return plan_fail(MIST_E_INVALID, "invalid stage point");
+        return lib_fail(MIST_E_INVALID, "invalid stage point");
       if (p.PP > MIST_MAX_STAGES || (pp && p.PP != pp)) continue;
       cand[{p.G, p.PP}][p.k][p.l].push_back(Pt{p.t, p.d, p.id});
     }
@@ -176,6 +176,6 @@ extern "C" mist_status mist_plan_points(const mist_stage_point* pts, int64_t n, 
     }
     return MIST_OK;
   } catch (const std::bad_alloc&) {
-    return plan_fail(MIST_E_NOMEM, "host allocation failed");
+    return lib_fail(MIST_E_NOMEM, "host allocation failed");
   }
 }

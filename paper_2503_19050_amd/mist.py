@@ -26,6 +26,8 @@ EXPORTS = [
     "mist_space_info", "mist_get_group_key", "mist_decode", "mist_eval_ids", "mist_set_timing",
     "mist_read_timing", "mist_launch_info", "mist_space_destroy", "mist_last_error",
     "mist_plan_points", "mist_plan_pipeline", "mist_eval_pareto_exact", "mist_get_pareto_exact",
+    "mist_corun_create", "mist_corun_run", "mist_corun_reduce", "mist_corun_measure", "mist_corun_destroy",
+    "mist_fit_phi", "mist_interference", "mist_measure_eta",
 ]
 
 
@@ -45,7 +47,7 @@ class ModelDesc(ctypes.Structure):
 class HwDesc(ctypes.Structure):
     _fields_ = [("flops", ctypes.c_double), ("mem_bytes", ctypes.c_double), ("pcie_bw", ctypes.c_double),
                 ("link_bw", ctypes.c_double), ("eta_max", ctypes.c_double), ("n_half", ctypes.c_double),
-                ("phi", (ctypes.c_double * 4) * 16)]
+                ("phi", (ctypes.c_double * 4) * 16), ("eta_tab", ctypes.c_double * 16)]
 
 
 class SpaceDesc(ctypes.Structure):
@@ -57,6 +59,18 @@ class SpaceDesc(ctypes.Structure):
 
 
 MAX_STAGES = 64
+CORUN_MAX_UNITS = 256
+CORUN_SAMPLES_PER_SHAPE = 28
+
+
+class CorunShape(ctypes.Structure):
+    _fields_ = [("gemm_m", ctypes.c_int64), ("gemm_n", ctypes.c_int64), ("gemm_k", ctypes.c_int64),
+                ("g2g_bytes", ctypes.c_int64), ("h2d_bytes", ctypes.c_int64), ("d2h_bytes", ctypes.c_int64)]
+
+
+class CorunSample(ctypes.Structure):
+    _fields_ = [("mask", ctypes.c_int32), ("stream", ctypes.c_int32), ("shape", ctypes.c_int32),
+                ("units", ctypes.c_int32), ("solo_s", ctypes.c_double), ("corun_s", ctypes.c_double)]
 
 
 class StagePoint(ctypes.Structure):
@@ -142,6 +156,18 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         L.mist_get_pareto_exact.argtypes = [vp, ctypes.c_int64, P(Result), ctypes.c_int64, P(ctypes.c_int64)]
         L.mist_plan_points.argtypes = [P(StagePoint), ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P(Plan)]
         L.mist_plan_pipeline.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, P(Plan)]
+        dp = P(ctypes.c_double)
+        ip = P(ctypes.c_int32)
+        L.mist_corun_create.argtypes = [P(CorunShape), ctypes.c_int32, P(vp)]
+        L.mist_corun_run.argtypes = [vp, ctypes.c_int32, P(CorunShape), ip, dp, ctypes.c_int32]
+        L.mist_corun_reduce.argtypes = [ctypes.c_int32, dp, ctypes.c_int32, ip, dp, ip]
+        L.mist_corun_measure.argtypes = [vp, P(CorunShape), ctypes.c_int32, ctypes.c_double, P(CorunSample),
+                                         ctypes.c_int32, ip]
+        L.mist_corun_destroy.argtypes = [vp]
+        L.mist_fit_phi.argtypes = [P(CorunSample), ctypes.c_int64, dp]
+        L.mist_interference.argtypes = [dp, dp, dp]
+        L.mist_measure_eta.argtypes = [P(ModelDesc), ip, ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
+                                       ctypes.c_int32, dp, dp]
         L.mist_last_error.restype = ctypes.c_char_p
         for name in EXPORTS:
             if name != "mist_last_error":
@@ -190,6 +216,8 @@ class Space:
             for m in range(16):
                 for j in range(4):
                     self._hw[i].phi[m][j] = float(h["phi"][m][j])
+            tab = [float(v) for v in h.get("eta_tab", [])]
+            self._hw[i].eta_tab[:len(tab)] = tab
         self._mb = np.ascontiguousarray(space["mb"], dtype=np.int32)
         self._ratios = np.ascontiguousarray(space["ratios"], dtype=np.float64)
         self._alphas = np.ascontiguousarray(space.get("alphas", []), dtype=np.float64)
@@ -371,3 +399,116 @@ def plan_points(points, n_layers: int, pp: int = 0) -> dict | None:
     out = Plan()
     _check(L, L.mist_plan_points(arr, len(pts), n_layers, pp, ctypes.byref(out)))
     return _plan_dict(out)
+
+
+# -- calibration ------------------------------------------------------------------------------
+def _dptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _iptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _shape(sh: dict) -> CorunShape:
+    return CorunShape(*(int(sh[k]) for k, _ in CorunShape._fields_))
+
+
+def corun_reduce(mask: int, t, units) -> tuple[np.ndarray, np.ndarray]:
+    """mist_corun_reduce: t[j] are stream j's timestamps (seconds); returns (mean[4], count[4])."""
+    L = load()
+    u = np.zeros(4, dtype=np.int32)
+    for j in range(4):
+        u[j] = units[j]
+    stride = int(max([u.max(), 1] + [len(x) - 1 for x in t])) + 1
+    tt = np.zeros((4, stride))
+    for j in range(4):
+        if mask >> j & 1:
+            tt[j, :len(t[j])] = t[j]
+    mean = np.zeros(4)
+    count = np.zeros(4, dtype=np.int32)
+    _check(L, L.mist_corun_reduce(int(mask), _dptr(tt), stride, _iptr(u), _dptr(mean), _iptr(count)))
+    return mean, count
+
+
+def fit_phi(samples) -> np.ndarray:
+    """mist_fit_phi: samples are (mask, stream, solo_s, corun_s) tuples or dicts; returns phi[16][4]."""
+    L = load()
+    arr = (CorunSample * max(len(samples), 1))()
+    for i, x in enumerate(samples):
+        if isinstance(x, dict):
+            arr[i] = CorunSample(x["mask"], x["stream"], x.get("shape", 0), x.get("units", 0), x["solo_s"], x["corun_s"])
+        else:
+            arr[i] = CorunSample(int(x[0]), int(x[1]), 0, 0, float(x[2]), float(x[3]))
+    phi = np.zeros(64)
+    _check(L, L.mist_fit_phi(arr, len(samples), _dptr(phi)))
+    return phi.reshape(16, 4)
+
+
+def interference(phi, x) -> float:
+    """mist_interference: Algorithm 1 on stream times x[4] with factors phi[16][4]."""
+    L = load()
+    p = np.ascontiguousarray(phi, dtype=np.float64).reshape(64)
+    xx = np.ascontiguousarray(x, dtype=np.float64).reshape(4)
+    out = ctypes.c_double()
+    _check(L, L.mist_interference(_dptr(p), _dptr(xx), ctypes.byref(out)))
+    return out.value
+
+
+def measure_eta(model: dict, mb, tp: int, peak_flops: float, reps: int = 5) -> tuple[np.ndarray, np.ndarray]:
+    """mist_measure_eta on the current device: (eta[i], seconds[i]) per microbatch size mb[i]."""
+    L = load()
+    m = ModelDesc(**{k: model[k] for k, _ in ModelDesc._fields_})
+    b = np.ascontiguousarray(mb, dtype=np.int32)
+    eta = np.zeros(len(b))
+    sec = np.zeros(len(b))
+    _check(L, L.mist_measure_eta(ctypes.byref(m), _iptr(b), len(b), int(tp), float(peak_flops), int(reps),
+                                 _dptr(eta), _dptr(sec)))
+    return eta, sec
+
+
+class Corun:
+    """The co-run benchmark's device state (mist_corun_create) on the current device."""
+
+    def __init__(self, max_shape: dict, g2g_blocks: int = 16):
+        self.L = load()
+        h = ctypes.c_void_p()
+        _check(self.L, self.L.mist_corun_create(ctypes.byref(_shape(max_shape)), int(g2g_blocks), ctypes.byref(h)))
+        self.h = h
+
+    def run(self, mask: int, shape: dict, units) -> list[np.ndarray]:
+        """Timestamps (seconds after the common start) of each member's units."""
+        u = np.zeros(4, dtype=np.int32)
+        for j in range(4):
+            u[j] = units[j]
+        stride = CORUN_MAX_UNITS + 1
+        t = np.zeros((4, stride))
+        _check(self.L, self.L.mist_corun_run(self.h, int(mask), ctypes.byref(_shape(shape)), _iptr(u), _dptr(t),
+                                             stride))
+        return [t[j, :u[j] + 1].copy() if mask >> j & 1 else np.zeros(0) for j in range(4)]
+
+    def measure(self, shapes, target_s: float = 0.02) -> list[dict]:
+        arr = (CorunShape * len(shapes))(*[_shape(s) for s in shapes])
+        cap = len(shapes) * CORUN_SAMPLES_PER_SHAPE
+        out = (CorunSample * cap)()
+        n = ctypes.c_int32()
+        _check(self.L, self.L.mist_corun_measure(self.h, arr, len(shapes), float(target_s), out, cap,
+                                                 ctypes.byref(n)))
+        return [_struct_to_dict(out[i]) for i in range(n.value)]
+
+    def close(self) -> None:
+        if getattr(self, "h", None):
+            _check(self.L, self.L.mist_corun_destroy(self.h))
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

@@ -161,6 +161,20 @@ def workload(name: str) -> dict:
 WORKLOADS = ["c1", "c2", "c3", "c4", "c5"]
 
 
+def with_eta_table(wl: dict, seed: int, lo: float = 0.30, hi: float = 0.90) -> dict:
+    """Copy of a workload whose hardware samples take a measured-style efficiency table in place of
+    the formula: eta_max = 0 and one efficiency per microbatch size drawn U[lo, hi] from
+    SplitMix64(seed + sample index), in microbatch order (the shape of an operator-database
+    table; the values are synthetic)."""
+    out = copy.deepcopy(wl)
+    n = len(out["space"]["mb"])
+    for i, hw in enumerate(out["hws"]):
+        g = SplitMix64(seed + i)
+        hw["eta_max"] = 0.0
+        hw["eta_tab"] = [lo + (hi - lo) * g.uniform() for _ in range(n)]
+    return out
+
+
 def scaled(wl: dict, *, flops=1.0, pcie=1.0, link=1.0, mem=1.0) -> dict:
     """Copy of a workload with every hardware sample's scalars multiplied."""
     out = copy.deepcopy(wl)
