@@ -333,10 +333,11 @@ typedef struct mist_corun_sample {
 /* The co-run benchmark: for each shape k, every stream alone (units[j] = clamp(ceil(target_s /
  * first-run unit time), 3, MIST_CORUN_MAX_UNITS)), then each of the 11 combinations of two or
  * more streams with the same unit counts (once more with doubled counts if a member has no
- * unit inside the window).  Writes MIST_CORUN_SAMPLES_PER_SHAPE samples per shape into host
- * out, in shape, mask, stream order.  Errors: MIST_E_RANGE (cap too small; *n_out receives the
- * count), MIST_E_INVALID, MIST_E_STATE (a member still without a unit inside its window),
- * MIST_E_DEVICE. */
+ * unit inside the window).  A member that still has none was starved while the others ran: its
+ * sample gets units = 0 and corun_s = the window's length, a lower bound of its unit time.
+ * Writes MIST_CORUN_SAMPLES_PER_SHAPE samples per shape into host out, in shape, mask, stream
+ * order.  Errors: MIST_E_RANGE (cap too small; *n_out receives the count), MIST_E_INVALID,
+ * MIST_E_STATE (a window is empty: the streams never ran together), MIST_E_DEVICE. */
 mist_status mist_corun_measure(mist_corun* C, const mist_corun_shape* shapes, int32_t n_shapes,
                                double target_s, mist_corun_sample* out, int32_t cap, int32_t* n_out);
 

@@ -318,19 +318,32 @@ mist_status mist_corun_measure(mist_corun* C, const mist_corun_shape* shapes, in
     for (int mask = 3; mask < 16; ++mask) {
       if (popcount4(mask) < 2) continue;
       int32_t V[4] = {U[0], U[1], U[2], U[3]};
-      bool ok = false;
-      for (int attempt = 0; attempt < 2 && !ok; ++attempt) {
+      for (int attempt = 0; attempt < 2; ++attempt) {
+        if (attempt) {  // a member had no whole unit inside the window: once more, twice as long
+          bool grown = false;
+          for (int j = 0; j < 4; ++j) {
+            const int32_t v = std::min(MIST_CORUN_MAX_UNITS, 2 * V[j]);
+            grown = grown || v != V[j];
+            V[j] = v;
+          }
+          if (!grown) break;
+        }
         mist_status st = mist_corun_run(C, mask, &sh, V, t.data(), stride);
         if (!st) st = mist_corun_reduce(mask, t.data(), stride, V, mean, count);
         if (st) return st;
-        ok = true;
+        bool ok = true;
         for (int j = 0; j < 4; ++j)
           if ((mask >> j & 1) && !(count[j] > 0 && mean[j] > 0.0)) ok = false;
-        for (int j = 0; j < 4; ++j) V[j] = std::min(MIST_CORUN_MAX_UNITS, 2 * V[j]);
+        if (ok) break;
       }
-      if (!ok)
-        return lib_fail(MIST_E_STATE, "shape " + std::to_string(k) + ", mask " + std::to_string(mask) +
-                                          ": a member has no whole unit inside the all-running window");
+      // A member starved for the whole window (its one unit there spans it) gets the window's
+      // length: a lower bound of its co-run unit time.
+      double lo = -HUGE_VAL, hi = HUGE_VAL;
+      for (int j = 0; j < 4; ++j) {
+        if (!(mask >> j & 1)) continue;
+        lo = std::max(lo, t[(size_t)j * stride]);
+        hi = std::min(hi, t[(size_t)j * stride + V[j]]);
+      }
       for (int j = 0; j < 4; ++j) {
         if (!(mask >> j & 1)) continue;
         mist_corun_sample& x = out[n++];
@@ -339,7 +352,10 @@ mist_status mist_corun_measure(mist_corun* C, const mist_corun_shape* shapes, in
         x.shape = k;
         x.units = count[j];
         x.solo_s = solo[j];
-        x.corun_s = mean[j];
+        x.corun_s = count[j] > 0 ? mean[j] : hi - lo;
+        if (!(x.corun_s > 0.0))
+          return lib_fail(MIST_E_STATE, "shape " + std::to_string(k) + ", mask " + std::to_string(mask) +
+                                            ": the streams never ran together");
       }
     }
   }

@@ -86,7 +86,7 @@ def test_corun_measure_and_fit(torch_cuda):
     assert len(samples) == 2 * mist.CORUN_SAMPLES_PER_SHAPE
     for x in samples:
         assert x["mask"] >> x["stream"] & 1 and bin(x["mask"]).count("1") >= 2
-        assert x["units"] >= 1
+        assert x["units"] >= 0     # 0: starved for the whole window (corun_s is its length)
         assert 0.0 < x["solo_s"] < 1.0 and 0.0 < x["corun_s"] < 1.0
     phi = mist.fit_phi(samples)
     assert np.all(np.isfinite(phi)) and np.all(phi >= 1.0) and np.all(phi < 100.0)
