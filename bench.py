@@ -38,11 +38,14 @@ def kernel_hash() -> str:
 
 
 def flops_per_config(name: str):
+    """(FP64 operations of the definition for one configuration on its own, the same with every
+    level shared among the configurations below it, as the oracle's loops evaluate it)."""
     try:
         with open(FLOPS_FILE) as f:
-            return json.load(f)["workloads"][name]["flops_per_config"]
+            w = json.load(f)["workloads"][name]
+            return w["flops_per_config"], w["flops_per_config_shared_levels"]
     except (OSError, KeyError, ValueError):
-        return None
+        return None, None
 
 
 def traffic_record(name: str, n_launch_configs: int):
@@ -159,14 +162,17 @@ def main() -> int:
     value = S.n_configs / (ms_per_step / 1e3)
     k1_avg = k1_ms / n
     k2_avg = k2_ms / n
-    fpc = flops_per_config(wl["name"])
+    fpc, fsh = flops_per_config(wl["name"])
     roofline = None
     if fpc is not None:
         achieved = fpc * S.n_configs / (k1_avg / 1e3) / 1e12
+        shared = fsh * S.n_configs / (k1_avg / 1e3) / 1e12
         traffic = traffic_record(wl["name"], S.n_configs)
         roofline = {"bound": "alu", "achieved": achieved, "peak": FP64_VECTOR_PEAK_TFLOPS,
                     "unit": "TFLOP/s", "frac": achieved / FP64_VECTOR_PEAK_TFLOPS, "traffic": traffic,
-                    "kernel": "k_eval", "flops_per_config": fpc}
+                    "kernel": "k_eval", "flops_per_config": fpc,
+                    "flops_per_config_shared_levels": fsh,
+                    "frac_shared_levels": shared / FP64_VECTOR_PEAK_TFLOPS}
 
     exact = None
     if args.exact_runs > 0:

@@ -843,4 +843,21 @@ int orc_count_flops(const Model* m, const Hw* hw, int32_t n_hw, const Space* s, 
   return 0;
 }
 
+// FP64 operations of the definition for single configurations evaluated from scratch: every
+// level of ids[i] once, nothing shared with other configurations.
+int orc_count_flops_ids(const Model* m, const Hw* hw, int32_t n_hw, const Space* s, const uint64_t* ids,
+                        int64_t n, uint64_t* flops) {
+  Ctx X;
+  if (!build_ctx(X, m, hw, n_hw, s)) return -1;
+  g_flops = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    const int gi = find_group(X, ids[i]);
+    if (gi < 0) return -5;
+    const Group& g = X.groups[gi];
+    walk_group<Counted>(X, g, single_box(X, g, ids[i] - g.base), nullptr, [](int64_t, double, double, double, double) {});
+  }
+  *flops = g_flops;
+  return 0;
+}
+
 }  // extern "C"

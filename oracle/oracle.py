@@ -67,6 +67,7 @@ def lib() -> ctypes.CDLL:
                                                ctypes.c_int64, P(ctypes.c_uint64), P(ctypes.c_double)]
             L.orc_pareto_exact.argtypes = args + [ctypes.c_int64, P(ctypes.c_uint64), P(ctypes.c_double),
                                                   P(ctypes.c_double), ctypes.c_int64, P(ctypes.c_int64)]
+            L.orc_count_flops_ids.argtypes = args + [P(ctypes.c_uint64), ctypes.c_int64, P(ctypes.c_uint64)]
             L.orc_interference.argtypes = [P(ctypes.c_double), P(ctypes.c_double)]
             L.orc_interference.restype = ctypes.c_double
             _lib = L
@@ -228,6 +229,15 @@ class Oracle:
         c = ctypes.c_uint64()
         self._check(self.L.orc_count_flops(*self._args(), g0, g1, ctypes.byref(f), ctypes.byref(c)))
         return f.value, c.value
+
+
+    def count_flops_ids(self, ids) -> int:
+        """FP64 operations of the definition for the given configurations, each evaluated from
+        scratch (no level shared between configurations)."""
+        a = np.ascontiguousarray(ids, dtype=np.uint64)
+        f = ctypes.c_uint64()
+        self._check(self.L.orc_count_flops_ids(*self._args(), _up(a), len(a), ctypes.byref(f)))
+        return f.value
 
 
 def interference(X, phi) -> float:

@@ -1,9 +1,16 @@
-"""Writes flops_per_config.json: FP64 operations of the cost-model definition per
-configuration, counted by the oracle's counting build (add/sub/mul 1, fma 2,
-min/max/compare 0) with each loop level counted once per combination of its digits.
+"""Writes flops_per_config.json: FP64 operations of the cost-model definition per configuration,
+counted by the oracle's counting build (add/sub/mul 1, fma 2, min/max/compare 0).
 
-c1 and c2 are counted over every group; c3-c5 over every 16th group (the count per
-configuration depends on the data only through Algorithm 1's pattern changes).
+Two counts per workload:
+
+* ``flops_per_config`` -- the definition evaluated for one configuration on its own: every level
+  of the listing (pair, recomputation, ZeRO, offload levels, both runs of Algorithm 1, the
+  objective) once, nothing shared with another configuration.  Averaged over every
+  configuration of c1 and over 2,000,000 evenly spaced configurations of c2-c5 (the count
+  depends on the data only through Algorithm 1's pattern changes).
+* ``flops_per_config_shared_levels`` -- the oracle's nested loops, which evaluate each level once
+  per combination of its digits and share it with every configuration below it; c1 and c2 over
+  every group, c3-c5 over every 16th group.
 
 Run: python tests/golden/make_flops.py   (calls only oracle/)
 """
@@ -13,17 +20,33 @@ import os
 import sys
 from concurrent.futures import ProcessPoolExecutor
 
+import numpy as np
+
 HERE = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, os.path.dirname(os.path.dirname(HERE)))
 
 from oracle import oracle as O  # noqa: E402
 from paper_2503_19050_amd import workloads as W  # noqa: E402
 
+SAMPLE = 2_000_000
+CHUNK = 100_000
 
-def _count(args):
+
+def _count_groups(args):
     name, g = args
     o = O.Oracle(W.workload(name))
     return o.count_flops(g, g + 1)
+
+
+def _count_ids(args):
+    name, k0, k1, n_ids, n_configs = args
+    o = O.Oracle(W.workload(name))
+    if n_ids >= n_configs:
+        ids = np.arange(k0, k1, dtype=np.uint64)
+    else:  # evenly spaced: id_k = floor((k + 1/2) * n_configs / n_ids)
+        k = np.arange(k0, k1, dtype=np.float64)
+        ids = np.floor((k + 0.5) * (n_configs / n_ids)).astype(np.uint64)
+    return o.count_flops_ids(ids), len(ids)
 
 
 def main():
@@ -31,14 +54,21 @@ def main():
     with ProcessPoolExecutor(max_workers=os.cpu_count()) as ex:
         for name in W.WORKLOADS:
             o = O.Oracle(W.workload(name))
+            n_ids = min(SAMPLE, o.n_configs)
+            jobs = [(name, k0, min(k0 + CHUNK, n_ids), n_ids, o.n_configs) for k0 in range(0, n_ids, CHUNK)]
+            res = list(ex.map(_count_ids, jobs))
+            single = sum(r[0] for r in res) / sum(r[1] for r in res)
             stride = 1 if name in ("c1", "c2") else 16
             groups = list(range(0, o.n_groups, stride))
-            res = list(ex.map(_count, [(name, g) for g in groups], chunksize=4))
+            res = list(ex.map(_count_groups, [(name, g) for g in groups], chunksize=4))
             flops = sum(r[0] for r in res)
             configs = sum(r[1] for r in res)
-            out["workloads"][name] = {"flops_per_config": flops / configs, "groups_counted": len(groups),
-                                      "group_stride": stride, "configs_counted": configs}
-            print(name, flops / configs, configs, flush=True)
+            out["workloads"][name] = {
+                "flops_per_config": single, "configs_sampled": n_ids,
+                "sample": "every configuration" if n_ids >= o.n_configs else "evenly spaced ids",
+                "flops_per_config_shared_levels": flops / configs, "groups_counted": len(groups),
+                "group_stride": stride, "configs_counted": configs}
+            print(name, single, flops / configs, flush=True)
     with open(os.path.join(HERE, "flops_per_config.json"), "w") as f:
         json.dump(out, f, indent=1)
 
