@@ -1,9 +1,11 @@
 // Exact time-vs-memory frontier (the staircase without memory buckets), second stage.  The
-// candidates of every group are put in (mem, obj, id) order by three stable segmented radix
-// sorts (rocPRIM), least significant key first: id, then the objective's bit pattern, then the
-// memory's (non-negative doubles order like their bit patterns).  In that order a candidate is
-// on the frontier exactly when its objective is below the minimum of every candidate before
-// it, a segmented prefix minimum: one wave per group walks its candidates in chunks of 64.
+// candidates of every group are sorted by memory with one segmented radix sort (rocPRIM; a
+// non-negative double orders like its bit pattern).  In (mem, obj, id) order a candidate is on the
+// frontier exactly when its objective is below that of every candidate before it; within a run of
+// equal memory only the run's (obj, id) minimum can be, and it is when its objective is below the
+// minima of every earlier run.  So the sort by memory alone suffices: one wave per group walks
+// its candidates in chunks of 64, reduces each run to its minimum (a segmented scan across the
+// lanes, carried over chunk boundaries) and keeps the runs that lower the running minimum.
 #include <hip/hip_runtime.h>
 
 #include <rocprim/device/device_segmented_radix_sort.hpp>
@@ -20,16 +22,16 @@ __global__ __launch_bounds__(256) void k_iota(uint32_t* __restrict__ idx, int64_
   if (i < n) idx[i] = (uint32_t)i;
 }
 
-// key[i] = src[idx[i]] (the next sort key in the current order).
-__global__ __launch_bounds__(256) void k_gather(const uint64_t* __restrict__ src, const uint32_t* __restrict__ idx,
-                                                uint64_t* __restrict__ key, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) key[i] = src[idx[i]];
+constexpr uint64_t kNoKey = ~0ull;  // no memory value has this bit pattern (it is a NaN)
+
+__device__ __forceinline__ bool lex_less(double o1, uint64_t i1, double o2, uint64_t i2) {
+  return o1 < o2 || (o1 == o2 && i1 < i2);
 }
 
-// One wave per group: candidates [seg[g], seg[g+1]) in (mem, obj, id) order.
+// One wave per group: candidates [seg[g], seg[g+1]) sorted by memory (keys in sorted_key, the
+// candidates' slots in order).
 __global__ __launch_bounds__(256) void k_front_scan(const uint32_t* __restrict__ order,
-                                                    const uint64_t* __restrict__ cand_key,
+                                                    const uint64_t* __restrict__ sorted_key,
                                                     const double* __restrict__ cand_obj,
                                                     const uint64_t* __restrict__ cand_id,
                                                     const int64_t* __restrict__ seg, int64_t n_groups,
@@ -40,13 +42,44 @@ __global__ __launch_bounds__(256) void k_front_scan(const uint32_t* __restrict__
   if (g >= n_groups) return;
   const int64_t b = seg[g], e = seg[g + 1];
   int64_t w = b;
-  double carry = __builtin_huge_val();  // minimum objective of the earlier chunks
+  double carry = __builtin_huge_val();  // minimum objective of the completed runs before
+  uint64_t run_key = kNoKey;            // a run continuing from the previous chunk: its memory
+  double run_obj = __builtin_huge_val();  // and its minimum so far
+  uint64_t run_id = kNoKey;
   for (int64_t c = b; c < e; c += 64) {
     const int64_t i = c + lane;
     const bool valid = i < e;
     const uint32_t k = valid ? order[i] : 0u;
-    const double o = valid ? cand_obj[k] : __builtin_huge_val();
-    double pm = o;  // inclusive prefix minimum over the chunk's lanes
+    const uint64_t key = valid ? sorted_key[i] : kNoKey;
+    const uint64_t next = i + 1 < e ? sorted_key[i + 1] : kNoKey;
+    double o = valid ? cand_obj[k] : __builtin_huge_val();
+    uint64_t id = valid ? cand_id[k] : kNoKey;
+    uint64_t prev = __shfl_up(key, 1, 64);
+    if (lane == 0) prev = run_key;
+    const bool start = valid && key != prev;
+    if (lane == 0 && valid && !start && lex_less(run_obj, run_id, o, id)) {
+      o = run_obj;
+      id = run_id;
+    }
+    // First lane of this lane's run in the chunk (0 for the run carried in), then the run's
+    // (obj, id) minimum up to this lane.
+    int head = start ? lane : 0;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int h = __shfl_up(head, off, 64);
+      if (lane >= off) head = max(head, h);
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const double vo = __shfl_up(o, off, 64);
+      const uint64_t vi = __shfl_up(id, off, 64);
+      if (lane - off >= head && lex_less(vo, vi, o, id)) {
+        o = vo;
+        id = vi;
+      }
+    }
+    const bool end = valid && next != key;  // last candidate of its run: (o, id) is the run's minimum
+    double pm = end ? o : __builtin_huge_val();  // inclusive prefix minimum over the run ends
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const double v = __shfl_up(pm, off, 64);
@@ -54,17 +87,22 @@ __global__ __launch_bounds__(256) void k_front_scan(const uint32_t* __restrict__
     }
     double before = __shfl_up(pm, 1, 64);
     before = lane == 0 ? carry : __builtin_fmin(carry, before);
-    const bool on = valid && o < before;
+    const bool on = end && o < before;
     const unsigned long long m = __builtin_amdgcn_ballot_w64(on);
     if (on) {
       const unsigned int rank =
           __builtin_amdgcn_mbcnt_hi((unsigned int)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)m, 0u));
-      front_key[w + rank] = cand_key[k];
+      front_key[w + rank] = key;
       front_obj[w + rank] = o;
-      front_id[w + rank] = cand_id[k];
+      front_id[w + rank] = id;
     }
     w += __builtin_popcountll(m);
     carry = __builtin_fmin(carry, __shfl(pm, 63, 64));
+    // The last lane's run goes on into the next chunk unless it ended here.
+    const bool open = __shfl((int)(valid && !end), 63, 64) != 0;
+    run_key = open ? __shfl(key, 63, 64) : kNoKey;
+    run_obj = __shfl(o, 63, 64);
+    run_id = __shfl(id, 63, 64);
   }
   if (lane == 0) front_cnt[g] = w - b;
 }
@@ -76,40 +114,32 @@ int last_error() {
 
 }  // namespace
 
-int exact_sort(const uint64_t* cand_key, const double* cand_obj, const uint64_t* cand_id, uint64_t* key_tmp,
-               uint64_t* key_out, uint32_t* idx_a, uint32_t* idx_b, int64_t n, int64_t n_groups, const int64_t* seg,
-               void* temp, size_t* temp_bytes, void* stream) {
+int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_in, uint32_t* idx_out, int64_t n,
+               int64_t n_groups, const int64_t* seg, void* temp, size_t* temp_bytes, void* stream) {
   hipStream_t st = (hipStream_t)stream;
   const unsigned int un = (unsigned int)n, ug = (unsigned int)n_groups;
-  if (!temp) {  // storage query (the three passes sort the same number of 64-bit keys)
-    const hipError_t e = rocprim::segmented_radix_sort_pairs(nullptr, *temp_bytes, key_tmp, key_out, idx_a, idx_b,
-                                                             un, ug, seg, seg + 1, 0, 64, st);
+  if (!temp) {  // storage query
+    const hipError_t e = rocprim::segmented_radix_sort_pairs(nullptr, *temp_bytes, cand_key, key_out, idx_in,
+                                                             idx_out, un, ug, seg, seg + 1, 0, 64, st);
     return e == hipSuccess ? 0 : (int)e;
   }
   if (n == 0) return 0;
-  const dim3 grid((unsigned)((n + 255) / 256)), block(256);
-  hipLaunchKernelGGL(k_iota, grid, block, 0, st, idx_a, n);
+  hipLaunchKernelGGL(k_iota, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, idx_in, n);
   int rc = last_error();
-  // Each pass: key_tmp = the next key in the current order idx_a, stable sort into idx_b.
-  const uint64_t* keys[3] = {cand_id, reinterpret_cast<const uint64_t*>(cand_obj), cand_key};
-  for (int pass = 0; pass < 3 && !rc; ++pass) {
-    hipLaunchKernelGGL(k_gather, grid, block, 0, st, keys[pass], idx_a, key_tmp, n);
-    rc = last_error();
-    if (rc) break;
-    const hipError_t e = rocprim::segmented_radix_sort_pairs(temp, *temp_bytes, key_tmp, key_out, idx_a, idx_b, un,
-                                                             ug, seg, seg + 1, 0, 64, st);
+  if (!rc) {
+    const hipError_t e = rocprim::segmented_radix_sort_pairs(temp, *temp_bytes, cand_key, key_out, idx_in, idx_out,
+                                                             un, ug, seg, seg + 1, 0, 64, st);
     if (e != hipSuccess) rc = (int)e;
-    std::swap(idx_a, idx_b);
   }
-  return rc;  // the final order is in the buffer passed as idx_b (three swaps)
+  return rc;
 }
 
-int launch_front_scan(const uint32_t* order, const uint64_t* cand_key, const double* cand_obj,
+int launch_front_scan(const uint32_t* order, const uint64_t* sorted_key, const double* cand_obj,
                       const uint64_t* cand_id, const int64_t* seg, int64_t n_groups, uint64_t* front_key,
                       double* front_obj, uint64_t* front_id, int64_t* front_cnt, void* stream) {
   if (n_groups <= 0) return 0;
   hipLaunchKernelGGL(k_front_scan, dim3((unsigned)((n_groups + 3) / 4)), dim3(256), 0, (hipStream_t)stream, order,
-                     cand_key, cand_obj, cand_id, seg, n_groups, front_key, front_obj, front_id, front_cnt);
+                     sorted_key, cand_obj, cand_id, seg, n_groups, front_key, front_obj, front_id, front_cnt);
   return last_error();
 }
 

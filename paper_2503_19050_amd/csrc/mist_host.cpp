@@ -100,7 +100,7 @@ struct mist_space {
   std::vector<int32_t> h_cnt;
   std::vector<int64_t> h_tile_off, h_seg;
   int64_t cand_cap = 0, n_cand = 0;
-  uint64_t *d_cand_key = nullptr, *d_cand_id = nullptr, *d_key_sorted = nullptr, *d_key_tmp = nullptr;
+  uint64_t *d_cand_key = nullptr, *d_cand_id = nullptr, *d_key_sorted = nullptr;
   double* d_cand_obj = nullptr;
   uint32_t *d_idx_in = nullptr, *d_idx_out = nullptr;
   uint64_t *d_front_key = nullptr, *d_front_id = nullptr;
@@ -795,14 +795,13 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
     S->h_seg[ng] = off;
     if (off >= ((int64_t)1 << 32)) return fail(MIST_E_RANGE, "exact frontier: more than 2^32 candidates");
     if (off > S->cand_cap) {
-      void* old[] = {S->d_cand_key, S->d_cand_id, S->d_key_sorted, S->d_key_tmp, S->d_cand_obj, S->d_idx_in, S->d_idx_out,
+      void* old[] = {S->d_cand_key, S->d_cand_id, S->d_key_sorted, S->d_cand_obj, S->d_idx_in, S->d_idx_out,
                      S->d_front_key, S->d_front_id, S->d_front_obj};
       for (void* p : old) dev_free_one(S, p);
       const size_t n = (size_t)off;
       S->d_cand_key = (uint64_t*)dev_alloc(S, n * 8);
       S->d_cand_id = (uint64_t*)dev_alloc(S, n * 8);
       S->d_key_sorted = (uint64_t*)dev_alloc(S, n * 8);
-      S->d_key_tmp = (uint64_t*)dev_alloc(S, n * 8);
       S->d_cand_obj = (double*)dev_alloc(S, n * 8);
       S->d_idx_in = (uint32_t*)dev_alloc(S, n * 4);
       S->d_idx_out = (uint32_t*)dev_alloc(S, n * 4);
@@ -810,15 +809,15 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       S->d_front_id = (uint64_t*)dev_alloc(S, n * 8);
       S->d_front_obj = (double*)dev_alloc(S, n * 8);
       S->cand_cap = off;
-      if (!S->d_cand_key || !S->d_cand_id || !S->d_key_sorted || !S->d_key_tmp || !S->d_cand_obj || !S->d_idx_in ||
+      if (!S->d_cand_key || !S->d_cand_id || !S->d_key_sorted || !S->d_cand_obj || !S->d_idx_in ||
           !S->d_idx_out || !S->d_front_key || !S->d_front_id || !S->d_front_obj) {
         S->cand_cap = 0;
         return fail(MIST_E_NOMEM, "device allocation failed: exact frontier candidates");
       }
     }
     size_t need = 0;
-    k = exact_sort(S->d_cand_key, S->d_cand_obj, S->d_cand_id, S->d_key_tmp, S->d_key_sorted, S->d_idx_in,
-                   S->d_idx_out, off, (int64_t)ng, S->d_seg, nullptr, &need, st);
+    k = exact_sort(S->d_cand_key, S->d_key_sorted, S->d_idx_in, S->d_idx_out, off, (int64_t)ng, S->d_seg, nullptr,
+                   &need, st);
     if (k) return fail_hip((hipError_t)k, "exact frontier: sort storage");
     if (need > S->sort_temp_bytes) {
       dev_free_one(S, S->d_sort_temp);
@@ -837,11 +836,11 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
     if (!k) k = launch_eval(ea, mode_grid(S, kModeEmit), kModeEmit, st);
     if (!k) {
       size_t bytes = S->sort_temp_bytes;
-      k = exact_sort(S->d_cand_key, S->d_cand_obj, S->d_cand_id, S->d_key_tmp, S->d_key_sorted, S->d_idx_in,
-                     S->d_idx_out, off, (int64_t)ng, S->d_seg, S->d_sort_temp, &bytes, st);
+      k = exact_sort(S->d_cand_key, S->d_key_sorted, S->d_idx_in, S->d_idx_out, off, (int64_t)ng, S->d_seg,
+                     S->d_sort_temp, &bytes, st);
     }
     if (!k)
-      k = launch_front_scan(S->d_idx_out, S->d_cand_key, S->d_cand_obj, S->d_cand_id, S->d_seg, (int64_t)ng,
+      k = launch_front_scan(S->d_idx_out, S->d_key_sorted, S->d_cand_obj, S->d_cand_id, S->d_seg, (int64_t)ng,
                             S->d_front_key, S->d_front_obj, S->d_front_id, S->d_front_cnt, st);
     if (k) return fail_hip((hipError_t)k, "exact frontier");
     S->n_cand = off;

@@ -152,13 +152,12 @@ int launch_reduce(const ReduceArgs& a, void* stream);
 int launch_eval_ids(const EvalArgs& a, const uint64_t* ids, int64_t n, double* out, void* stream);
 int launch_filter(const EvalArgs& a, const double* bucket_obj, const uint64_t* bucket_id, FiltEntry* filt,
                   void* stream);
-// Exact frontier, mist_exact.hip: the candidates of group g are [seg[g], seg[g+1]); three
-// stable segmented sorts (id, objective, memory) leave their (mem, obj, id) order in idx_b,
-// and the per-group scan keeps the staircase.
-int exact_sort(const uint64_t* cand_key, const double* cand_obj, const uint64_t* cand_id, uint64_t* key_tmp,
-               uint64_t* key_out, uint32_t* idx_a, uint32_t* idx_b, int64_t n, int64_t n_groups, const int64_t* seg,
-               void* temp, size_t* temp_bytes, void* stream);
-int launch_front_scan(const uint32_t* order, const uint64_t* cand_key, const double* cand_obj,
+// Exact frontier, mist_exact.hip: the candidates of group g are [seg[g], seg[g+1]); one
+// segmented sort by memory leaves the sorted keys in key_out and the candidates' slots in
+// idx_out, and the per-group scan keeps the staircase.
+int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_in, uint32_t* idx_out, int64_t n,
+               int64_t n_groups, const int64_t* seg, void* temp, size_t* temp_bytes, void* stream);
+int launch_front_scan(const uint32_t* order, const uint64_t* sorted_key, const double* cand_obj,
                       const uint64_t* cand_id, const int64_t* seg, int64_t n_groups, uint64_t* front_key,
                       double* front_obj, uint64_t* front_id, int64_t* front_cnt, void* stream);
 
