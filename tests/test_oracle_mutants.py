@@ -19,7 +19,7 @@ from oracle import oracle as O
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PINS = ["tests/test_oracle_pins.py", "tests/test_oracle_terms.py", "tests/test_oracle_reduce.py",
-        "tests/test_oracle_alpha.py", "tests/test_oracle_pareto.py"]
+        "tests/test_oracle_alpha.py", "tests/test_oracle_pareto.py", "tests/test_oracle_calib.py"]
 
 MUTANTS = {
     "forward peak drops the optimizer-step unit": (
@@ -73,6 +73,22 @@ MUTANTS = {
         "    if (a.obj != b.obj) return a.obj < b.obj;\n    if (a.mem != b.mem) return a.mem < b.mem;"),
     "pipeline sends counted once for middle stages": (
         "(int64_t)((k > 1) + (k < PP))", "(int64_t)((k > 1) || (k < PP))"),
+    "measured efficiency multiplied instead of divided": (
+        "ie.push_back(1.0 / h.eta_tab[i]);", "ie.push_back(h.eta_tab[i]);"),
+    "measured efficiency of the next microbatch size": (
+        "ie.push_back(1.0 / h.eta_tab[i]);", "ie.push_back(1.0 / h.eta_tab[(i + 1) % X.mb.size()]);"),
+}
+
+# Planted mistakes in the plain-Python calibration reference (co-run window and fit).
+CALIB_MUTANTS = {
+    "fit takes the ratio of sums": ("        num[mask][j] += c * s\n        den[mask][j] += s * s",
+                                    "        num[mask][j] += c\n        den[mask][j] += s"),
+    "fit keeps speed-ups below 1": ("phi[mask][j] = max(1.0, num[mask][j] / den[mask][j])",
+                                    "phi[mask][j] = num[mask][j] / den[mask][j]"),
+    "window opens at the earliest start": ("lo = max(t[j][0] for j in members)", "lo = min(t[j][0] for j in members)"),
+    "window keeps units that start before it": ("if t[j][i] >= lo and t[j][i + 1] <= hi:",
+                                                "if t[j][i + 1] >= lo and t[j][i + 1] <= hi:"),
+    "window mean over all units": ("            mean[j] = total / n", "            mean[j] = total / (len(t[j]) - 1)"),
 }
 
 
@@ -110,3 +126,41 @@ def test_planted_mistakes_are_caught():
     assert ok, out
     survivors = [names[k] for k, (passed, _) in sorted(results.items()) if passed]
     assert not survivors, "pins did not catch: %s" % survivors
+
+
+def test_planted_mistakes_in_the_calibration_reference_are_caught():
+    """Each variant of oracle/calib_oracle.py shadows the real one in a copy of the oracle package;
+    the calibration pins must fail on every variant and pass on the unedited copy."""
+    import shutil
+    src_path = os.path.join(ROOT, "oracle", "calib_oracle.py")
+    with open(src_path) as f:
+        src = f.read()
+    lib = O.build(force=False)
+    variants = {"unchanged": src}
+    for i, (what, (old, new)) in enumerate(CALIB_MUTANTS.items()):
+        assert src.count(old) == 1, what
+        variants["c%02d" % i] = src.replace(old, new)
+    names = {"c%02d" % i: what for i, what in enumerate(CALIB_MUTANTS)}
+    with tempfile.TemporaryDirectory() as tmp:
+        def run(item):
+            key, text = item
+            pkg = os.path.join(tmp, key, "oracle")
+            os.makedirs(pkg)
+            for fn in os.listdir(os.path.join(ROOT, "oracle")):
+                if fn.endswith(".py"):
+                    shutil.copy(os.path.join(ROOT, "oracle", fn), pkg)
+            with open(os.path.join(pkg, "calib_oracle.py"), "w") as f:
+                f.write(text)
+            env = dict(os.environ, MIST_ORACLE_LIB=lib,
+                       PYTHONPATH=os.pathsep.join([os.path.join(tmp, key), ROOT]))
+            r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                                "-p", "no:randomly", "--rootdir", os.path.join(tmp, key),
+                                os.path.join(ROOT, "tests", "test_oracle_calib.py")],
+                               cwd=os.path.join(tmp, key), env=env, capture_output=True, text=True, timeout=300)
+            return key, (r.returncode == 0, r.stdout[-1500:])
+        with ThreadPoolExecutor(max_workers=min(6, os.cpu_count() or 1)) as ex:
+            results = dict(ex.map(run, variants.items()))
+    ok, out = results.pop("unchanged")
+    assert ok, out
+    survivors = [names[k] for k, (passed, _) in sorted(results.items()) if passed]
+    assert not survivors, "calibration pins did not catch: %s" % survivors
