@@ -222,3 +222,35 @@ def test_error_paths(torch_cuda):
         S.best(S.n_groups, 1)
     assert e.value.status == -5
     S.close()
+
+
+@pytest.mark.parametrize("R", list(range(1, 17)))
+def test_every_ratio_count(R, torch_cuda):
+    """The evaluation kernel is compiled per ratio count R (1..16, with activation-ratio blocks
+    that change shape with R): every variant — buckets, weight samples and the exact frontier's
+    count and emit passes — against the oracle on a small space, every group in full."""
+    from paper_2503_19050_amd import mist
+    wl = W.workload("tiny")
+    wl["space"]["ratios"] = [i / (R - 1) for i in range(R)] if R > 1 else [0.0]
+    wl["space"]["mb"] = [1, 2]
+    wl["space"]["n_devices"] = 2
+    wl["space"]["global_batch"] = 32
+    alphas = [0.0, 0.3, 1.0]
+    wl["space"]["alphas"] = alphas
+    o = O.Oracle(wl)
+    say("R", R, o.n_configs, "configs")
+    S = mist.from_workload(wl)
+    S.eval()
+    S.eval_pareto_exact()
+    torch_cuda.cuda.synchronize()
+    _compare_groups(S, o.run(), list(range(o.n_groups)))
+    ref = o.run_alpha(alphas)
+    res = S.alpha(0, S.n_groups)
+    assert np.array_equal(np.array([[r["id"] for r in row] for row in res], dtype=np.uint64), ref["id"])
+    assert np.array_equal(np.array([[r["obj"] for r in row] for row in res]), ref["obj"])
+    for g in range(o.n_groups):
+        got, want = S.pareto_exact(g), o.pareto_exact(g)
+        assert [r["id"] for r in got] == [int(i) for i in want["id"]], g
+        assert [r["obj"] for r in got] == list(want["obj"]), g
+    _compare_ids(S, o, _sample_ids(o, np.random.default_rng(R), 300))
+    S.close()
