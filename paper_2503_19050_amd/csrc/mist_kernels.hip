@@ -488,6 +488,8 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
           const OoK O = oo_level(s_oo[tid], rr[io], om[io], iP);
           const bool zero_oo = zero_strip && io == 0;
           const unsigned int lid_oo = lid_strip + (unsigned int)(io * R);
+          [[maybe_unused]] double dn_blk[AL ? IB : 1];  // weight samples: the block's deltas (NaN
+                                                        // when infeasible)
 #pragma unroll
           for (int c = 0; c < IB; ++c) {
             const int ia = ib + c;
@@ -558,43 +560,57 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
               if (cand && key == k_new) atomicMin(&be->lid, lid);
             }
 
-            if constexpr (AL) {
-              // Eq. 4 for every weight sample, feasible configurations only: an infeasible
-              // one carries a NaN delta, so each of its weighted values is NaN and compares
-              // false.  All lanes address the sample's single entry; the same three-step
-              // LDS sequence keeps the lexicographic minimum.
-              const double dn = mem <= M ? d : __builtin_nan("");
-              // First every sample against the entries as they stand (no lane can beat an
-              // entry it does not beat now: entries only decrease), in straight-line code;
-              // the exact sequence only when some lane of the wave may win.
-              wave_sync();
+            if constexpr (AL) dn_blk[c] = mem <= M ? d : __builtin_nan("");
+          }
+
+          if constexpr (AL) {
+            // Eq. 4 for every weight sample, feasible configurations only: an infeasible one
+            // carries a NaN delta, so each of its weighted values is NaN and compares false.
+            // First the block's configurations against every sample's entry as it stands (no
+            // lane can beat an entry it does not beat now: entries only decrease), each
+            // sample's values read once for the block; the exact sequence only when some lane
+            // of the wave may win.  All lanes address the sample's single entry; the same
+            // three-step LDS sequence as the buckets' keeps the lexicographic minimum.
+            wave_sync();
+            unsigned int qmask = 0;  // samples some lane of the wave may win
+#pragma unroll 1
+            for (int q = 0; q < a.n_alpha; ++q) {
+              const double2 ab = s_ab[wave][q];
+              const double cur = s_aent[wave][q].val;
               bool any = false;
 #pragma unroll
-              for (int q = 0; q < kMaxAlphas; ++q) {
-                if (q >= a.n_alpha) break;
-                const double2 ab = s_ab[wave][q];
-                any = any | (__builtin_fma(ab.x, tv, ab.y * dn) <= s_aent[wave][q].val);
+              for (int c = 0; c < IB; ++c) {
+                if (ib + c >= R) break;
+                any = any | (__builtin_fma(ab.x, tt[c], ab.y * dn_blk[c]) <= cur);
               }
-              if (!__builtin_amdgcn_ballot_w64(any)) continue;
+              if (__builtin_amdgcn_ballot_w64(any)) qmask |= 1u << q;
+            }
+            if (qmask) {
 #pragma unroll 1
-              for (int q = 0; q < a.n_alpha; ++q) {
+              for (unsigned int qs = qmask; qs; qs &= qs - 1) {
+                const int q = __builtin_ctz(qs);
                 const double2 ab = s_ab[wave][q];
-                const double v = __builtin_fma(ab.x, tv, ab.y * dn);
                 AlphaEntry* const e = &s_aent[wave][q];
-                wave_sync();
-                const double cur = e->val;
-                if (__builtin_amdgcn_ballot_w64(v <= cur)) {
-                  const unsigned int lid = lid_oo + (unsigned int)ia;
-                  const unsigned long long ak = order_key(v);
-                  const unsigned long long ak_old = e->key;
-                  const unsigned int ai_old = e->lid;
-                  const bool cand = (v <= cur) & ((ak < ak_old) | ((ak == ak_old) & (lid < ai_old)));
-                  if (cand) atomicMin(&e->key, ak);
-                  const unsigned long long ak_new = cand ? e->key : 0ull;
-                  if (cand && ak_new < ak_old) e->lid = 0xFFFFFFFFu;
-                  if (cand && ak == ak_new) {
-                    atomicMin(&e->lid, lid);
-                    e->val = v;
+#pragma unroll
+                for (int c = 0; c < IB; ++c) {
+                  const int ia = ib + c;
+                  if (ia >= R) break;
+                  const double v = __builtin_fma(ab.x, tt[c], ab.y * dn_blk[c]);
+                  wave_sync();
+                  const double cur = e->val;
+                  if (__builtin_amdgcn_ballot_w64(v <= cur)) {
+                    const unsigned int lid = lid_oo + (unsigned int)ia;
+                    const unsigned long long ak = order_key(v);
+                    const unsigned long long ak_old = e->key;
+                    const unsigned int ai_old = e->lid;
+                    const bool cand = (v <= cur) & ((ak < ak_old) | ((ak == ak_old) & (lid < ai_old)));
+                    if (cand) atomicMin(&e->key, ak);
+                    const unsigned long long ak_new = cand ? e->key : 0ull;
+                    if (cand && ak_new < ak_old) e->lid = 0xFFFFFFFFu;
+                    if (cand && ak == ak_new) {
+                      atomicMin(&e->lid, lid);
+                      e->val = v;
+                    }
                   }
                 }
               }
