@@ -666,7 +666,8 @@ __global__ __launch_bounds__(kReduceBlock) void k_reduce(ReduceArgs a) {
   const DevGroup grp = a.groups[g];
   double obj = __builtin_huge_val();
   uint64_t id = kNone;
-  if (lane < a.NB) {
+  if (lane < a.NB) {  // several tiles' loads in flight
+#pragma unroll 4
     for (int t = grp.tile_begin; t < grp.tile_begin + grp.n_tiles; ++t) {
       const double o = a.part_obj[(size_t)t * 64 + lane];
       const uint64_t i = a.part_id[(size_t)t * 64 + lane];
@@ -675,6 +676,7 @@ __global__ __launch_bounds__(kReduceBlock) void k_reduce(ReduceArgs a) {
         id = i;
       }
     }
+#pragma unroll 4
     for (int t = grp.tail_begin; t < grp.tail_begin + grp.n_tail; ++t) {
       const double o = a.part_obj[(size_t)t * 64 + lane];
       const uint64_t i = a.part_id[(size_t)t * 64 + lane];
