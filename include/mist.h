@@ -109,6 +109,10 @@ typedef struct mist_space_desc {
   int32_t n_alphas;      /* 0..MIST_MAX_ALPHAS weight samples of Eq. 4; 0 (or a zeroed tail of
                             the struct) turns the weight-sampled argmins off */
   const double* alphas;  /* host: the samples alpha_a in [0, 1] (any order, repeats allowed) */
+  int64_t tile_configs;  /* launch geometry, results do not depend on it: configurations per
+                            full-size tile of the evaluation kernel, at least (0: 8192) */
+  int32_t max_blocks;    /* cap on the evaluation kernel's grid (0: every block that fits on the
+                            device at once) */
 } mist_space_desc;
 
 /* Device memory provider, e.g. PyTorch's caching allocator.  alloc returns NULL on

@@ -72,6 +72,8 @@ struct mist_space {
   int32_t* d_pk_group = nullptr;
   int32_t* d_work = nullptr;
   int32_t eval_grid = 0;
+  int64_t tile_configs = 0;  // configurations per full-size tile, at least
+  int32_t max_blocks = 0;    // cap on the evaluation grid (0: none)
   double* d_part_obj = nullptr;
   uint64_t* d_part_id = nullptr;
   double* d_bucket_obj = nullptr;
@@ -211,6 +213,8 @@ std::string validate(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n
   if (s->l_rule != MIST_L_FULL && s->l_rule != MIST_L_BALANCED) return "unknown l_rule";
   if (s->n_alphas < 0 || s->n_alphas > MIST_MAX_ALPHAS || (s->n_alphas > 0 && !s->alphas))
     return "n_alphas out of range";
+  if (s->tile_configs < 0 || s->tile_configs > ((int64_t)1 << 40) || s->max_blocks < 0)
+    return "tile_configs and max_blocks must be non-negative";
   for (int32_t i = 0; i < s->n_alphas; ++i)
     if (!(s->alphas[i] >= 0.0 && s->alphas[i] <= 1.0)) return "weight samples must lie in [0, 1]";
   return "";
@@ -524,8 +528,9 @@ namespace {
 // width).  Every wave of the persistent evaluation grid takes tile number (its global wave
 // index) first and claims further tiles from the device counter, in tile order.  A space of
 // at most kStaticStrips strips per resident wave is cut into about one tile per resident wave,
-// so that no claim is made.  A larger one is cut into tiles of at least kMinTileConfigs
-// configurations (claims on one counter serialize) and at most kMaxTiles tiles; the last
+// so that no claim is made.  A larger one is cut into tiles of at least the space's
+// tile_configs configurations (kMinTileConfigs unless the descriptor asks for another size;
+// claims on one counter serialize) and at most kMaxTiles tiles; the last
 // kTailPercent percent of a group's strips (rounded up to its last full-size tile) go into
 // tiles a quarter of that size, placed after all full-size tiles, so that the waves that
 // finish last wait for a small tile.
@@ -546,7 +551,7 @@ std::string build_tiles(mist_space* S, int64_t resident_waves) {
   if (single)
     spt = align((total_strips + W - 1) / W);
   else
-    spt = align(std::max<uint64_t>(((uint64_t)kMinTileConfigs + R2 - 1) / R2,
+    spt = align(std::max<uint64_t>(((uint64_t)S->tile_configs + R2 - 1) / R2,
                                    (total_strips + (uint64_t)kMaxTiles - 1) / (uint64_t)kMaxTiles));
   const uint64_t spt_tail = single ? spt : align(spt / 4);
   S->strips_per_tile = (int32_t)spt;
@@ -606,6 +611,8 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
     S->l_rule = s->l_rule;
     S->ratio_om.assign(s->ratios, s->ratios + s->n_ratios);
     for (int32_t i = 0; i < s->n_ratios; ++i) S->ratio_om.push_back(1.0 - s->ratios[i]);
+    S->tile_configs = s->tile_configs > 0 ? s->tile_configs : kMinTileConfigs;
+    S->max_blocks = s->max_blocks;
     S->A = s->n_alphas;
     S->alphas.assign(s->alphas, s->alphas + s->n_alphas);
     for (int32_t i = 0; i < s->n_alphas; ++i) S->betas.push_back(1.0 - s->alphas[i]);
@@ -628,6 +635,7 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
       if (e != hipSuccess) rc = fail_hip(e, "device attributes");
       const int per_cu = eval_blocks_per_cu(S->R, S->A > 0 ? kModeAlpha : kModeBuckets);
       resident_blocks = std::max<int64_t>(1, (int64_t)cus * (per_cu > 0 ? per_cu : 1));
+      if (S->max_blocks > 0) resident_blocks = std::min<int64_t>(resident_blocks, S->max_blocks);
       S->cus = cus;
     }
     if (!rc) {
@@ -743,7 +751,8 @@ mist_status mist_eval_space(mist_space* S, void* hip_stream) {
 // Grid of the persistent evaluation kernel in a given variant.
 static int32_t mode_grid(const mist_space* S, int mode) {
   const int per_cu = eval_blocks_per_cu(S->R, mode);
-  const int64_t resident = std::max<int64_t>(1, (int64_t)S->cus * (per_cu > 0 ? per_cu : 1));
+  int64_t resident = std::max<int64_t>(1, (int64_t)S->cus * (per_cu > 0 ? per_cu : 1));
+  if (S->max_blocks > 0) resident = std::min<int64_t>(resident, S->max_blocks);
   const int64_t waves_needed = (int64_t)(S->tiles.size() + kWaves - 1) / kWaves;
   return (int32_t)std::max<int64_t>(1, std::min<int64_t>(resident, waves_needed));
 }

@@ -254,3 +254,72 @@ def test_every_ratio_count(R, torch_cuda):
         assert [r["obj"] for r in got] == list(want["obj"]), g
     _compare_ids(S, o, _sample_ids(o, np.random.default_rng(R), 300))
     S.close()
+
+
+def test_launch_geometry_does_not_change_results(torch_cuda):
+    """The reductions are order-independent lexicographic minima: other tile sizes and other grid
+    sizes (many more claims per wave) give bit-identical buckets, best results, weight-sample
+    argmins and exact frontiers."""
+    from paper_2503_19050_amd import mist
+
+    def outputs(wl):
+        S = mist.from_workload(wl)
+        S.eval()
+        S.eval_pareto_exact()
+        torch_cuda.cuda.synchronize()
+        ids, objs, masks = S.buckets(0, S.n_groups)
+        al = S.alpha(0, S.n_groups)
+        aid = np.array([[r["id"] for r in row] for row in al], dtype=np.uint64)
+        ex = [[r["id"] for r in S.pareto_exact(g)] for g in range(0, S.n_groups, max(1, S.n_groups // 40))]
+        info = S.launch_info()
+        S.close()
+        return (ids, objs, masks, aid, ex), info
+
+    for name, variants in (("c2", [{"tile_configs": 2048}, {"tile_configs": 65536, "max_blocks": 37}]),
+                           ("tiny", [{"max_blocks": 1}, {"tile_configs": 100000}])):
+        wl = W.workload(name)
+        wl["space"]["alphas"] = [0.2, 0.7]
+        ref, info0 = outputs(wl)
+        for v in variants:
+            w2 = W.workload(name)
+            w2["space"]["alphas"] = [0.2, 0.7]
+            w2["space"].update(v)
+            got, info = outputs(w2)
+            say(name, v, "tiles", info0, "->", info)
+            for a, b in zip(ref[:4], got[:4]):
+                assert np.array_equal(a, b), (name, v)
+            assert ref[4] == got[4], (name, v)
+
+
+def test_allocator_failure_is_reported(torch_cuda):
+    """An allocator that returns NULL (after a given number of successful calls) makes
+    mist_space_create fail with MIST_E_NOMEM and release what it had allocated."""
+    import ctypes
+    from paper_2503_19050_amd import mist
+    L = mist.load()
+    wl = W.workload("tiny")
+    S = mist.from_workload(wl)          # descriptors built by the binding
+    model, hw, space = S._model, S._hw, S._space
+    S.close()
+    for ok_calls in (0, 3):
+        live = {}
+        calls = [0]
+
+        def alloc(nbytes, ctx):
+            calls[0] += 1
+            if calls[0] > ok_calls:
+                return None
+            t = torch_cuda.empty(int(nbytes), dtype=torch_cuda.uint8, device="cuda")
+            live[t.data_ptr()] = t
+            return t.data_ptr()
+
+        def free(ptr, ctx):
+            live.pop(ptr, None)
+
+        cb = (mist.ALLOC_FN(alloc), mist.FREE_FN(free))
+        al = mist.Allocator(cb[0], cb[1], None)
+        h = ctypes.c_void_p()
+        rc = L.mist_space_create(ctypes.byref(model), hw, len(wl["hws"]), ctypes.byref(space), ctypes.byref(al),
+                                 ctypes.byref(h))
+        assert rc == -2 and "allocation" in L.mist_last_error().decode()
+        assert not live, "buffers left behind"
