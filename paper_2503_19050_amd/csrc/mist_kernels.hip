@@ -537,7 +537,8 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
               n_cand += __builtin_popcountll(m);
               continue;
             }
-            BucketEntry* const be = reinterpret_cast<BucketEntry*>(b0 + (mem > e0 ? sizeof(BucketEntry) : 0));
+            const bool up = mem > e0;
+            BucketEntry* const be = reinterpret_cast<BucketEntry*>(b0 + (up ? sizeof(BucketEntry) : 0));
 
             // Lexicographic (obj, id) minimum per bucket without a serial loop: the lanes
             // that beat their bucket's entry lower the objective bits with an LDS atomic
@@ -547,7 +548,10 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
             // the one before, so each step sees the previous one's result.
             const unsigned long long key = (unsigned long long)__double_as_longlong(obj);
             wave_sync();  // read the entry after every earlier update of the wave
-            const unsigned long long k_old = be->key;
+            // Both candidate entries' keys in one LDS round trip (entry 64 exists: a sink).
+            const unsigned long long k_lo = reinterpret_cast<const BucketEntry*>(b0)->key;
+            const unsigned long long k_hi = reinterpret_cast<const BucketEntry*>(b0 + sizeof(BucketEntry))->key;
+            const unsigned long long k_old = up ? k_hi : k_lo;
             // A candidate beats the entry: key < k_old, or an equal key with a lower id.  No
             // lane with key > k_old is one, so the exact test waits for a lane with key <= k_old.
             if (__builtin_amdgcn_ballot_w64(key <= k_old)) {
