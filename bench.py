@@ -107,7 +107,7 @@ def main() -> int:
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the evaluation of one space runs on a single device "
-              "(multi-GPU sharding by group is described in DESIGN.md, not run here)", file=sys.stderr)
+              "(sharding the groups over several GPUs needs no exchange and is not run here)", file=sys.stderr)
         return 2
 
     import torch
