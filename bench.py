@@ -2,7 +2,7 @@
 (cost model + feasibility filter + per-bucket and per-group reductions) and the FP64
 vector roofline fraction of the evaluation kernel.
 
-One step = one mist_eval_space over the whole space of the workload (default c2: GPT
+One step = one mist_eval_space over the whole space of the workload (default gpt2.7b-d16: GPT
 L32 h2560, 273,952,500 configurations, 4,527 groups), inputs resident on the GPU.
 Prints one JSON line; its "alpha_frontier" field times the same space with weight samples of
 Eq. 4 added (the per-group (t, d) argmins).  The CPU baseline is the plain oracle timed on this host over a
@@ -91,7 +91,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--workload", default="gpt2.7b-d16", choices=["gpt1.3b-d8", "gpt2.7b-d16", "llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--alphas", type=int, default=8,

@@ -18,7 +18,7 @@ One device cannot exercise a GPU-GPU link: that stream is a copy kernel on a few
 (the footprint of a collective's kernel), and link_bw keeps the nominal value given on the
 command line.
 
-    python -m paper_2503_19050_amd.calibrate --workload c2 --out calib.json
+    python -m paper_2503_19050_amd.calibrate --workload gpt2.7b-d16 --out calib.json
 """
 from __future__ import annotations
 
@@ -81,7 +81,7 @@ def validate(C, shapes, samples, phi, rng, n_runs):
 
 def main() -> int:
     ap = argparse.ArgumentParser()
-    ap.add_argument("--workload", default="c2", choices=W.WORKLOADS + ["tiny", "tiny_llama"])
+    ap.add_argument("--workload", default="gpt2.7b-d16", choices=W.WORKLOADS + ["tiny", "tiny_llama"])
     ap.add_argument("--tp", type=int, default=1)
     ap.add_argument("--peak", type=float, default=MI355X_BF16_DENSE)
     ap.add_argument("--link", type=float, default=MI355X_XGMI_LINK)

@@ -113,29 +113,29 @@ def _space(D, mb, R, rule, nb=64):
 
 # name -> (description, model, hardware list, space)
 def workload(name: str) -> dict:
-    """Descriptors of a named workload (c1..c5 or a tiny test space)."""
-    if name == "c1":
+    """Descriptors of a named workload (one of WORKLOADS, or a tiny test space)."""
+    if name == "gpt1.3b-d8":
         # GPT L24 h2048 (1.3B class), 8 devices, fixed seed-0 hardware.
         model = _model(GPT, 24, 2048, 16, 16, 8192, 2048, 50257)
         hws = [hw_sample(0, {"flops": 200e12, "mem_bytes": 24e9, "pcie_bw": 32e9, "link_bw": 100e9})]
         space = _space(8, [1, 2, 4, 8, 16], 2, L_FULL)
         desc = "GPT L24 h2048 16 heads s2048 V50257, D=8, B=128, b 1..16, ratios {0,1}"
-    elif name == "c2":
+    elif name == "gpt2.7b-d16":
         model = _model(GPT, 32, 2560, 32, 32, 10240, 2048, 50257)
         hws = [hw_sample(2)]
         space = _space(16, POW2_32, 5, L_FULL)
         desc = "GPT L32 h2560 32 heads s2048 V50257, D=16, B=256, b 1..32, 5 ratios"
-    elif name == "c3":
+    elif name == "llama7b-d32":
         model = _model(LLAMA, 32, 4096, 32, 32, 11008, 4096, 32000)
         hws = [hw_sample(3)]
         space = _space(32, POW2_32, 9, L_FULL)
         desc = "Llama L32 h4096 f11008 32 heads s4096 V32000, D=32, B=512, b 1..32, 9 ratios"
-    elif name == "c4":
+    elif name == "llama13b-d64":
         model = _model(LLAMA, 40, 5120, 40, 40, 13824, 4096, 32000)
         hws = [hw_sample(4)]
         space = _space(64, POW2_32, 11, L_FULL)
         desc = "Llama L40 h5120 f13824 40 heads s4096 V32000, D=64, B=1024, b 1..32, 11 ratios"
-    elif name == "c5":
+    elif name == "llama42b-d128-hw64":
         model = _model(LLAMA, 60, 8192, 64, 8, 22016, 8192, 32000)
         hws = [hw_sample(100 + i) for i in range(64)]
         space = _space(128, POW2_32, 9, L_BALANCED)
@@ -158,7 +158,7 @@ def workload(name: str) -> dict:
     return {"name": name, "desc": desc, "model": model, "hws": hws, "space": space}
 
 
-WORKLOADS = ["c1", "c2", "c3", "c4", "c5"]
+WORKLOADS = ["gpt1.3b-d8", "gpt2.7b-d16", "llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"]
 
 
 def with_eta_table(wl: dict, seed: int, lo: float = 0.30, hi: float = 0.90) -> dict:

@@ -6,11 +6,11 @@ Two counts per workload:
 * ``flops_per_config`` -- the definition evaluated for one configuration on its own: every level
   of the listing (pair, recomputation, ZeRO, offload levels, both runs of Algorithm 1, the
   objective) once, nothing shared with another configuration.  Averaged over every
-  configuration of c1 and over 2,000,000 evenly spaced configurations of c2-c5 (the count
-  depends on the data only through Algorithm 1's pattern changes).
+  configuration of gpt1.3b-d8 and over 2,000,000 evenly spaced configurations of each larger
+  workload (the count depends on the data only through Algorithm 1's pattern changes).
 * ``flops_per_config_shared_levels`` -- the oracle's nested loops, which evaluate each level once
-  per combination of its digits and share it with every configuration below it; c1 and c2 over
-  every group, c3-c5 over every 16th group.
+  per combination of its digits and share it with every configuration below it; gpt1.3b-d8 and
+  gpt2.7b-d16 over every group, the Llama workloads over every 16th group.
 
 Run: python tests/golden/make_flops.py   (calls only oracle/)
 """
@@ -58,7 +58,7 @@ def main():
             jobs = [(name, k0, min(k0 + CHUNK, n_ids), n_ids, o.n_configs) for k0 in range(0, n_ids, CHUNK)]
             res = list(ex.map(_count_ids, jobs))
             single = sum(r[0] for r in res) / sum(r[1] for r in res)
-            stride = 1 if name in ("c1", "c2") else 16
+            stride = 1 if name in ("gpt1.3b-d8", "gpt2.7b-d16") else 16
             groups = list(range(0, o.n_groups, stride))
             res = list(ex.map(_count_groups, [(name, g) for g in groups], chunksize=4))
             flops = sum(r[0] for r in res)

@@ -1,10 +1,10 @@
-"""Writes full_<workload>.npz for the large workloads c3, c4 and c5: the oracle run over every
-group, reduced to one digest per group (tests/golden/digest.py) plus the space's counts.
-The GPU parity test evaluates the whole space with the library and compares every group's
-digest.
+"""Writes full_<workload>.npz for the large workloads (llama7b-d32, llama13b-d64,
+llama42b-d128-hw64): the oracle run over every group, reduced to one digest per group
+(tests/golden/digest.py) plus the space's counts.  The GPU parity test evaluates the whole space
+with the library and compares every group's digest.
 
-Run: python tests/golden/make_full_oracle.py [c3 c4 c5]   (calls only oracle/; all cores;
-c5 takes about 8 minutes on 8 cores)
+Run: python tests/golden/make_full_oracle.py [llama7b-d32 llama13b-d64 llama42b-d128-hw64]
+(calls only oracle/; all cores; llama42b-d128-hw64 takes about 8 minutes on 8 cores)
 """
 
 import os
@@ -52,4 +52,4 @@ def main(names):
 
 
 if __name__ == "__main__":
-    main(sys.argv[1:] or ["c3", "c4", "c5"])
+    main(sys.argv[1:] or ["llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"])

@@ -15,7 +15,7 @@ sys.path.insert(0, GOLDEN)
 from digest import group_digests  # noqa: E402
 
 
-@pytest.mark.parametrize("name", ["c3", "c4", "c5"])
+@pytest.mark.parametrize("name", ["llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"])
 def test_stored_digests_match_the_enumeration(name):
     gold = np.load(os.path.join(GOLDEN, "full_%s.npz" % name))
     o = O.Oracle(W.workload(name))

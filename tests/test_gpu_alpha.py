@@ -45,14 +45,14 @@ def _gpu_alpha(S, groups=None):
     return ids, objs, res
 
 
-@pytest.mark.parametrize("name", ["tiny", "tiny_llama", "c1", "c2"])
+@pytest.mark.parametrize("name", ["tiny", "tiny_llama", "gpt1.3b-d8", "gpt2.7b-d16"])
 def test_alpha_parity_full(name, torch_cuda):
     wl = W.workload(name)
     S = _space(wl, ALPHAS)
     S.eval()
     torch_cuda.cuda.synchronize()
     o = O.Oracle(wl)
-    if name == "c2":
+    if name == "gpt2.7b-d16":
         ref = O.run_alpha_groups(wl, ALPHAS, range(o.n_groups), procs=PROCS)
     else:
         ref = o.run_alpha(ALPHAS)
@@ -70,7 +70,7 @@ def test_alpha_parity_full(name, torch_cuda):
     S.close()
 
 
-@pytest.mark.parametrize("name", ["c3", "c4", "c5"])
+@pytest.mark.parametrize("name", ["llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"])
 def test_alpha_parity_sampled(name, torch_cuda):
     wl = W.workload(name)
     S = _space(wl, ALPHAS)
@@ -90,7 +90,7 @@ def test_alpha_half_is_the_best_and_buckets_unchanged(torch_cuda):
     """alpha = 1/2 weighs fma(G, t, d) by exactly one half, so its argmin is each group's best;
     evaluating the samples leaves the bucket tables, best and frontier as without them."""
     from paper_2503_19050_amd import mist
-    wl = W.workload("c2")
+    wl = W.workload("gpt2.7b-d16")
     S = _space(wl, ALPHAS)
     S.eval()
     P = mist.from_workload(wl)

@@ -26,7 +26,7 @@ def torch_cuda():
     return torch
 
 
-@pytest.mark.parametrize("name", ["tiny", "tiny_llama", "c1"])
+@pytest.mark.parametrize("name", ["tiny", "tiny_llama", "gpt1.3b-d8"])
 def test_eta_table_full_parity(name, torch_cuda):
     from paper_2503_19050_amd import mist
     wl = W.with_eta_table(W.workload(name), seed=77)

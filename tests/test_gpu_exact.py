@@ -31,7 +31,7 @@ def _tight():
     return wl
 
 
-@pytest.mark.parametrize("name", ["tiny", "tiny_llama", "tight", "c1", "c2", "c3", "c4", "c5"])
+@pytest.mark.parametrize("name", ["tiny", "tiny_llama", "tight", "gpt1.3b-d8", "gpt2.7b-d16", "llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"])
 def test_exact_frontier(name, torch_cuda):
     from paper_2503_19050_amd import mist
     wl = _tight() if name == "tight" else W.workload(name)
@@ -40,7 +40,7 @@ def test_exact_frontier(name, torch_cuda):
     S.eval_pareto_exact()
     torch_cuda.cuda.synchronize()
     o = O.Oracle(wl)
-    if name in ("tiny", "tiny_llama", "tight", "c1"):
+    if name in ("tiny", "tiny_llama", "tight", "gpt1.3b-d8"):
         groups = range(o.n_groups)
     else:
         rng = np.random.default_rng(4)

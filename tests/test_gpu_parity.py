@@ -2,8 +2,8 @@
 
 Bar: identical argmin ids, bucket tables and frontier bits, and every cost value within
 1e-12 relative (the kernels follow the same IEEE operation sequence, so the values are
-compared bit for bit).  Full-size workloads c3-c5 run in the benchmark's launch
-configuration; every group is compared with the oracle's stored whole-space run (one digest
+compared bit for bit).  The full-size Llama workloads (llama7b-d32, llama13b-d64,
+llama42b-d128-hw64) run in the benchmark's launch configuration; every group is compared with the oracle's stored whole-space run (one digest
 per group), and the oracle recomputes a sample of whole groups and single configurations in
 full.
 """
@@ -76,7 +76,7 @@ def _sample_ids(o, rng, n):
     return np.unique(np.concatenate([np.array(edges, dtype=np.uint64), rand]))
 
 
-@pytest.mark.parametrize("name", ["tiny", "tiny_llama", "c1", "c2"])
+@pytest.mark.parametrize("name", ["tiny", "tiny_llama", "gpt1.3b-d8", "gpt2.7b-d16"])
 def test_full_parity_small(name, torch_cuda):
     wl = W.workload(name)
     S = _space(wl, torch_cuda)
@@ -85,13 +85,13 @@ def test_full_parity_small(name, torch_cuda):
     _eval(S, torch_cuda)
     say("oracle", name, o.n_configs, "configs on", PROCS, "processes")
     groups = list(range(o.n_groups))
-    ref = O.run_groups(wl, groups, procs=PROCS) if name == "c2" else o.run()
+    ref = O.run_groups(wl, groups, procs=PROCS) if name == "gpt2.7b-d16" else o.run()
     _compare_groups(S, ref, groups)
     _compare_ids(S, o, _sample_ids(o, np.random.default_rng(1), 3000))
     S.close()
 
 
-@pytest.mark.parametrize("name", ["c3", "c4", "c5"])
+@pytest.mark.parametrize("name", ["llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"])
 def test_full_size_sampled_parity(name, torch_cuda):
     wl = W.workload(name)
     S = _space(wl, torch_cuda)
@@ -111,7 +111,7 @@ def test_full_size_sampled_parity(name, torch_cuda):
     S.close()
 
 
-@pytest.mark.parametrize("name", ["c3", "c4", "c5"])
+@pytest.mark.parametrize("name", ["llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"])
 def test_full_parity_large(name, torch_cuda):
     """Every group of the full-size workloads against the oracle's whole-space run, stored as
     one digest per group by tests/golden/make_full_oracle.py (which calls only the oracle)."""
@@ -136,7 +136,7 @@ def test_full_parity_large(name, torch_cuda):
 
 def test_results_api_consistent(torch_cuda):
     """mist_get_best / mist_get_pareto agree with the bucket table and with per-id values."""
-    wl = W.workload("c1")
+    wl = W.workload("gpt1.3b-d8")
     S = _space(wl, torch_cuda)
     o = O.Oracle(wl)
     _eval(S, torch_cuda)
@@ -161,7 +161,7 @@ def test_results_api_consistent(torch_cuda):
 
 
 def test_deterministic_and_rerunnable(torch_cuda):
-    wl = W.workload("c2")
+    wl = W.workload("gpt2.7b-d16")
     S = _space(wl, torch_cuda)
     _eval(S, torch_cuda)
     a = S.buckets()
@@ -275,7 +275,7 @@ def test_launch_geometry_does_not_change_results(torch_cuda):
         S.close()
         return (ids, objs, masks, aid, ex), info
 
-    for name, variants in (("c2", [{"tile_configs": 2048}, {"tile_configs": 65536, "max_blocks": 37}]),
+    for name, variants in (("gpt2.7b-d16", [{"tile_configs": 2048}, {"tile_configs": 65536, "max_blocks": 37}]),
                            ("tiny", [{"max_blocks": 1}, {"tile_configs": 100000}])):
         wl = W.workload(name)
         wl["space"]["alphas"] = [0.2, 0.7]

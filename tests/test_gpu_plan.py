@@ -27,7 +27,7 @@ def torch_cuda():
     return torch
 
 
-@pytest.mark.parametrize("name,pps", [("tiny", (0, 1, 2, 4)), ("tiny_llama", (0, 1, 2, 4)), ("c1", (1, 2))])
+@pytest.mark.parametrize("name,pps", [("tiny", (0, 1, 2, 4)), ("tiny_llama", (0, 1, 2, 4)), ("gpt1.3b-d8", (1, 2))])
 def test_plan_matches_exhaustive_search(name, pps, torch_cuda):
     from paper_2503_19050_amd import mist
     wl = W.workload(name)
@@ -60,16 +60,16 @@ def test_plan_matches_exhaustive_search(name, pps, torch_cuda):
 
 
 def test_plan_full_size(torch_cuda):
-    """c4 with weight samples: a plan exists, uses every layer once and its value is Eq. 2 of its
+    """llama13b-d64 with weight samples: a plan exists, uses every layer once and its value is Eq. 2 of its
     points; no single-stage plan is better."""
     from paper_2503_19050_amd import mist
-    wl = W.workload("c4")
+    wl = W.workload("llama13b-d64")
     wl["space"] = dict(wl["space"], alphas=[k / 7.0 for k in range(8)])
     S = mist.from_workload(wl)
     S.eval()
     plan = S.plan(0, 0)
     one = S.plan(0, 1)
-    say("c4 plan", plan["G"], plan["PP"], plan["F"], [st["l"] for st in plan["stages"]])
+    say("llama13b-d64 plan", plan["G"], plan["PP"], plan["F"], [st["l"] for st in plan["stages"]])
     assert sum(st["l"] for st in plan["stages"]) == wl["model"]["n_layers"]
     assert plan["F"] == PO.plan_value(plan["G"], [st["t"] for st in plan["stages"]],
                                       [st["d"] for st in plan["stages"]])

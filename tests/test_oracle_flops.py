@@ -39,5 +39,5 @@ def test_stored_counts():
     for name in W.WORKLOADS:
         w = d[name]
         assert w["flops_per_config"] > w["flops_per_config_shared_levels"] > 0
-    o = O.Oracle(W.workload("c1"))
-    assert d["c1"]["configs_sampled"] == o.n_configs    # c1: every configuration
+    o = O.Oracle(W.workload("gpt1.3b-d8"))
+    assert d["gpt1.3b-d8"]["configs_sampled"] == o.n_configs    # gpt1.3b-d8: every configuration

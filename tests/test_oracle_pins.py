@@ -145,19 +145,19 @@ def _cid(wl, key, b, tp, c, z, wo, go, oo, ao):
 
 
 def _llama7b_space():
-    wl = W.workload("c3")          # Llama-2-7B shapes
+    wl = W.workload("llama7b-d32")          # Llama-2-7B shapes
     wl["space"] = {"n_devices": 4, "global_batch": 64, "mb": [1, 2], "ratios": [0.0, 0.5, 1.0],
                    "n_buckets": 64, "l_rule": W.L_FULL}
     return wl
 
 
-# Published parameter counts of the Llama 2 models whose shapes c3 and c4 use
+# Published parameter counts of the Llama 2 models whose shapes llama7b-d32 and llama13b-d64 use
 # (Touvron et al., "Llama 2", 2023; 7B: 6,738,415,616; 13B: 13,015,864,320).
 LLAMA2_7B = 6_738_415_616
 LLAMA2_13B = 13_015_864_320
 
 
-@pytest.mark.parametrize("name,count", [("c3", LLAMA2_7B), ("c4", LLAMA2_13B)])
+@pytest.mark.parametrize("name,count", [("llama7b-d32", LLAMA2_7B), ("llama13b-d64", LLAMA2_13B)])
 def test_whole_model_parameters_match_published_llama2(name, count):
     """A single stage (PP = 1) without TP holds the whole model: embedding,
     L layers and LM head; with ZeRO-0 and no offload its resident states are
@@ -211,7 +211,7 @@ def test_full_offload_working_buffers():
 
 
 def _gpt_small():
-    wl = W.workload("c1")
+    wl = W.workload("gpt1.3b-d8")
     wl["space"] = {"n_devices": 4, "global_batch": 64, "mb": [1, 2, 4], "ratios": [0.0, 1.0],
                    "n_buckets": 64, "l_rule": W.L_FULL}
     return wl
@@ -338,7 +338,7 @@ def test_optimizer_offload_time_plausible():
     states of a 7B model at PP = 4 on L4 GPUs (Sec. 3.2).  With PCIe Gen3 x16
     (about 16 GB/s) the first-microbatch state traffic of the first of four
     stages must be within an order of magnitude of that."""
-    wl = W.workload("c3")
+    wl = W.workload("llama7b-d32")
     wl["hws"] = [W.hw_sample(0, {"flops": 121e12, "mem_bytes": 24e9, "pcie_bw": 16e9, "link_bw": 12.5e9})]
     wl["space"] = {"n_devices": 8, "global_batch": 64, "mb": [1], "ratios": [0.0, 1.0],
                    "n_buckets": 64, "l_rule": W.L_FULL}
@@ -356,11 +356,11 @@ def test_optimizer_offload_time_plausible():
 # descriptor: PP | D with PP <= L; TP | D/PP, TP | heads, TP | ffn; G = B/(b DP)
 # integral; k = 1..PP; stage sizes per rule; 4 ZeRO levels; c = 0..l; R^4).
 TABLE = {
-    "c1": (1_686_400, 1_514),
-    "c2": (273_952_500, 4_527),
-    "c3": (4_218_539_292, 5_370),
-    "c4": (20_314_621_756, 9_634),
-    "c5": (29_939_155_200, 66_496),
+    "gpt1.3b-d8": (1_686_400, 1_514),
+    "gpt2.7b-d16": (273_952_500, 4_527),
+    "llama7b-d32": (4_218_539_292, 5_370),
+    "llama13b-d64": (20_314_621_756, 9_634),
+    "llama42b-d128-hw64": (29_939_155_200, 66_496),
 }
 
 
@@ -393,7 +393,7 @@ def _count_by_brute_force(wl):
     return configs * len(wl["hws"]), groups * len(wl["hws"])
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
+@pytest.mark.parametrize("name", ["gpt1.3b-d8", "gpt2.7b-d16", "llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"])
 def test_space_sizes(name):
     wl = W.workload(name)
     o = O.Oracle(wl)

@@ -23,11 +23,11 @@ def close(a, b, ulps=8):
 
 def _wl(arch="gpt"):
     if arch == "gpt":
-        wl = W.workload("c1")
+        wl = W.workload("gpt1.3b-d8")
         wl["space"] = {"n_devices": 8, "global_batch": 128, "mb": [1, 2, 4], "ratios": [0.0, 0.5, 1.0],
                        "n_buckets": 64, "l_rule": W.L_FULL}
     else:
-        wl = W.workload("c5")
+        wl = W.workload("llama42b-d128-hw64")
         wl["hws"] = wl["hws"][:1]
         wl["space"] = {"n_devices": 16, "global_batch": 256, "mb": [1, 2], "ratios": [0.0, 0.5, 1.0],
                        "n_buckets": 64, "l_rule": W.L_FULL}
