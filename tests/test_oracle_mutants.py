@@ -128,19 +128,35 @@ def test_planted_mistakes_are_caught():
     assert not survivors, "pins did not catch: %s" % survivors
 
 
-def test_planted_mistakes_in_the_calibration_reference_are_caught():
-    """Each variant of oracle/calib_oracle.py shadows the real one in a copy of the oracle package;
-    the calibration pins must fail on every variant and pass on the unedited copy."""
+# Planted mistakes in the plain-Python inter-stage planner (Eq. 1-3).
+PLAN_MUTANTS = {
+    "inner sum includes the stage itself": ("        v = d - t_sum\n        m = v if m is None else max(m, v)\n        t_sum = t_sum + t",
+                                            "        t_sum = t_sum + t\n        v = d - t_sum\n        m = v if m is None else max(m, v)"),
+    "G microbatches behind the bottleneck": ("return (float(G - 1) * t_max + t_sum) + m", "return (float(G) * t_max + t_sum) + m"),
+    "stage i draws from the wrong in-flight count": ("cand.get((G, PP, PP - i, parts[i]), [])", "cand.get((G, PP, i + 1, parts[i]), [])"),
+    "delta ignored": ("return (float(G - 1) * t_max + t_sum) + m", "return float(G - 1) * t_max + t_sum"),
+}
+
+
+@pytest.mark.parametrize("module,mutants,pins", [
+    ("calib_oracle", "CALIB_MUTANTS", ["tests/test_oracle_calib.py"]),
+    ("plan_oracle", "PLAN_MUTANTS", ["tests/test_oracle_plan.py", "tests/test_plan.py"]),
+])
+def test_planted_mistakes_in_the_python_references_are_caught(module, mutants, pins):
+    """Each variant of a plain-Python reference (the calibration's window and fit, the planner)
+    shadows the real one in a copy of the oracle package; its pins must fail on every variant and
+    pass on the unedited copy."""
     import shutil
-    src_path = os.path.join(ROOT, "oracle", "calib_oracle.py")
+    src_path = os.path.join(ROOT, "oracle", module + ".py")
     with open(src_path) as f:
         src = f.read()
     lib = O.build(force=False)
+    table = globals()[mutants]
     variants = {"unchanged": src}
-    for i, (what, (old, new)) in enumerate(CALIB_MUTANTS.items()):
+    for i, (what, (old, new)) in enumerate(table.items()):
         assert src.count(old) == 1, what
         variants["c%02d" % i] = src.replace(old, new)
-    names = {"c%02d" % i: what for i, what in enumerate(CALIB_MUTANTS)}
+    names = {"c%02d" % i: what for i, what in enumerate(table)}
     with tempfile.TemporaryDirectory() as tmp:
         def run(item):
             key, text = item
@@ -149,13 +165,13 @@ def test_planted_mistakes_in_the_calibration_reference_are_caught():
             for fn in os.listdir(os.path.join(ROOT, "oracle")):
                 if fn.endswith(".py"):
                     shutil.copy(os.path.join(ROOT, "oracle", fn), pkg)
-            with open(os.path.join(pkg, "calib_oracle.py"), "w") as f:
+            with open(os.path.join(pkg, module + ".py"), "w") as f:
                 f.write(text)
             env = dict(os.environ, MIST_ORACLE_LIB=lib,
                        PYTHONPATH=os.pathsep.join([os.path.join(tmp, key), ROOT]))
             r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                                 "-p", "no:randomly", "--rootdir", os.path.join(tmp, key),
-                                os.path.join(ROOT, "tests", "test_oracle_calib.py")],
+                                *[os.path.join(ROOT, p) for p in pins]],
                                cwd=os.path.join(tmp, key), env=env, capture_output=True, text=True, timeout=300)
             return key, (r.returncode == 0, r.stdout[-1500:])
         with ThreadPoolExecutor(max_workers=min(6, os.cpu_count() or 1)) as ex:
@@ -163,4 +179,4 @@ def test_planted_mistakes_in_the_calibration_reference_are_caught():
     ok, out = results.pop("unchanged")
     assert ok, out
     survivors = [names[k] for k, (passed, _) in sorted(results.items()) if passed]
-    assert not survivors, "calibration pins did not catch: %s" % survivors
+    assert not survivors, "pins did not catch: %s" % survivors
