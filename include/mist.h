@@ -176,7 +176,9 @@ typedef struct mist_group_key {
 /* Validates and copies the descriptors (the caller may free them afterwards), enumerates
  * the groups, builds the tables and uploads them to the current HIP device.  hw points to
  * n_hw >= 1 samples.  alloc may be NULL (hipMalloc/hipFree).  On success *out owns every
- * device and host buffer.  Errors: MIST_E_INVALID, MIST_E_NOMEM, MIST_E_DEVICE. */
+ * device and host buffer.  A space may hold no configuration (when no microbatch size and
+ * parallel split fits the global batch): it has no group, and every later call succeeds with
+ * empty results.  Errors: MIST_E_INVALID, MIST_E_NOMEM, MIST_E_DEVICE. */
 mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n_hw,
                               const mist_space_desc* s, const mist_allocator* alloc,
                               mist_space** out);

@@ -30,6 +30,15 @@ mist_status fail_hip(hipError_t e, const char* what) {
   return fail(MIST_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+// Copies that accept an empty range (a space may have no group; a caller may ask for none).
+hipError_t copy_sync(void* dst, const void* src, size_t bytes, hipMemcpyKind kind) {
+  return bytes ? hipMemcpy(dst, src, bytes, kind) : hipSuccess;
+}
+
+hipError_t copy_async(void* dst, const void* src, size_t bytes, hipMemcpyKind kind, hipStream_t st) {
+  return bytes ? hipMemcpyAsync(dst, src, bytes, kind, st) : hipSuccess;
+}
+
 constexpr int64_t kExact = (int64_t)1 << 53;  // integers below this convert to double exactly
 constexpr int64_t kStaticStrips = 512;        // strips per resident wave up to which a space is
                                               // cut into one tile per wave
@@ -328,7 +337,6 @@ std::string enumerate(mist_space* S) {
     }
   }
   S->n_configs = base;
-  if (S->groups.empty()) return "the space has no configuration";
   if (S->groups.size() > (size_t)INT32_MAX) return "too many groups";
 
   // Pair-constant entries, group-major.
@@ -400,7 +408,7 @@ mist_status upload(mist_space* S, T** dst, const std::vector<T>& src, const char
   *dst = (T*)dev_alloc(S, src.size() * sizeof(T));
   if (!*dst) return fail(MIST_E_NOMEM, std::string("device allocation failed: ") + what);
   if (src.empty()) return MIST_OK;
-  const hipError_t e = hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
+  const hipError_t e = copy_sync(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
   if (e != hipSuccess) return fail_hip(e, what);
   return MIST_OK;
 }
@@ -473,11 +481,11 @@ mist_status eval_ids_impl(mist_space* S, const uint64_t* ids, int64_t n, double*
   TempBuf dids(S, (size_t)n * sizeof(uint64_t));
   TempBuf dout(S, (size_t)n * 4 * sizeof(double));
   if (!dids.p || !dout.p) return fail(MIST_E_NOMEM, "device allocation failed: eval_ids");
-  hipError_t e = hipMemcpyAsync(dids.p, ids, (size_t)n * sizeof(uint64_t), hipMemcpyHostToDevice, st);
+  hipError_t e = copy_async(dids.p, ids, (size_t)n * sizeof(uint64_t), hipMemcpyHostToDevice, st);
   if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync ids");
   const int rc = launch_eval_ids(eval_args(S), (const uint64_t*)dids.p, n, (double*)dout.p, st);
   if (rc) return fail_hip((hipError_t)rc, "eval_ids launch");
-  e = hipMemcpyAsync(out, dout.p, (size_t)n * 4 * sizeof(double), hipMemcpyDeviceToHost, st);
+  e = copy_async(out, dout.p, (size_t)n * 4 * sizeof(double), hipMemcpyDeviceToHost, st);
   if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync out");
   e = hipStreamSynchronize(st);
   if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
@@ -782,7 +790,7 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
     if (!k) k = launch_eval(ea, mode_grid(S, kModeCount), kModeCount, st);
     if (k) return fail_hip((hipError_t)k, "exact frontier: count");
     S->h_cnt.resize(nt);
-    hipError_t e = hipMemcpyAsync(S->h_cnt.data(), S->d_cnt_tile, nt * sizeof(int32_t), hipMemcpyDeviceToHost, st);
+    hipError_t e = copy_async(S->h_cnt.data(), S->d_cnt_tile, nt * sizeof(int32_t), hipMemcpyDeviceToHost, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     if (e != hipSuccess) return fail_hip(e, "exact frontier: counts");
     // Candidate slots in group order: a group's full-size tiles, then its small ones.
@@ -834,9 +842,9 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       S->sort_temp_bytes = S->d_sort_temp ? need : 0;
       if (!S->d_sort_temp) return fail(MIST_E_NOMEM, "device allocation failed: sort storage");
     }
-    e = hipMemcpyAsync(S->d_tile_off, S->h_tile_off.data(), nt * sizeof(int64_t), hipMemcpyHostToDevice, st);
+    e = copy_async(S->d_tile_off, S->h_tile_off.data(), nt * sizeof(int64_t), hipMemcpyHostToDevice, st);
     if (e == hipSuccess)
-      e = hipMemcpyAsync(S->d_seg, S->h_seg.data(), (ng + 1) * sizeof(int64_t), hipMemcpyHostToDevice, st);
+      e = copy_async(S->d_seg, S->h_seg.data(), (ng + 1) * sizeof(int64_t), hipMemcpyHostToDevice, st);
     if (e != hipSuccess) return fail_hip(e, "exact frontier: offsets");
     ea.cand_key = S->d_cand_key;
     ea.cand_obj = S->d_cand_obj;
@@ -869,7 +877,7 @@ mist_status mist_get_pareto_exact(mist_space* S, int64_t g, mist_result* out, in
   if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
   try {
     int64_t n = 0;
-    e = hipMemcpy(&n, S->d_front_cnt + g, sizeof(int64_t), hipMemcpyDeviceToHost);
+    e = copy_sync(&n, S->d_front_cnt + g, sizeof(int64_t), hipMemcpyDeviceToHost);
     if (e != hipSuccess) return fail_hip(e, "hipMemcpy frontier count");
     *n_out = n;
     if (n > cap) return fail(MIST_E_RANGE, "cap is smaller than the frontier");
@@ -877,9 +885,9 @@ mist_status mist_get_pareto_exact(mist_space* S, int64_t g, mist_result* out, in
     const size_t b = (size_t)S->h_seg[g];
     std::vector<uint64_t> keys(n), ids(n);
     std::vector<double> objs(n);
-    e = hipMemcpy(keys.data(), S->d_front_key + b, n * 8, hipMemcpyDeviceToHost);
-    if (e == hipSuccess) e = hipMemcpy(ids.data(), S->d_front_id + b, n * 8, hipMemcpyDeviceToHost);
-    if (e == hipSuccess) e = hipMemcpy(objs.data(), S->d_front_obj + b, n * 8, hipMemcpyDeviceToHost);
+    e = copy_sync(keys.data(), S->d_front_key + b, n * 8, hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = copy_sync(ids.data(), S->d_front_id + b, n * 8, hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = copy_sync(objs.data(), S->d_front_obj + b, n * 8, hipMemcpyDeviceToHost);
     if (e != hipSuccess) return fail_hip(e, "hipMemcpy frontier");
     mist_status rc = fill_results(S, ids.data(), objs.data(), n, out);
     if (rc) return rc;
@@ -903,9 +911,9 @@ mist_status mist_get_best(mist_space* S, int64_t g0, int64_t n, mist_result* out
   try {
     std::vector<uint64_t> ids(n);
     std::vector<double> objs(n);
-    hipError_t e = hipMemcpy(ids.data(), S->d_best_id + g0, n * sizeof(uint64_t), hipMemcpyDeviceToHost);
+    hipError_t e = copy_sync(ids.data(), S->d_best_id + g0, n * sizeof(uint64_t), hipMemcpyDeviceToHost);
     if (e == hipSuccess)
-      e = hipMemcpy(objs.data(), S->d_best_obj + g0, n * sizeof(double), hipMemcpyDeviceToHost);
+      e = copy_sync(objs.data(), S->d_best_obj + g0, n * sizeof(double), hipMemcpyDeviceToHost);
     if (e != hipSuccess) return fail_hip(e, "hipMemcpy best");
     return fill_results(S, ids.data(), objs.data(), n, out);
   } catch (const std::bad_alloc&) {
@@ -924,10 +932,10 @@ mist_status mist_get_alpha(mist_space* S, int64_t g0, int64_t n, mist_result* ou
     const size_t A = (size_t)S->A, m = (size_t)n * A;
     std::vector<uint64_t> ids(m);
     std::vector<double> objs(m);
-    hipError_t e = hipMemcpy(ids.data(), S->d_alpha_id + (size_t)g0 * A, m * sizeof(uint64_t),
+    hipError_t e = copy_sync(ids.data(), S->d_alpha_id + (size_t)g0 * A, m * sizeof(uint64_t),
                              hipMemcpyDeviceToHost);
     if (e == hipSuccess)
-      e = hipMemcpy(objs.data(), S->d_alpha_obj + (size_t)g0 * A, m * sizeof(double), hipMemcpyDeviceToHost);
+      e = copy_sync(objs.data(), S->d_alpha_obj + (size_t)g0 * A, m * sizeof(double), hipMemcpyDeviceToHost);
     if (e != hipSuccess) return fail_hip(e, "hipMemcpy weight-sample results");
     std::vector<uint64_t> want;
     for (size_t i = 0; i < m; ++i)
@@ -972,9 +980,9 @@ mist_status mist_plan_pipeline(mist_space* S, int32_t hw, int32_t pp, mist_plan*
   try {
     const size_t A = (size_t)S->A, ng = S->groups.size();
     std::vector<uint64_t> best(ng), alpha(ng * A);
-    hipError_t e = hipMemcpy(best.data(), S->d_best_id, ng * sizeof(uint64_t), hipMemcpyDeviceToHost);
+    hipError_t e = copy_sync(best.data(), S->d_best_id, ng * sizeof(uint64_t), hipMemcpyDeviceToHost);
     if (e == hipSuccess && A)
-      e = hipMemcpy(alpha.data(), S->d_alpha_id, ng * A * sizeof(uint64_t), hipMemcpyDeviceToHost);
+      e = copy_sync(alpha.data(), S->d_alpha_id, ng * A * sizeof(uint64_t), hipMemcpyDeviceToHost);
     if (e != hipSuccess) return fail_hip(e, "hipMemcpy frontier points");
     std::vector<mist_stage_point> pts;
     std::vector<uint64_t> ids;
@@ -1021,13 +1029,13 @@ mist_status mist_get_buckets(mist_space* S, int64_t g0, int64_t n, uint64_t* ids
     const int NB = S->NB;
     std::vector<uint64_t> bid((size_t)n * 64);
     std::vector<double> bobj((size_t)n * 64);
-    hipError_t e = hipMemcpy(bid.data(), S->d_bucket_id + g0 * 64, bid.size() * sizeof(uint64_t),
+    hipError_t e = copy_sync(bid.data(), S->d_bucket_id + g0 * 64, bid.size() * sizeof(uint64_t),
                              hipMemcpyDeviceToHost);
     if (e == hipSuccess)
-      e = hipMemcpy(bobj.data(), S->d_bucket_obj + g0 * 64, bobj.size() * sizeof(double),
+      e = copy_sync(bobj.data(), S->d_bucket_obj + g0 * 64, bobj.size() * sizeof(double),
                     hipMemcpyDeviceToHost);
     if (e == hipSuccess && masks)
-      e = hipMemcpy(masks, S->d_frontier + g0, n * sizeof(uint64_t), hipMemcpyDeviceToHost);
+      e = copy_sync(masks, S->d_frontier + g0, n * sizeof(uint64_t), hipMemcpyDeviceToHost);
     if (e != hipSuccess) return fail_hip(e, "hipMemcpy buckets");
     for (int64_t i = 0; i < n; ++i)
       for (int j = 0; j < NB; ++j) {

@@ -161,6 +161,46 @@ def workload(name: str) -> dict:
 WORKLOADS = ["gpt1.3b-d8", "gpt2.7b-d16", "llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"]
 
 
+def random_space(seed: int) -> dict:
+    """A small seeded random workload for coverage: GPT or Llama (grouped-query) shapes, flash or
+    not, any device count among 1, 2, 3, 4, 6, 8, a random subset of microbatch sizes, 1-6
+    offload ratios drawn from the eighths of [0, 1], 1, 3, 16 or 64 buckets, either layer rule,
+    one or two hardware samples with budgets from 1 MB to 10 GB (log-uniform) and 0-3 weight
+    samples.  Sizes vary widely; callers bound them."""
+    g = SplitMix64(0x5EED0000 + seed)
+
+    def pick(xs):
+        return xs[min(len(xs) - 1, int(g.uniform() * len(xs)))]
+
+    arch = pick([GPT, LLAMA])
+    heads = pick([4, 8, 16])
+    d_h = pick([16, 32, 64])
+    kv = heads if arch == GPT else pick([d for d in (1, 2, 4, 8, 16) if heads % d == 0])
+    L = 2 + int(g.uniform() * 7)
+    h = heads * d_h
+    model = _model(arch, L, h, heads, kv, h * pick([2, 3, 4]), pick([32, 64, 128, 256]),
+                   500 + int(g.uniform() * 3000))
+    model["flash"] = pick([0, 1])
+    D = pick([1, 2, 3, 4, 6, 8])
+    mb = [b for i, b in enumerate([1, 2, 4, 8]) if g.next_u64() >> (7 + i) & 1] or [1]
+    R = 1 + int(g.uniform() * 6)
+    grid = [j / 8 for j in range(9)]
+    ratios_ = []
+    while len(ratios_) < R:
+        r = pick(grid)
+        if r not in ratios_:
+            ratios_.append(r)
+    space = {"n_devices": D, "global_batch": D * pick([4, 8, 16]), "mb": mb, "ratios": sorted(ratios_),
+             "n_buckets": pick([1, 3, 16, 64]), "l_rule": pick([L_FULL, L_BALANCED])}
+    n_alpha = int(g.uniform() * 4)
+    if n_alpha:
+        space["alphas"] = [g.uniform() for _ in range(n_alpha)]
+    hws = [hw_sample(seed * 7 + i, {"mem_bytes": 10.0 ** (6.0 + 4.0 * g.uniform())})
+           for i in range(1 + int(g.uniform() * 2))]
+    return {"name": "random%d" % seed, "desc": "random small space %d" % seed, "model": model, "hws": hws,
+            "space": space}
+
+
 def with_eta_table(wl: dict, seed: int, lo: float = 0.30, hi: float = 0.90) -> dict:
     """Copy of a workload whose hardware samples take a measured-style efficiency table in place of
     the formula: eta_max = 0 and one efficiency per microbatch size drawn U[lo, hi] from

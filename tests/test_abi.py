@@ -98,3 +98,14 @@ def test_null_arguments():
     assert L.mist_eval_space(None, None) == -1
     assert L.mist_space_destroy(None) == 0
     assert L.mist_last_error() is not None
+
+
+def test_random_small_spaces_are_valid():
+    """The seeded random spaces the GPU parity test draws are accepted by the oracle's checks,
+    and most are small enough for it."""
+    from oracle import oracle as O
+    small = 0
+    for seed in range(60):
+        o = O.Oracle(W.random_space(seed))
+        small += o.n_configs <= 1_500_000
+    assert small >= 50

@@ -49,7 +49,7 @@ def _eval(S, torch_cuda):
 def _compare_groups(S, ref, groups):
     ids, objs, masks = S.buckets(0, S.n_groups)
     best = S.best(0, S.n_groups)
-    gi = np.asarray(groups)
+    gi = np.asarray(groups, dtype=np.int64)
     assert np.array_equal(ids[gi], ref["bucket_id"]), "bucket ids differ"
     assert np.array_equal(objs[gi], ref["bucket_obj"]), "bucket objectives differ"
     assert np.array_equal(masks[gi], ref["frontier"]), "frontier bits differ"
@@ -323,3 +323,46 @@ def test_allocator_failure_is_reported(torch_cuda):
                                  ctypes.byref(h))
         assert rc == -2 and "allocation" in L.mist_last_error().decode()
         assert not live, "buffers left behind"
+
+
+@pytest.mark.parametrize("chunk", range(4))
+def test_random_small_spaces(chunk, torch_cuda):
+    """Seeded random small spaces (GPT and grouped-query Llama shapes, flash or not, device counts
+    1-8 including 3 and 6, random microbatch subsets, 1-6 ratios from the eighths of [0, 1], 1-64
+    buckets, both layer rules, one or two hardware samples with budgets from 1 MB to 10 GB,
+    0-3 weight samples): buckets, best, frontier bits, weight samples and exact frontiers of every
+    group, and sampled per-configuration values, against the oracle."""
+    from paper_2503_19050_amd import mist
+    n = 0
+    for seed in range(chunk * 15, chunk * 15 + 15):
+        wl = W.random_space(seed)
+        o = O.Oracle(wl)
+        if o.n_configs > 1_500_000:
+            continue
+        say("random space", seed, o.n_configs, "configs", o.n_groups, "groups")
+        S = mist.from_workload(wl)
+        S.eval()
+        S.eval_pareto_exact()
+        torch_cuda.cuda.synchronize()
+        if o.n_configs == 0:  # no (b, TP) pair fits the batch: every call succeeds, results empty
+            assert S.n_groups == 0 and S.best() == [] and S.alpha() == []
+            assert S.plan(0) is None
+            with pytest.raises(mist.MistError):
+                S.pareto(0)
+            S.close()
+            continue
+        _compare_groups(S, o.run(), list(range(o.n_groups)))
+        alphas = wl["space"].get("alphas", [])
+        if alphas:
+            ref = o.run_alpha(alphas)
+            res = S.alpha(0, S.n_groups)
+            assert np.array_equal(np.array([[r["id"] for r in row] for row in res], dtype=np.uint64), ref["id"])
+            assert np.array_equal(np.array([[r["obj"] for r in row] for row in res]), ref["obj"])
+        for g in range(o.n_groups):
+            got, want = S.pareto_exact(g), o.pareto_exact(g)
+            assert [r["id"] for r in got] == [int(i) for i in want["id"]], (seed, g)
+            assert [r["obj"] for r in got] == list(want["obj"]), (seed, g)
+        _compare_ids(S, o, _sample_ids(o, np.random.default_rng(seed), 300))
+        S.close()
+        n += 1
+    assert n >= 10
