@@ -187,7 +187,8 @@ def main() -> int:
         runs.sort()
         exact = {"ms_per_run": runs[len(runs) // 2], "runs": len(runs),
                  "what": "exact time-vs-memory frontier of every group after the evaluation: candidate filter, "
-                         "count and emit passes of the evaluation kernel, segmented sort by memory, scan; host "
+                         "one candidate pass of the evaluation kernel (plus the tiles whose candidates overflowed their "
+                         "window), segmented sort by memory, scan; host "
                          "wall time including its one synchronisation"}
 
     alpha = None

@@ -113,6 +113,10 @@ typedef struct mist_space_desc {
                             full-size tile of the evaluation kernel, at least (0: 8192) */
   int32_t max_blocks;    /* cap on the evaluation kernel's grid (0: every block that fits on the
                             device at once) */
+  int32_t cand_window;   /* exact frontier, results do not depend on it: each tile first writes
+                            its candidates to a window of ceil(configurations / cand_window)
+                            slots, and a tile with more is evaluated a second time (0: 8, raised
+                            as needed to keep all windows within 2^27 slots) */
 } mist_space_desc;
 
 /* Device memory provider, e.g. PyTorch's caching allocator.  alloc returns NULL on
@@ -231,8 +235,10 @@ mist_status mist_plan_pipeline(mist_space* S, int32_t hw, int32_t pp, mist_plan*
  * mist_eval_space, finds for each group the feasible configurations whose obj is strictly
  * below that of every configuration before them in (mem, obj, id) order.  A candidate pass
  * keeps only configurations that beat every lower bucket's minimum and are not dominated by
- * their bucket's winner; they are sorted by memory per group and scanned.  Waits for the
- * evaluation and once more for the candidate count, then enqueues the rest on hip_stream.
+ * their bucket's winner (each tile writes them to a window of its own and counts them; tiles
+ * with more than their window holds are evaluated a second time, see cand_window); they are
+ * sorted by memory per group and scanned.  Waits for the evaluation and once more for the
+ * candidate counts, then enqueues the rest on hip_stream.
  * Errors: MIST_E_STATE (no evaluation yet), MIST_E_RANGE (2^32 candidates or more),
  * MIST_E_NOMEM, MIST_E_DEVICE. */
 mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream);

@@ -107,6 +107,27 @@ __global__ __launch_bounds__(256) void k_front_scan(const uint32_t* __restrict__
   if (lane == 0) front_cnt[g] = w - b;
 }
 
+// One wave per tile: its window's candidates, in order, to the tile's place in group order.
+__global__ __launch_bounds__(256) void k_compact(const uint64_t* __restrict__ slab_key,
+                                                 const double* __restrict__ slab_obj,
+                                                 const uint64_t* __restrict__ slab_id,
+                                                 const int64_t* __restrict__ slab_begin,
+                                                 const int32_t* __restrict__ cnt,
+                                                 const int64_t* __restrict__ tile_off, int32_t n_tiles,
+                                                 uint64_t* __restrict__ cand_key, double* __restrict__ cand_obj,
+                                                 uint64_t* __restrict__ cand_id) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= n_tiles) return;
+  const int64_t src = slab_begin[t], n = cnt[t], dst = tile_off[t];
+  if (n > slab_begin[t + 1] - src) return;  // overflowed: the tile is evaluated again
+  for (int64_t i = lane; i < n; i += 64) {
+    cand_key[dst + i] = slab_key[src + i];
+    cand_obj[dst + i] = slab_obj[src + i];
+    cand_id[dst + i] = slab_id[src + i];
+  }
+}
+
 int last_error() {
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? 0 : (int)e;
@@ -132,6 +153,15 @@ int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_in, ui
     if (e != hipSuccess) rc = (int)e;
   }
   return rc;
+}
+
+int launch_compact(const uint64_t* slab_key, const double* slab_obj, const uint64_t* slab_id,
+                   const int64_t* slab_begin, const int32_t* cnt, const int64_t* tile_off, int32_t n_tiles,
+                   uint64_t* cand_key, double* cand_obj, uint64_t* cand_id, void* stream) {
+  if (n_tiles <= 0) return 0;
+  hipLaunchKernelGGL(k_compact, dim3((unsigned)((n_tiles + 3) / 4)), dim3(256), 0, (hipStream_t)stream, slab_key,
+                     slab_obj, slab_id, slab_begin, cnt, tile_off, n_tiles, cand_key, cand_obj, cand_id);
+  return last_error();
 }
 
 int launch_front_scan(const uint32_t* order, const uint64_t* sorted_key, const double* cand_obj,

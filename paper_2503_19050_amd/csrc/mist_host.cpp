@@ -44,6 +44,9 @@ constexpr int64_t kStaticStrips = 512;        // strips per resident wave up to 
                                               // cut into one tile per wave
 constexpr int64_t kMinTileConfigs = 8192;     // configurations per tile of a larger space, at least
 constexpr int64_t kMaxTiles = 131072;         // and tiles per space, at most
+constexpr int64_t kWindowDiv = 8;             // exact frontier: candidate window of a tile,
+                                              // 1/kWindowDiv of its configurations
+constexpr int64_t kWindowSlots = (int64_t)1 << 27;  // and all windows together, at most
 constexpr int64_t kTailPercent = 10;          // share of each group's strips in small tiles
 constexpr int64_t kStripAlign = kWaveTile;    // strips per tile: a multiple of the wave
 
@@ -83,6 +86,7 @@ struct mist_space {
   int32_t eval_grid = 0;
   int64_t tile_configs = 0;  // configurations per full-size tile, at least
   int32_t max_blocks = 0;    // cap on the evaluation grid (0: none)
+  int32_t cand_window = 0;   // exact frontier: window divisor (0: automatic)
   double* d_part_obj = nullptr;
   uint64_t* d_part_id = nullptr;
   double* d_bucket_obj = nullptr;
@@ -106,11 +110,20 @@ struct mist_space {
   FiltEntry* d_filt = nullptr;
   int32_t* d_cnt_tile = nullptr;
   int64_t* d_tile_off = nullptr;
+  int64_t* d_tile_end = nullptr;
+  int32_t* d_list = nullptr;
+  // Candidate windows: tile t writes to slots [slab_begin[t], slab_begin[t+1]) first.
+  std::vector<int64_t> h_slab_begin, h_tile_end;
+  std::vector<int32_t> h_list;
+  int64_t* d_slab_begin = nullptr;
+  uint64_t *d_slab_key = nullptr, *d_slab_id = nullptr;
+  double* d_slab_obj = nullptr;
   int64_t* d_seg = nullptr;
   int64_t* d_front_cnt = nullptr;
   std::vector<int32_t> h_cnt;
   std::vector<int64_t> h_tile_off, h_seg;
   int64_t cand_cap = 0, n_cand = 0;
+  int32_t n_rerun = 0;  // tiles the last call evaluated a second time
   uint64_t *d_cand_key = nullptr, *d_cand_id = nullptr, *d_key_sorted = nullptr;
   double* d_cand_obj = nullptr;
   uint32_t *d_idx_in = nullptr, *d_idx_out = nullptr;
@@ -222,8 +235,8 @@ std::string validate(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n
   if (s->l_rule != MIST_L_FULL && s->l_rule != MIST_L_BALANCED) return "unknown l_rule";
   if (s->n_alphas < 0 || s->n_alphas > MIST_MAX_ALPHAS || (s->n_alphas > 0 && !s->alphas))
     return "n_alphas out of range";
-  if (s->tile_configs < 0 || s->tile_configs > ((int64_t)1 << 40) || s->max_blocks < 0)
-    return "tile_configs and max_blocks must be non-negative";
+  if (s->tile_configs < 0 || s->tile_configs > ((int64_t)1 << 40) || s->max_blocks < 0 || s->cand_window < 0)
+    return "tile_configs, max_blocks and cand_window must be non-negative";
   for (int32_t i = 0; i < s->n_alphas; ++i)
     if (!(s->alphas[i] >= 0.0 && s->alphas[i] <= 1.0)) return "weight samples must lie in [0, 1]";
   return "";
@@ -621,6 +634,7 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
     for (int32_t i = 0; i < s->n_ratios; ++i) S->ratio_om.push_back(1.0 - s->ratios[i]);
     S->tile_configs = s->tile_configs > 0 ? s->tile_configs : kMinTileConfigs;
     S->max_blocks = s->max_blocks;
+    S->cand_window = s->cand_window;
     S->A = s->n_alphas;
     S->alphas.assign(s->alphas, s->alphas + s->n_alphas);
     for (int32_t i = 0; i < s->n_alphas; ++i) S->betas.push_back(1.0 - s->alphas[i]);
@@ -773,41 +787,87 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
     hipStream_t st = (hipStream_t)hip_stream;
     const size_t nt = S->tiles.size(), ng = S->groups.size();
     if (!S->d_filt) {
-      S->d_filt = (FiltEntry*)dev_alloc(S, ng * 64 * sizeof(FiltEntry));
-      S->d_cnt_tile = (int32_t*)dev_alloc(S, nt * sizeof(int32_t));
-      S->d_tile_off = (int64_t*)dev_alloc(S, nt * sizeof(int64_t));
+      // Windows: ceil(configurations / div) slots per tile.
+      const int64_t R2 = (int64_t)S->R * S->R;
+      auto slots = [&](int64_t div) {
+        int64_t n = 0;
+        for (const DevTile& T : S->tiles) n += ((int64_t)(T.strip_end - T.strip_begin) * R2 + div - 1) / div;
+        return n;
+      };
+      int64_t div = S->cand_window > 0 ? S->cand_window : kWindowDiv;
+      if (S->cand_window == 0)
+        while (slots(div) > kWindowSlots) div *= 2;
+      S->h_slab_begin.assign(nt + 1, 0);
+      for (size_t t = 0; t < nt; ++t) {
+        const DevTile& T = S->tiles[t];
+        S->h_slab_begin[t + 1] = S->h_slab_begin[t] + ((int64_t)(T.strip_end - T.strip_begin) * R2 + div - 1) / div;
+      }
+      const size_t n_slab = (size_t)std::max<int64_t>(S->h_slab_begin[nt], 1);
+      S->d_filt = (FiltEntry*)dev_alloc(S, std::max<size_t>(ng, 1) * 64 * sizeof(FiltEntry));
+      S->d_cnt_tile = (int32_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int32_t));
+      S->d_tile_off = (int64_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int64_t));
+      S->d_tile_end = (int64_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int64_t));
+      S->d_list = (int32_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int32_t));
       S->d_seg = (int64_t*)dev_alloc(S, (ng + 1) * sizeof(int64_t));
-      S->d_front_cnt = (int64_t*)dev_alloc(S, ng * sizeof(int64_t));
-      if (!S->d_filt || !S->d_cnt_tile || !S->d_tile_off || !S->d_seg || !S->d_front_cnt)
+      S->d_front_cnt = (int64_t*)dev_alloc(S, std::max<size_t>(ng, 1) * sizeof(int64_t));
+      S->d_slab_begin = (int64_t*)dev_alloc(S, (nt + 1) * sizeof(int64_t));
+      S->d_slab_key = (uint64_t*)dev_alloc(S, n_slab * 8);
+      S->d_slab_obj = (double*)dev_alloc(S, n_slab * 8);
+      S->d_slab_id = (uint64_t*)dev_alloc(S, n_slab * 8);
+      void** bufs[] = {(void**)&S->d_filt,      (void**)&S->d_cnt_tile,   (void**)&S->d_tile_off,
+                       (void**)&S->d_tile_end,  (void**)&S->d_list,       (void**)&S->d_seg,
+                       (void**)&S->d_front_cnt, (void**)&S->d_slab_begin, (void**)&S->d_slab_key,
+                       (void**)&S->d_slab_obj,  (void**)&S->d_slab_id};
+      bool ok = true;
+      for (void** b : bufs) ok = ok && *b;
+      if (!ok) {  // free what was allocated: the next call starts over
+        for (void** b : bufs) {
+          dev_free_one(S, *b);
+          *b = nullptr;
+        }
         return fail(MIST_E_NOMEM, "device allocation failed: exact frontier");
+      }
+      const hipError_t e = copy_sync(S->d_slab_begin, S->h_slab_begin.data(), (nt + 1) * sizeof(int64_t),
+                                     hipMemcpyHostToDevice);
+      if (e != hipSuccess) return fail_hip(e, "exact frontier: windows");
     }
+    // Pass 1: every tile writes its candidates to its window and counts them.
     EvalArgs ea = eval_args(S);
     ea.filt = S->d_filt;
     ea.cnt_tile = S->d_cnt_tile;
-    ea.tile_off = S->d_tile_off;
+    ea.win_begin = S->d_slab_begin;
+    ea.win_end = S->d_slab_begin + 1;
+    ea.tile_list = nullptr;
+    ea.n_list = 0;
+    ea.cand_key = S->d_slab_key;
+    ea.cand_obj = S->d_slab_obj;
+    ea.cand_id = S->d_slab_id;
     int k = launch_filter(ea, S->d_bucket_obj, S->d_bucket_id, S->d_filt, st);
     if (!k) k = launch_pairs(ea, st);  // also resets the tile counters
-    if (!k) k = launch_eval(ea, mode_grid(S, kModeCount), kModeCount, st);
-    if (k) return fail_hip((hipError_t)k, "exact frontier: count");
+    if (!k) k = launch_eval(ea, mode_grid(S, kModeEmit), kModeEmit, st);
+    if (k) return fail_hip((hipError_t)k, "exact frontier: candidates");
     S->h_cnt.resize(nt);
     hipError_t e = copy_async(S->h_cnt.data(), S->d_cnt_tile, nt * sizeof(int32_t), hipMemcpyDeviceToHost, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     if (e != hipSuccess) return fail_hip(e, "exact frontier: counts");
-    // Candidate slots in group order: a group's full-size tiles, then its small ones.
+    // Candidate slots in group order: a group's full-size tiles, then its small ones.  Tiles
+    // whose candidates overflowed their window are listed for pass 2.
     S->h_tile_off.assign(nt, 0);
+    S->h_tile_end.assign(nt, 0);
     S->h_seg.assign(ng + 1, 0);
+    S->h_list.clear();
     int64_t off = 0;
+    auto place = [&](int32_t t) {
+      S->h_tile_off[t] = off;
+      off += S->h_cnt[t];
+      S->h_tile_end[t] = off;
+      if (S->h_cnt[t] > S->h_slab_begin[t + 1] - S->h_slab_begin[t]) S->h_list.push_back(t);
+    };
     for (size_t g = 0; g < ng; ++g) {
       const DevGroup& G = S->groups[g];
       S->h_seg[g] = off;
-      for (int32_t t = G.tile_begin; t < G.tile_begin + G.n_tiles; ++t) {
-        S->h_tile_off[t] = off;
-        off += S->h_cnt[t];
-      }
-      for (int32_t t = G.tail_begin; t < G.tail_begin + G.n_tail; ++t) {
-        S->h_tile_off[t] = off;
-        off += S->h_cnt[t];
-      }
+      for (int32_t t = G.tile_begin; t < G.tile_begin + G.n_tiles; ++t) place(t);
+      for (int32_t t = G.tail_begin; t < G.tail_begin + G.n_tail; ++t) place(t);
     }
     S->h_seg[ng] = off;
     if (off >= ((int64_t)1 << 32)) return fail(MIST_E_RANGE, "exact frontier: more than 2^32 candidates");
@@ -842,15 +902,30 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       S->sort_temp_bytes = S->d_sort_temp ? need : 0;
       if (!S->d_sort_temp) return fail(MIST_E_NOMEM, "device allocation failed: sort storage");
     }
+    const int32_t n_list = (int32_t)S->h_list.size();
     e = copy_async(S->d_tile_off, S->h_tile_off.data(), nt * sizeof(int64_t), hipMemcpyHostToDevice, st);
     if (e == hipSuccess)
       e = copy_async(S->d_seg, S->h_seg.data(), (ng + 1) * sizeof(int64_t), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess && n_list > 0)
+      e = copy_async(S->d_tile_end, S->h_tile_end.data(), nt * sizeof(int64_t), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess && n_list > 0)
+      e = copy_async(S->d_list, S->h_list.data(), (size_t)n_list * sizeof(int32_t), hipMemcpyHostToDevice, st);
     if (e != hipSuccess) return fail_hip(e, "exact frontier: offsets");
-    ea.cand_key = S->d_cand_key;
-    ea.cand_obj = S->d_cand_obj;
-    ea.cand_id = S->d_cand_id;
-    k = launch_pairs(ea, st);
-    if (!k) k = launch_eval(ea, mode_grid(S, kModeEmit), kModeEmit, st);
+    // The windows that held their tile's candidates move to group order; pass 2 evaluates the
+    // listed tiles again, writing straight to their slots.
+    k = launch_compact(S->d_slab_key, S->d_slab_obj, S->d_slab_id, S->d_slab_begin, S->d_cnt_tile, S->d_tile_off,
+                       (int32_t)nt, S->d_cand_key, S->d_cand_obj, S->d_cand_id, st);
+    if (!k && n_list > 0) {
+      ea.win_begin = S->d_tile_off;
+      ea.win_end = S->d_tile_end;
+      ea.tile_list = S->d_list;
+      ea.n_list = n_list;
+      ea.cand_key = S->d_cand_key;
+      ea.cand_obj = S->d_cand_obj;
+      ea.cand_id = S->d_cand_id;
+      k = launch_pairs(ea, st);
+      if (!k) k = launch_eval(ea, mode_grid(S, kModeEmit), kModeEmit, st);
+    }
     if (!k) {
       size_t bytes = S->sort_temp_bytes;
       k = exact_sort(S->d_cand_key, S->d_key_sorted, S->d_idx_in, S->d_idx_out, off, (int64_t)ng, S->d_seg,
@@ -861,6 +936,7 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
                             S->d_front_key, S->d_front_obj, S->d_front_id, S->d_front_cnt, st);
     if (k) return fail_hip((hipError_t)k, "exact frontier");
     S->n_cand = off;
+    S->n_rerun = n_list;
     S->exact_done = true;
     S->exact_stream = st;
     return MIST_OK;

@@ -89,8 +89,7 @@ struct FiltEntry {
 // Evaluation kernel variants.
 constexpr int kModeBuckets = 0;  // bucket minima (and per-tile partials)
 constexpr int kModeAlpha = 1;    // bucket minima and the weight-sampled argmins
-constexpr int kModeCount = 2;    // exact frontier: count each tile's candidates
-constexpr int kModeEmit = 3;     // exact frontier: write each tile's candidates
+constexpr int kModeEmit = 2;     // exact frontier: write and count each tile's candidates
 
 struct EvalArgs {
   DevModel m;
@@ -117,10 +116,16 @@ struct EvalArgs {
   const double* beta;    // [n_alpha]
   double* part_aobj;     // [n_tiles][n_alpha]
   uint64_t* part_aid;    // [n_tiles][n_alpha]
-  // Exact frontier (count and emit variants).
+  // Exact frontier (emit variant).  Tile t writes its candidates, in evaluation order, to
+  // slots [win_begin[t], win_end[t]) of cand_* and drops those past the window; its total
+  // count goes to cnt_tile[t].  With tile_list set, the kernel runs only the n_list tiles
+  // listed there.
   const FiltEntry* filt;     // [n_groups][64]
-  int32_t* cnt_tile;         // [n_tiles] candidates per tile (count variant)
-  const int64_t* tile_off;   // [n_tiles] first candidate slot of each tile (emit variant)
+  int32_t* cnt_tile;         // [n_tiles]
+  const int64_t* win_begin;  // [n_tiles]
+  const int64_t* win_end;    // [n_tiles]
+  const int32_t* tile_list;  // nullptr: every tile
+  int32_t n_list;
   uint64_t* cand_key;        // memory bit patterns (a non-negative double orders like its bits)
   double* cand_obj;
   uint64_t* cand_id;
@@ -157,6 +162,11 @@ int launch_filter(const EvalArgs& a, const double* bucket_obj, const uint64_t* b
 // idx_out, and the per-group scan keeps the staircase.
 int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_in, uint32_t* idx_out, int64_t n,
                int64_t n_groups, const int64_t* seg, void* temp, size_t* temp_bytes, void* stream);
+// Moves each tile's candidates from its window [slab_begin[t], slab_begin[t+1]) to
+// [tile_off[t], tile_off[t] + cnt[t]); tiles whose count exceeds the window are skipped.
+int launch_compact(const uint64_t* slab_key, const double* slab_obj, const uint64_t* slab_id,
+                   const int64_t* slab_begin, const int32_t* cnt, const int64_t* tile_off, int32_t n_tiles,
+                   uint64_t* cand_key, double* cand_obj, uint64_t* cand_id, void* stream);
 int launch_front_scan(const uint32_t* order, const uint64_t* sorted_key, const double* cand_obj,
                       const uint64_t* cand_id, const int64_t* seg, int64_t n_groups, uint64_t* front_key,
                       double* front_obj, uint64_t* front_id, int64_t* front_cnt, void* stream);

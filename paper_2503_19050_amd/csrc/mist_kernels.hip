@@ -345,13 +345,13 @@ template <int R>
 constexpr int eval_waves() { return 4; }
 
 // MODE kModeBuckets: bucket minima; kModeAlpha: also the weight-sampled argmins of Eq. 4
-// (a.n_alpha samples); kModeCount / kModeEmit: the exact frontier's candidates, counted or
-// written per tile (the bucket reduction is skipped).
+// (a.n_alpha samples); kModeEmit: the exact frontier's candidates, written and counted per
+// tile (the bucket reduction is skipped).
 template <int R, int MODE>
 __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, const double* __restrict__ ratio,
                                                                  const PairK* __restrict__ pk) {
   constexpr bool AL = MODE == kModeAlpha;
-  constexpr bool EX = MODE == kModeCount || MODE == kModeEmit;
+  constexpr bool EX = MODE == kModeEmit;
   constexpr int R2 = R * R;
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
   constexpr int IB = ia_block<R>();
@@ -373,17 +373,21 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
   BucketEntry* bucket = s_bucket[wave];
   const unsigned long long kEmpty = (unsigned long long)__double_as_longlong(__builtin_huge_val());
 
-  // Tile schedule: wave w of the grid takes tile w.  Tile n_waves + x + kClaimCounters * c
-  // goes to the claim that draws number c from counter x (counters reset to 0 by K0); a wave
-  // draws from the counter of its block's XCD and moves to the next counter when one runs
-  // out, until all have.  When the grid has at least as many waves as there are tiles no
-  // claim is made.
+  // Tile schedule: wave w of the grid takes work item w.  Item n_waves + x + kClaimCounters
+  // * c goes to the claim that draws number c from counter x (counters reset to 0 by K0); a
+  // wave draws from the counter of its block's XCD and moves to the next counter when one
+  // runs out, until all have.  When the grid has at least as many waves as there are items
+  // no claim is made.  Item x is tile x, or tile tile_list[x] when the emit variant runs a
+  // list.
+  const bool listed = EX && a.tile_list != nullptr;
+  const int n_items = listed ? a.n_list : a.n_tiles;
   const int n_waves = (int)gridDim.x * kWaves;
-  const bool claims = a.n_tiles > n_waves;
+  const bool claims = n_items > n_waves;
   int counter = (int)(blockIdx.x % kClaimCounters);
   int exhausted = 0;
   int loaded_hw = -1;
-  for (int t = (int)blockIdx.x * kWaves + wave; t < a.n_tiles;) {
+  for (int x = (int)blockIdx.x * kWaves + wave; x < n_items;) {
+    const int t = listed ? a.tile_list[x] : x;
     const DevTile tile = a.tiles[t];
     const DevGroup g = a.groups[tile.group];
     const DevHw& hw = a.hws[g.hw];
@@ -403,14 +407,14 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
       bucket[64].lid = 0u;
     }
     const double Gd = (double)g.G;
-    int64_t n_cand = 0;  // exact frontier: candidates counted, or the next slot to write
-    int64_t n_end = 0;   // emit: end of the tile's slots (the count pass's total)
+    int64_t n_cand = 0;  // exact frontier: the next candidate's slot
+    int64_t n_beg = 0;   // and the tile's window of slots
+    int64_t n_end = 0;
     if constexpr (EX) {
       s_filt[wave][lane] = a.filt[(size_t)tile.group * 64 + lane];
-      if constexpr (MODE == kModeEmit) {
-        n_cand = a.tile_off[t];
-        n_end = n_cand + a.cnt_tile[t];
-      }
+      n_beg = a.win_begin[t];
+      n_end = a.win_end[t];
+      n_cand = n_beg;
     }
     if constexpr (AL) {
       if (lane < a.n_alpha) {
@@ -522,16 +526,14 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
               const bool cand = (mem <= M) & (obj < f.pm) &
                                 !(((obj > f.bobj) & (mem >= f.bmem)) | ((obj >= f.bobj) & (mem > f.bmem)));
               const unsigned long long m = __builtin_amdgcn_ballot_w64(cand);
-              if constexpr (MODE == kModeEmit) {
-                if (cand) {
-                  const unsigned int below = __builtin_amdgcn_mbcnt_hi(
-                      (unsigned int)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)m, 0u));
-                  const int64_t slot = n_cand + below;
-                  if (slot < n_end) {  // the count pass evaluated the same operations
-                    a.cand_key[slot] = (unsigned long long)__double_as_longlong(mem);
-                    a.cand_obj[slot] = obj;
-                    a.cand_id[slot] = g.base + (uint64_t)(lid_oo + (unsigned int)ia);
-                  }
+              if (cand) {
+                const unsigned int below = __builtin_amdgcn_mbcnt_hi(
+                    (unsigned int)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)m, 0u));
+                const int64_t slot = n_cand + below;
+                if (slot < n_end) {  // past the window: counted only
+                  a.cand_key[slot] = (unsigned long long)__double_as_longlong(mem);
+                  a.cand_obj[slot] = obj;
+                  a.cand_id[slot] = g.base + (uint64_t)(lid_oo + (unsigned int)ia);
                 }
               }
               n_cand += __builtin_popcountll(m);
@@ -625,7 +627,7 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
     }
     // The tile's partials: lane j = bucket j.
     if constexpr (EX) {
-      if (MODE == kModeCount && lane == 0) a.cnt_tile[t] = (int32_t)n_cand;
+      if (lane == 0) a.cnt_tile[t] = (int32_t)(n_cand - n_beg);
     } else {
       wave_sync();
       const unsigned int bl = bucket[lane].lid;
@@ -645,12 +647,12 @@ __global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, co
       if (lane == 0) c = atomicAdd(a.work + counter * kCounterStride, 1);
       c = __builtin_amdgcn_readfirstlane(__shfl(c, 0, 64));
       const int64_t next = (int64_t)n_waves + counter + (int64_t)kClaimCounters * c;
-      if (next < a.n_tiles) {
-        t = (int)next;
+      if (next < n_items) {
+        x = (int)next;
         break;
       }
-      if (++exhausted == kClaimCounters) {  // every counter has run out: no tile is left
-        t = a.n_tiles;
+      if (++exhausted == kClaimCounters) {  // every counter has run out: no item is left
+        x = n_items;
         break;
       }
       counter = counter + 1 == kClaimCounters ? 0 : counter + 1;
@@ -846,7 +848,6 @@ template <int R>
 void launch_eval_r(const EvalArgs& a, int blocks, int mode, hipStream_t st) {
   switch (mode) {
     case kModeAlpha: launch_eval_rm<R, kModeAlpha>(a, blocks, st); break;
-    case kModeCount: launch_eval_rm<R, kModeCount>(a, blocks, st); break;
     case kModeEmit: launch_eval_rm<R, kModeEmit>(a, blocks, st); break;
     default: launch_eval_rm<R, kModeBuckets>(a, blocks, st); break;
   }
@@ -862,7 +863,6 @@ template <int R>
 int blocks_per_cu_r(int mode) {
   switch (mode) {
     case kModeAlpha: return blocks_per_cu_rm<R, kModeAlpha>();
-    case kModeCount: return blocks_per_cu_rm<R, kModeCount>();
     case kModeEmit: return blocks_per_cu_rm<R, kModeEmit>();
     default: return blocks_per_cu_rm<R, kModeBuckets>();
   }

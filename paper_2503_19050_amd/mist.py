@@ -56,7 +56,8 @@ class SpaceDesc(ctypes.Structure):
                 ("ratios", ctypes.POINTER(ctypes.c_double)), ("n_ratios", ctypes.c_int32),
                 ("n_buckets", ctypes.c_int32), ("l_rule", ctypes.c_int32),
                 ("n_alphas", ctypes.c_int32), ("alphas", ctypes.POINTER(ctypes.c_double)),
-                ("tile_configs", ctypes.c_int64), ("max_blocks", ctypes.c_int32)]
+                ("tile_configs", ctypes.c_int64), ("max_blocks", ctypes.c_int32),
+                ("cand_window", ctypes.c_int32)]
 
 
 MAX_STAGES = 64
@@ -228,7 +229,8 @@ class Space:
                                 self._ratios.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
                                 len(self._ratios), space["n_buckets"], space["l_rule"], self.n_alphas,
                                 self._alphas.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
-                                int(space.get("tile_configs", 0)), int(space.get("max_blocks", 0)))
+                                int(space.get("tile_configs", 0)), int(space.get("max_blocks", 0)),
+                                int(space.get("cand_window", 0)))
         self._alloc = None
         if allocator == "torch":
             self._alloc = self._torch_allocator()

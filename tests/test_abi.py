@@ -58,7 +58,7 @@ def _create(wl, **over):
                            len(mb), r.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), len(r),
                            s["n_buckets"], s["l_rule"], n_al,
                            al.ctypes.data_as(ctypes.POINTER(ctypes.c_double)) if len(al) else None,
-                           s.get("tile_configs", 0), s.get("max_blocks", 0))
+                           s.get("tile_configs", 0), s.get("max_blocks", 0), s.get("cand_window", 0))
     h = ctypes.c_void_p()
     rc = L.mist_space_create(ctypes.byref(model), hw, len(hws), ctypes.byref(space), None, ctypes.byref(h))
     return rc, L.mist_last_error().decode()
@@ -72,7 +72,7 @@ def _create(wl, **over):
     {"s__ratios": [j / 16 for j in range(17)]},
     {"s__alphas": [0.5, 1.5]}, {"s__alphas": [-0.25]}, {"s__alphas": [float("nan")]},
     {"s__alphas": [0.5] * 17}, {"s__n_alphas": 2}, {"s__n_alphas": -1},
-    {"s__tile_configs": -1}, {"s__max_blocks": -4},
+    {"s__tile_configs": -1}, {"s__max_blocks": -4}, {"s__cand_window": -1},
 ])
 def test_invalid_descriptors_are_rejected(over):
     rc, msg = _create(W.workload("tiny"), **over)

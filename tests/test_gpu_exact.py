@@ -83,3 +83,31 @@ def test_exact_and_plan_states(torch_cuda):
     with pytest.raises(mist.MistError):
         S.pareto_exact(0)
     S.close()
+
+
+@pytest.mark.parametrize("name", ["tight", "gpt1.3b-d8", "gpt2.7b-d16"])
+def test_candidate_windows_do_not_change_results(name, torch_cuda):
+    """The frontier does not depend on the candidate windows: windows as large as their tiles
+    (no tile evaluated twice), the default, small ones (many tiles evaluated twice) and windows
+    of one slot (every tile with two or more candidates evaluated twice); each space evaluated
+    twice in a row, against the oracle on a sample of groups."""
+    from paper_2503_19050_amd import mist
+    wl = _tight() if name == "tight" else W.workload(name)
+    o = O.Oracle(wl)
+    rng = np.random.default_rng(11)
+    groups = sorted({0, o.n_groups - 1} | set(int(g) for g in rng.choice(o.n_groups, size=min(12, o.n_groups),
+                                                                           replace=False)))
+    want = {g: o.pareto_exact(g) for g in groups}
+    for window in (1, 0, 64, 1 << 30):
+        say(name, "cand_window", window)
+        w = dict(wl, space=dict(wl["space"], cand_window=window))
+        S = mist.from_workload(w)
+        for _ in range(2):
+            S.eval()
+            S.eval_pareto_exact()
+            for g in groups:
+                got = S.pareto_exact(g)
+                assert [r["id"] for r in got] == [int(i) for i in want[g]["id"]], (window, g)
+                assert [r["obj"] for r in got] == list(want[g]["obj"]), (window, g)
+                assert [r["mem"] for r in got] == list(want[g]["mem"]), (window, g)
+        S.close()

@@ -228,7 +228,7 @@ def test_error_paths(torch_cuda):
 def test_every_ratio_count(R, torch_cuda):
     """The evaluation kernel is compiled per ratio count R (1..16, with activation-ratio blocks
     that change shape with R): every variant — buckets, weight samples and the exact frontier's
-    count and emit passes — against the oracle on a small space, every group in full."""
+    candidate pass — against the oracle on a small space, every group in full."""
     from paper_2503_19050_amd import mist
     wl = W.workload("tiny")
     wl["space"]["ratios"] = [i / (R - 1) for i in range(R)] if R > 1 else [0.0]
