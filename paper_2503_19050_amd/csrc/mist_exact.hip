@@ -28,8 +28,47 @@ __device__ __forceinline__ bool lex_less(double o1, uint64_t i1, double o2, uint
   return o1 < o2 || (o1 == o2 && i1 < i2);
 }
 
+// A wave takes a group's sorted candidates 512 at a time, eight consecutive ones per lane.
+constexpr int kScanItems = 8;
+constexpr int kScanStep = 64 * kScanItems;
+
+struct ScanKeys {  // a step's memory keys and candidate slots
+  uint64_t key[kScanItems];
+  uint32_t ord[kScanItems];
+};
+struct ScanVals {  // and its candidates' objectives and ids
+  double obj[kScanItems];
+  uint64_t id[kScanItems];
+};
+
+// The lane's items i0..i0+7 (past e: no key).
+__device__ __forceinline__ void scan_keys(ScanKeys& k, const uint32_t* __restrict__ order,
+                                          const uint64_t* __restrict__ sorted_key, int64_t i0, int64_t e) {
+#pragma unroll
+  for (int q = 0; q < kScanItems; ++q) {
+    const bool valid = i0 + q < e;
+    k.key[q] = valid ? sorted_key[i0 + q] : kNoKey;
+    k.ord[q] = valid ? order[i0 + q] : 0u;
+  }
+}
+
+__device__ __forceinline__ void scan_vals(ScanVals& v, const ScanKeys& k, const double* __restrict__ cand_obj,
+                                          const uint64_t* __restrict__ cand_id, int64_t i0, int64_t e) {
+#pragma unroll
+  for (int q = 0; q < kScanItems; ++q) {
+    const bool valid = i0 + q < e;
+    v.obj[q] = valid ? cand_obj[k.ord[q]] : __builtin_huge_val();
+    v.id[q] = valid ? cand_id[k.ord[q]] : kNoKey;
+  }
+}
+
 // One wave per group: candidates [seg[g], seg[g+1]) sorted by memory (keys in sorted_key, the
-// candidates' slots in order).
+// candidates' slots in order).  Per step: each run of equal memory is reduced to its (obj, id)
+// minimum by a segmented scan (within the lane over its items, then across the lanes, with the
+// run that crosses into the step carried in); a run's minimum is on the frontier when its
+// objective is below the minima of every earlier run (a prefix minimum over the run ends,
+// within the lane, across the lanes, and over the earlier steps).  Loads run ahead of the
+// scan: keys and slots two steps, objectives and ids one step.
 __global__ __launch_bounds__(256) void k_front_scan(const uint32_t* __restrict__ order,
                                                     const uint64_t* __restrict__ sorted_key,
                                                     const double* __restrict__ cand_obj,
@@ -41,68 +80,142 @@ __global__ __launch_bounds__(256) void k_front_scan(const uint32_t* __restrict__
   const int64_t g = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (g >= n_groups) return;
   const int64_t b = seg[g], e = seg[g + 1];
+  const int64_t li = (int64_t)lane * kScanItems;
   int64_t w = b;
   double carry = __builtin_huge_val();  // minimum objective of the completed runs before
-  uint64_t run_key = kNoKey;            // a run continuing from the previous chunk: its memory
+  uint64_t run_key = kNoKey;            // a run continuing from the previous step: its memory
   double run_obj = __builtin_huge_val();  // and its minimum so far
   uint64_t run_id = kNoKey;
-  for (int64_t c = b; c < e; c += 64) {
-    const int64_t i = c + lane;
-    const bool valid = i < e;
-    const uint32_t k = valid ? order[i] : 0u;
-    const uint64_t key = valid ? sorted_key[i] : kNoKey;
-    const uint64_t next = i + 1 < e ? sorted_key[i + 1] : kNoKey;
-    double o = valid ? cand_obj[k] : __builtin_huge_val();
-    uint64_t id = valid ? cand_id[k] : kNoKey;
-    uint64_t prev = __shfl_up(key, 1, 64);
-    if (lane == 0) prev = run_key;
-    const bool start = valid && key != prev;
-    if (lane == 0 && valid && !start && lex_less(run_obj, run_id, o, id)) {
-      o = run_obj;
-      id = run_id;
+  ScanKeys k0, k1;
+  ScanVals v0;
+  if (b < e) {
+    scan_keys(k0, order, sorted_key, b + li, e);
+    scan_vals(v0, k0, cand_obj, cand_id, b + li, e);
+    if (b + kScanStep < e) scan_keys(k1, order, sorted_key, b + kScanStep + li, e);
+  }
+  for (int64_t c = b; c < e; c += kScanStep) {
+    const bool more = c + kScanStep < e;
+    ScanVals v1;
+    ScanKeys k2;
+    if (more) scan_vals(v1, k1, cand_obj, cand_id, c + kScanStep + li, e);
+    if (c + 2 * kScanStep < e) scan_keys(k2, order, sorted_key, c + 2 * kScanStep + li, e);
+    const int64_t i0 = c + li;
+
+    // Runs: an item starts one when its memory differs from the item before it (for lane 0's
+    // first item: from the run carried in); it ends one when the item after it differs.
+    const uint64_t before_key = __shfl_up(k0.key[kScanItems - 1], 1, 64);
+    const uint64_t after_key = __shfl_down(k0.key[0], 1, 64);
+    const uint64_t next_step_key = more ? __shfl(k1.key[0], 0, 64) : kNoKey;
+    bool st[kScanItems], en[kScanItems];
+    double o[kScanItems];
+    uint64_t id[kScanItems];
+#pragma unroll
+    for (int q = 0; q < kScanItems; ++q) {
+      const bool valid = i0 + q < e;
+      const uint64_t prev = q > 0 ? k0.key[q - 1] : (lane == 0 ? run_key : before_key);
+      const uint64_t next = q + 1 < kScanItems ? k0.key[q + 1] : (lane == 63 ? next_step_key : after_key);
+      st[q] = valid && k0.key[q] != prev;
+      en[q] = valid && k0.key[q] != next;
+      o[q] = v0.obj[q];
+      id[q] = v0.id[q];
     }
-    // First lane of this lane's run in the chunk (0 for the run carried in), then the run's
-    // (obj, id) minimum up to this lane.
-    int head = start ? lane : 0;
+    if (lane == 0 && i0 < e && !st[0] && lex_less(run_obj, run_id, o[0], id[0])) {
+      o[0] = run_obj;  // the carried run goes on
+      id[0] = run_id;
+    }
+    // Within the lane: each item's run minimum from the run's start (or from the lane's first
+    // item).
+    bool any_start = st[0];
+#pragma unroll
+    for (int q = 1; q < kScanItems; ++q) {
+      if (!st[q] && lex_less(o[q - 1], id[q - 1], o[q], id[q])) {
+        o[q] = o[q - 1];
+        id[q] = id[q - 1];
+      }
+      any_start = any_start || st[q];
+    }
+    // Across the lanes: segmented inclusive scan of (a run starts in the lane, the lane's last
+    // minimum), then the exclusive value from the lane before.
+    bool sf = any_start;
+    double so = o[kScanItems - 1];
+    uint64_t si = id[kScanItems - 1];
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
-      const int h = __shfl_up(head, off, 64);
-      if (lane >= off) head = max(head, h);
-    }
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const double vo = __shfl_up(o, off, 64);
-      const uint64_t vi = __shfl_up(id, off, 64);
-      if (lane - off >= head && lex_less(vo, vi, o, id)) {
-        o = vo;
-        id = vi;
+      const int pf = __shfl_up((int)sf, off, 64);
+      const double po = __shfl_up(so, off, 64);
+      const uint64_t pi = __shfl_up(si, off, 64);
+      if (lane >= off) {
+        if (!sf && lex_less(po, pi, so, si)) {
+          so = po;
+          si = pi;
+        }
+        sf = sf || pf != 0;
       }
     }
-    const bool end = valid && next != key;  // last candidate of its run: (o, id) is the run's minimum
-    double pm = end ? o : __builtin_huge_val();  // inclusive prefix minimum over the run ends
+    double in_o = __shfl_up(so, 1, 64);
+    uint64_t in_i = __shfl_up(si, 1, 64);
+    if (lane == 0) {
+      in_o = __builtin_huge_val();
+      in_i = kNoKey;
+    }
+    // Items before the lane's first start continue the run coming from the lanes before.
+    bool open = true;
+#pragma unroll
+    for (int q = 0; q < kScanItems; ++q) {
+      open = open && !st[q];
+      if (open && lex_less(in_o, in_i, o[q], id[q])) {
+        o[q] = in_o;
+        id[q] = in_i;
+      }
+    }
+    // Prefix minimum over the run ends: within the lane, then across the lanes and steps.
+    double lp[kScanItems];
+#pragma unroll
+    for (int q = 0; q < kScanItems; ++q) {
+      const double v = en[q] ? o[q] : __builtin_huge_val();
+      lp[q] = q > 0 ? __builtin_fmin(lp[q - 1], v) : v;
+    }
+    double pm = lp[kScanItems - 1];
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const double v = __shfl_up(pm, off, 64);
       if (lane >= off) pm = __builtin_fmin(pm, v);
     }
-    double before = __shfl_up(pm, 1, 64);
-    before = lane == 0 ? carry : __builtin_fmin(carry, before);
-    const bool on = end && o < before;
-    const unsigned long long m = __builtin_amdgcn_ballot_w64(on);
-    if (on) {
-      const unsigned int rank =
-          __builtin_amdgcn_mbcnt_hi((unsigned int)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)m, 0u));
-      front_key[w + rank] = key;
-      front_obj[w + rank] = o;
-      front_id[w + rank] = id;
+    double lane_before = __shfl_up(pm, 1, 64);
+    lane_before = lane == 0 ? carry : __builtin_fmin(carry, lane_before);
+    bool on[kScanItems];
+    unsigned int below = 0;  // frontier items of the lanes before this one
+    unsigned int total = 0;
+#pragma unroll
+    for (int q = 0; q < kScanItems; ++q) {
+      const double before = q > 0 ? __builtin_fmin(lane_before, lp[q - 1]) : lane_before;
+      on[q] = en[q] && o[q] < before;
+      const unsigned long long m = __builtin_amdgcn_ballot_w64(on[q]);
+      below += __builtin_amdgcn_mbcnt_hi((unsigned int)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)m, 0u));
+      total += (unsigned int)__builtin_popcountll(m);
     }
-    w += __builtin_popcountll(m);
+    int64_t slot = w + below;
+#pragma unroll
+    for (int q = 0; q < kScanItems; ++q) {
+      if (on[q]) {
+        front_key[slot] = k0.key[q];
+        front_obj[slot] = o[q];
+        front_id[slot] = id[q];
+        ++slot;
+      }
+    }
+    w += total;
     carry = __builtin_fmin(carry, __shfl(pm, 63, 64));
-    // The last lane's run goes on into the next chunk unless it ended here.
-    const bool open = __shfl((int)(valid && !end), 63, 64) != 0;
-    run_key = open ? __shfl(key, 63, 64) : kNoKey;
-    run_obj = __shfl(o, 63, 64);
-    run_id = __shfl(id, 63, 64);
+    // The step's last run goes on into the next step unless it ended here.
+    const bool last_open = __shfl((int)!en[kScanItems - 1], 63, 64) != 0;
+    run_key = last_open ? __shfl(k0.key[kScanItems - 1], 63, 64) : kNoKey;
+    run_obj = __shfl(o[kScanItems - 1], 63, 64);
+    run_id = __shfl(id[kScanItems - 1], 63, 64);
+    if (more) {
+      k0 = k1;
+      v0 = v1;
+      k1 = k2;
+    }
   }
   if (lane == 0) front_cnt[g] = w - b;
 }
