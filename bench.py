@@ -188,7 +188,7 @@ def main() -> int:
         exact = {"ms_per_run": runs[len(runs) // 2], "runs": len(runs),
                  "what": "exact time-vs-memory frontier of every group after the evaluation: candidate filter, "
                          "one candidate pass of the evaluation kernel (plus the tiles whose candidates overflowed their "
-                         "window), segmented sort by memory, scan; host "
+                         "window), exact pre-filter, segmented sort by memory, scan; host "
                          "wall time including its one synchronisation"}
 
     alpha = None

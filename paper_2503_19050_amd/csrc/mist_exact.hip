@@ -62,7 +62,7 @@ __device__ __forceinline__ void scan_vals(ScanVals& v, const ScanKeys& k, const 
   }
 }
 
-// One wave per group: candidates [seg[g], seg[g+1]) sorted by memory (keys in sorted_key, the
+// One wave per group: candidates [seg_begin[g], seg_end[g]) sorted by memory (keys in sorted_key, the
 // candidates' slots in order).  Per step: each run of equal memory is reduced to its (obj, id)
 // minimum by a segmented scan (within the lane over its items, then across the lanes, with the
 // run that crosses into the step carried in); a run's minimum is on the frontier when its
@@ -73,13 +73,14 @@ __global__ __launch_bounds__(256) void k_front_scan(const uint32_t* __restrict__
                                                     const uint64_t* __restrict__ sorted_key,
                                                     const double* __restrict__ cand_obj,
                                                     const uint64_t* __restrict__ cand_id,
-                                                    const int64_t* __restrict__ seg, int64_t n_groups,
+                                                    const int64_t* __restrict__ seg_begin,
+                                                    const int64_t* __restrict__ seg_end, int64_t n_groups,
                                                     uint64_t* __restrict__ front_key, double* __restrict__ front_obj,
                                                     uint64_t* __restrict__ front_id, int64_t* __restrict__ front_cnt) {
   const int lane = threadIdx.x & 63;
   const int64_t g = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (g >= n_groups) return;
-  const int64_t b = seg[g], e = seg[g + 1];
+  const int64_t b = seg_begin[g], e = seg_end[g];
   const int64_t li = (int64_t)lane * kScanItems;
   int64_t w = b;
   double carry = __builtin_huge_val();  // minimum objective of the completed runs before
@@ -220,6 +221,111 @@ __global__ __launch_bounds__(256) void k_front_scan(const uint32_t* __restrict__
   if (lane == 0) front_cnt[g] = w - b;
 }
 
+// Exact pre-filter, one block per group: a candidate with at least as large an objective as a
+// candidate of strictly smaller memory is not on the frontier.  The group's memory range is cut
+// into kSub sub-ranges by a monotone map, so every candidate of a lower sub-range has strictly
+// smaller memory; the candidates whose objective is not below the minimum of all lower
+// sub-ranges are dropped, and the others are moved to the front of the group's slots in
+// order.  seg_end[g] receives the end of the survivors.
+constexpr int kSub = 4096;
+
+__device__ __forceinline__ int sub_range(uint64_t key, double lo, double kap) {
+  const double m = __longlong_as_double((long long)key);
+  return min((int)((m - lo) * kap), kSub - 1);
+}
+
+__global__ __launch_bounds__(256) void k_prefilter(uint64_t* __restrict__ key, double* __restrict__ obj,
+                                                   uint64_t* __restrict__ id, const int64_t* __restrict__ seg,
+                                                   int64_t* __restrict__ seg_end) {
+  __shared__ unsigned long long s_min[kSub];
+  __shared__ double s_lo[4], s_hi[4], s_wmin[4];
+  __shared__ int s_cnt[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t g = blockIdx.x;
+  const int64_t b = seg[g], e = seg[g + 1];
+  if (b == e) {
+    if (tid == 0) seg_end[g] = e;
+    return;
+  }
+  // The group's memory range.
+  double lo = __builtin_huge_val(), hi = 0.0;
+  for (int64_t i = b + tid; i < e; i += 256) {
+    const double m = __longlong_as_double((long long)key[i]);
+    lo = __builtin_fmin(lo, m);
+    hi = __builtin_fmax(hi, m);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    lo = __builtin_fmin(lo, __shfl_xor(lo, off, 64));
+    hi = __builtin_fmax(hi, __shfl_xor(hi, off, 64));
+  }
+  if (lane == 0) {
+    s_lo[wave] = lo;
+    s_hi[wave] = hi;
+  }
+  for (int j = tid; j < kSub; j += 256) s_min[j] = kNoKey;
+  __syncthreads();
+  lo = __builtin_fmin(__builtin_fmin(s_lo[0], s_lo[1]), __builtin_fmin(s_lo[2], s_lo[3]));
+  hi = __builtin_fmax(__builtin_fmax(s_hi[0], s_hi[1]), __builtin_fmax(s_hi[2], s_hi[3]));
+  const double kap = hi > lo ? (double)kSub / (hi - lo) : 0.0;
+  // Minimum objective per sub-range (a non-negative double orders like its bits).
+  for (int64_t i = b + tid; i < e; i += 256)
+    atomicMin(&s_min[sub_range(key[i], lo, kap)], (unsigned long long)__double_as_longlong(obj[i]));
+  __syncthreads();
+  // Exclusive prefix minimum over the sub-ranges: thread t holds sub-ranges [16t, 16t + 16).
+  constexpr int kPer = kSub / 256;
+  double run = __builtin_huge_val();
+  double own[kPer];
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const unsigned long long v = s_min[tid * kPer + q];
+    own[q] = v == kNoKey ? __builtin_huge_val() : __longlong_as_double((long long)v);
+    run = __builtin_fmin(run, own[q]);
+  }
+  double incl = run;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const double v = __shfl_up(incl, off, 64);
+    if (lane >= off) incl = __builtin_fmin(incl, v);
+  }
+  if (lane == 63) s_wmin[wave] = incl;
+  __syncthreads();
+  double before = __shfl_up(incl, 1, 64);
+  if (lane == 0) before = __builtin_huge_val();
+  for (int w = 0; w < wave; ++w) before = __builtin_fmin(before, s_wmin[w]);
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    s_min[tid * kPer + q] = (unsigned long long)__double_as_longlong(before);
+    before = __builtin_fmin(before, own[q]);
+  }
+  __syncthreads();
+  // Keep the candidates below every lower sub-range's minimum, in order, at the front.  A
+  // chunk's writes land below its own start, after every thread of the block read the chunk.
+  int64_t wp = b;
+  for (int64_t c = b; c < e; c += 256) {
+    const int64_t i = c + tid;
+    const bool valid = i < e;
+    const uint64_t k = valid ? key[i] : 0ull;
+    const double o = valid ? obj[i] : 0.0;
+    const uint64_t d = valid ? id[i] : 0ull;
+    const bool keep = valid && o < __longlong_as_double((long long)s_min[sub_range(k, lo, kap)]);
+    const unsigned long long m = __builtin_amdgcn_ballot_w64(keep);
+    if (lane == 0) s_cnt[wave] = __builtin_popcountll(m);
+    __syncthreads();
+    int rank = __builtin_amdgcn_mbcnt_hi((unsigned int)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)m, 0u));
+    for (int w = 0; w < wave; ++w) rank += s_cnt[w];
+    const int total = s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
+    if (keep) {
+      key[wp + rank] = k;
+      obj[wp + rank] = o;
+      id[wp + rank] = d;
+    }
+    wp += total;
+    __syncthreads();
+  }
+  if (tid == 0) seg_end[g] = wp;
+}
+
 // One wave per tile: its window's candidates, in order, to the tile's place in group order.
 __global__ __launch_bounds__(256) void k_compact(const uint64_t* __restrict__ slab_key,
                                                  const double* __restrict__ slab_obj,
@@ -249,12 +355,13 @@ int last_error() {
 }  // namespace
 
 int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_in, uint32_t* idx_out, int64_t n,
-               int64_t n_groups, const int64_t* seg, void* temp, size_t* temp_bytes, void* stream) {
+               int64_t n_groups, const int64_t* seg_begin, const int64_t* seg_end, void* temp, size_t* temp_bytes,
+               void* stream) {
   hipStream_t st = (hipStream_t)stream;
   const unsigned int un = (unsigned int)n, ug = (unsigned int)n_groups;
   if (!temp) {  // storage query
     const hipError_t e = rocprim::segmented_radix_sort_pairs(nullptr, *temp_bytes, cand_key, key_out, idx_in,
-                                                             idx_out, un, ug, seg, seg + 1, 0, 64, st);
+                                                             idx_out, un, ug, seg_begin, seg_end, 0, 64, st);
     return e == hipSuccess ? 0 : (int)e;
   }
   if (n == 0) return 0;
@@ -262,7 +369,7 @@ int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_in, ui
   int rc = last_error();
   if (!rc) {
     const hipError_t e = rocprim::segmented_radix_sort_pairs(temp, *temp_bytes, cand_key, key_out, idx_in, idx_out,
-                                                             un, ug, seg, seg + 1, 0, 64, st);
+                                                             un, ug, seg_begin, seg_end, 0, 64, st);
     if (e != hipSuccess) rc = (int)e;
   }
   return rc;
@@ -277,12 +384,21 @@ int launch_compact(const uint64_t* slab_key, const double* slab_obj, const uint6
   return last_error();
 }
 
+int launch_prefilter(uint64_t* cand_key, double* cand_obj, uint64_t* cand_id, const int64_t* seg,
+                     int64_t n_groups, int64_t* seg_end, void* stream) {
+  if (n_groups <= 0) return 0;
+  hipLaunchKernelGGL(k_prefilter, dim3((unsigned)n_groups), dim3(256), 0, (hipStream_t)stream, cand_key, cand_obj,
+                     cand_id, seg, seg_end);
+  return last_error();
+}
+
 int launch_front_scan(const uint32_t* order, const uint64_t* sorted_key, const double* cand_obj,
-                      const uint64_t* cand_id, const int64_t* seg, int64_t n_groups, uint64_t* front_key,
-                      double* front_obj, uint64_t* front_id, int64_t* front_cnt, void* stream) {
+                      const uint64_t* cand_id, const int64_t* seg_begin, const int64_t* seg_end, int64_t n_groups,
+                      uint64_t* front_key, double* front_obj, uint64_t* front_id, int64_t* front_cnt, void* stream) {
   if (n_groups <= 0) return 0;
   hipLaunchKernelGGL(k_front_scan, dim3((unsigned)((n_groups + 3) / 4)), dim3(256), 0, (hipStream_t)stream, order,
-                     sorted_key, cand_obj, cand_id, seg, n_groups, front_key, front_obj, front_id, front_cnt);
+                     sorted_key, cand_obj, cand_id, seg_begin, seg_end, n_groups, front_key, front_obj, front_id,
+                     front_cnt);
   return last_error();
 }
 

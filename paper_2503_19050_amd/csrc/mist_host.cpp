@@ -119,6 +119,7 @@ struct mist_space {
   uint64_t *d_slab_key = nullptr, *d_slab_id = nullptr;
   double* d_slab_obj = nullptr;
   int64_t* d_seg = nullptr;
+  int64_t* d_seg_end = nullptr;  // end of each group's candidates after the pre-filter
   int64_t* d_front_cnt = nullptr;
   std::vector<int32_t> h_cnt;
   std::vector<int64_t> h_tile_off, h_seg;
@@ -809,13 +810,14 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       S->d_tile_end = (int64_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int64_t));
       S->d_list = (int32_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int32_t));
       S->d_seg = (int64_t*)dev_alloc(S, (ng + 1) * sizeof(int64_t));
+      S->d_seg_end = (int64_t*)dev_alloc(S, std::max<size_t>(ng, 1) * sizeof(int64_t));
       S->d_front_cnt = (int64_t*)dev_alloc(S, std::max<size_t>(ng, 1) * sizeof(int64_t));
       S->d_slab_begin = (int64_t*)dev_alloc(S, (nt + 1) * sizeof(int64_t));
       S->d_slab_key = (uint64_t*)dev_alloc(S, n_slab * 8);
       S->d_slab_obj = (double*)dev_alloc(S, n_slab * 8);
       S->d_slab_id = (uint64_t*)dev_alloc(S, n_slab * 8);
       void** bufs[] = {(void**)&S->d_filt,      (void**)&S->d_cnt_tile,   (void**)&S->d_tile_off,
-                       (void**)&S->d_tile_end,  (void**)&S->d_list,       (void**)&S->d_seg,
+                       (void**)&S->d_tile_end,  (void**)&S->d_list,       (void**)&S->d_seg, (void**)&S->d_seg_end,
                        (void**)&S->d_front_cnt, (void**)&S->d_slab_begin, (void**)&S->d_slab_key,
                        (void**)&S->d_slab_obj,  (void**)&S->d_slab_id};
       bool ok = true;
@@ -893,8 +895,8 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       }
     }
     size_t need = 0;
-    k = exact_sort(S->d_cand_key, S->d_key_sorted, S->d_idx_in, S->d_idx_out, off, (int64_t)ng, S->d_seg, nullptr,
-                   &need, st);
+    k = exact_sort(S->d_cand_key, S->d_key_sorted, S->d_idx_in, S->d_idx_out, off, (int64_t)ng, S->d_seg,
+                   S->d_seg_end, nullptr, &need, st);
     if (k) return fail_hip((hipError_t)k, "exact frontier: sort storage");
     if (need > S->sort_temp_bytes) {
       dev_free_one(S, S->d_sort_temp);
@@ -926,14 +928,15 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       k = launch_pairs(ea, st);
       if (!k) k = launch_eval(ea, mode_grid(S, kModeEmit), kModeEmit, st);
     }
+    if (!k) k = launch_prefilter(S->d_cand_key, S->d_cand_obj, S->d_cand_id, S->d_seg, (int64_t)ng, S->d_seg_end, st);
     if (!k) {
       size_t bytes = S->sort_temp_bytes;
       k = exact_sort(S->d_cand_key, S->d_key_sorted, S->d_idx_in, S->d_idx_out, off, (int64_t)ng, S->d_seg,
-                     S->d_sort_temp, &bytes, st);
+                     S->d_seg_end, S->d_sort_temp, &bytes, st);
     }
     if (!k)
-      k = launch_front_scan(S->d_idx_out, S->d_key_sorted, S->d_cand_obj, S->d_cand_id, S->d_seg, (int64_t)ng,
-                            S->d_front_key, S->d_front_obj, S->d_front_id, S->d_front_cnt, st);
+      k = launch_front_scan(S->d_idx_out, S->d_key_sorted, S->d_cand_obj, S->d_cand_id, S->d_seg, S->d_seg_end,
+                            (int64_t)ng, S->d_front_key, S->d_front_obj, S->d_front_id, S->d_front_cnt, st);
     if (k) return fail_hip((hipError_t)k, "exact frontier");
     S->n_cand = off;
     S->n_rerun = n_list;

@@ -157,18 +157,23 @@ int launch_reduce(const ReduceArgs& a, void* stream);
 int launch_eval_ids(const EvalArgs& a, const uint64_t* ids, int64_t n, double* out, void* stream);
 int launch_filter(const EvalArgs& a, const double* bucket_obj, const uint64_t* bucket_id, FiltEntry* filt,
                   void* stream);
-// Exact frontier, mist_exact.hip: the candidates of group g are [seg[g], seg[g+1]); one
-// segmented sort by memory leaves the sorted keys in key_out and the candidates' slots in
-// idx_out, and the per-group scan keeps the staircase.
+// Exact frontier, mist_exact.hip: the candidates of group g are [seg[g], seg[g+1]).  The
+// pre-filter drops, per group, candidates that one of strictly smaller memory dominates and
+// moves the rest to the front (their end in seg_end); one segmented sort by memory over
+// [seg[g], seg_end[g]) leaves the sorted keys in key_out and the candidates' slots in idx_out,
+// and the per-group scan keeps the staircase.
+int launch_prefilter(uint64_t* cand_key, double* cand_obj, uint64_t* cand_id, const int64_t* seg,
+                     int64_t n_groups, int64_t* seg_end, void* stream);
 int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_in, uint32_t* idx_out, int64_t n,
-               int64_t n_groups, const int64_t* seg, void* temp, size_t* temp_bytes, void* stream);
+               int64_t n_groups, const int64_t* seg_begin, const int64_t* seg_end, void* temp, size_t* temp_bytes,
+               void* stream);
 // Moves each tile's candidates from its window [slab_begin[t], slab_begin[t+1]) to
 // [tile_off[t], tile_off[t] + cnt[t]); tiles whose count exceeds the window are skipped.
 int launch_compact(const uint64_t* slab_key, const double* slab_obj, const uint64_t* slab_id,
                    const int64_t* slab_begin, const int32_t* cnt, const int64_t* tile_off, int32_t n_tiles,
                    uint64_t* cand_key, double* cand_obj, uint64_t* cand_id, void* stream);
 int launch_front_scan(const uint32_t* order, const uint64_t* sorted_key, const double* cand_obj,
-                      const uint64_t* cand_id, const int64_t* seg, int64_t n_groups, uint64_t* front_key,
-                      double* front_obj, uint64_t* front_id, int64_t* front_cnt, void* stream);
+                      const uint64_t* cand_id, const int64_t* seg_begin, const int64_t* seg_end, int64_t n_groups,
+                      uint64_t* front_key, double* front_obj, uint64_t* front_id, int64_t* front_cnt, void* stream);
 
 }  // namespace mist
