@@ -340,15 +340,18 @@ template <int R>
 constexpr int ia_block() { return R <= 6 ? R : (R + 2) / 3; }
 
 // Waves per SIMD the register allocation aims at: four, the most the LDS use of a block
-// allows (a few strip-level values spill; the occupancy is worth more).
-template <int R>
-constexpr int eval_waves() { return 4; }
+// allows (a few strip-level values spill; the occupancy is worth more).  The exact frontier's
+// candidate variant keeps more per configuration live; with a whole strip's activation ratios
+// in one block (R <= 6) three waves and fewer spills are faster (1.60 against 1.83 ms for the
+// exact frontier on gpt2.7b-d16), with larger R four.
+template <int R, int MODE>
+constexpr int eval_waves() { return MODE == kModeEmit && R <= 6 ? 3 : 4; }
 
 // MODE kModeBuckets: bucket minima; kModeAlpha: also the weight-sampled argmins of Eq. 4
 // (a.n_alpha samples); kModeEmit: the exact frontier's candidates, written and counted per
 // tile (the bucket reduction is skipped).
 template <int R, int MODE>
-__global__ __launch_bounds__(kBlock, eval_waves<R>()) void k_eval(EvalArgs a, const double* __restrict__ ratio,
+__global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalArgs a, const double* __restrict__ ratio,
                                                                  const PairK* __restrict__ pk) {
   constexpr bool AL = MODE == kModeAlpha;
   constexpr bool EX = MODE == kModeEmit;
