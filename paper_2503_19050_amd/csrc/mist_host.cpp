@@ -859,6 +859,8 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
     S->h_seg.assign(ng + 1, 0);
     S->h_list.clear();
     int64_t off = 0;
+    for (size_t t = 0; t < nt; ++t)
+      if (S->h_cnt[t] == INT32_MAX) return fail(MIST_E_RANGE, "exact frontier: 2^31 or more candidates in a tile");
     auto place = [&](int32_t t) {
       S->h_tile_off[t] = off;
       off += S->h_cnt[t];

@@ -630,7 +630,9 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
     }
     // The tile's partials: lane j = bucket j.
     if constexpr (EX) {
-      if (lane == 0) a.cnt_tile[t] = (int32_t)(n_cand - n_beg);
+      // Saturated at 2^31 - 1, which the host rejects (no tile of a space with fewer than
+      // 2^32 candidates reaches it).
+      if (lane == 0) a.cnt_tile[t] = (int32_t)min(n_cand - n_beg, (int64_t)0x7FFFFFFF);
     } else {
       wave_sync();
       const unsigned int bl = bucket[lane].lid;
