@@ -106,6 +106,7 @@ struct mist_space {
   int32_t cus = 0;
   // exact frontier (mist_eval_pareto_exact)
   bool exact_done = false;
+  bool exact_launched = false;  // some call enqueued uploads of the host offset tables
   hipStream_t exact_stream = nullptr;
   FiltEntry* d_filt = nullptr;
   int32_t* d_cnt_tile = nullptr;
@@ -787,6 +788,13 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
   try {
     hipStream_t st = (hipStream_t)hip_stream;
     const size_t nt = S->tiles.size(), ng = S->groups.size();
+    // The host offset tables below are uploaded asynchronously: a previous call on another
+    // stream must be done with them before they are rewritten.
+    if (S->exact_launched && S->exact_stream != st) {
+      const hipError_t e = hipStreamSynchronize(S->exact_stream);
+      if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+    }
+    S->exact_done = false;
     if (!S->d_filt) {
       // Windows: ceil(configurations / div) slots per tile.
       const int64_t R2 = (int64_t)S->R * S->R;
@@ -907,6 +915,8 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       if (!S->d_sort_temp) return fail(MIST_E_NOMEM, "device allocation failed: sort storage");
     }
     const int32_t n_list = (int32_t)S->h_list.size();
+    S->exact_launched = true;
+    S->exact_stream = st;
     e = copy_async(S->d_tile_off, S->h_tile_off.data(), nt * sizeof(int64_t), hipMemcpyHostToDevice, st);
     if (e == hipSuccess)
       e = copy_async(S->d_seg, S->h_seg.data(), (ng + 1) * sizeof(int64_t), hipMemcpyHostToDevice, st);
@@ -1232,6 +1242,8 @@ mist_status mist_launch_info(const mist_space* S, int64_t* n_tiles, int32_t* blo
 mist_status mist_space_destroy(mist_space* S) {
   if (!S) return MIST_OK;
   if (S->evaluated) (void)hipStreamSynchronize(S->stream);
+  // The exact frontier may run on another stream; its buffers and host tables go below.
+  if (S->exact_launched && S->exact_stream != S->stream) (void)hipStreamSynchronize(S->exact_stream);
   for (hipEvent_t e : S->events) (void)hipEventDestroy(e);
   dev_free_all(S);
   delete S;

@@ -111,3 +111,24 @@ def test_candidate_windows_do_not_change_results(name, torch_cuda):
                 assert [r["obj"] for r in got] == list(want[g]["obj"]), (window, g)
                 assert [r["mem"] for r in got] == list(want[g]["mem"]), (window, g)
         S.close()
+
+
+def test_exact_frontier_on_several_streams(torch_cuda):
+    """Calls on different streams, one after another, give the oracle's frontier; a space
+    destroyed right after a call on another stream waits for it."""
+    from paper_2503_19050_amd import mist
+    wl = W.workload("gpt1.3b-d8")
+    o = O.Oracle(wl)
+    S = mist.from_workload(wl)
+    S.eval()
+    streams = [torch_cuda.cuda.Stream(), torch_cuda.cuda.Stream()]
+    for st in streams + streams[::-1]:
+        S.eval_pareto_exact(stream=st)
+    for g in range(o.n_groups):
+        want = o.pareto_exact(g)
+        got = S.pareto_exact(g)
+        assert [r["id"] for r in got] == [int(i) for i in want["id"]], g
+        assert [r["obj"] for r in got] == list(want["obj"]), g
+    S.eval_pareto_exact(stream=streams[1])
+    S.close()
+    torch_cuda.cuda.synchronize()
