@@ -190,7 +190,9 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
 /* Enqueues the evaluation of every configuration (cost model, feasibility filter, per
  * bucket and per group reductions; Sec. 5.3, Eq. 4-6, Algorithm 1) on hip_stream
  * (a hipStream_t; NULL = the null stream) and returns without waiting.  Re-runnable; each
- * run overwrites the previous results.  Errors: MIST_E_INVALID, MIST_E_DEVICE. */
+ * run overwrites the previous results.  On a stream other than the one of the space's
+ * previous evaluation or exact frontier, it first waits on the host for the work queued
+ * there (the two share buffers).  Errors: MIST_E_INVALID, MIST_E_DEVICE. */
 mist_status mist_eval_space(mist_space* S, void* hip_stream);
 
 /* Waits for the last evaluation and writes, for groups g0..g0+n-1, the feasible

@@ -722,6 +722,16 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
 mist_status mist_eval_space(mist_space* S, void* hip_stream) {
   if (!S) return fail(MIST_E_INVALID, "space is null");
   hipStream_t st = (hipStream_t)hip_stream;
+  // Work of this space still queued on another stream uses the same buffers and tile
+  // counters: it finishes first.
+  if (S->evaluated && S->stream != st) {
+    const hipError_t e = hipStreamSynchronize(S->stream);
+    if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+  }
+  if (S->exact_launched && S->exact_stream != st) {
+    const hipError_t e = hipStreamSynchronize(S->exact_stream);
+    if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+  }
   const EvalArgs ea = eval_args(S);
   int rc = launch_pairs(ea, st);
   if (rc) return fail_hip((hipError_t)rc, "pair kernel launch");

@@ -132,3 +132,25 @@ def test_exact_frontier_on_several_streams(torch_cuda):
     S.eval_pareto_exact(stream=streams[1])
     S.close()
     torch_cuda.cuda.synchronize()
+
+
+def test_evaluations_and_exact_frontier_interleaved_on_streams(torch_cuda):
+    """Evaluations and exact frontiers alternating between two streams with no synchronisation
+    by the caller: the library orders them, and the results are the oracle's."""
+    from paper_2503_19050_amd import mist
+    wl = W.workload("gpt1.3b-d8")
+    o = O.Oracle(wl)
+    want_best = o.run()
+    S = mist.from_workload(wl)
+    s1, s2 = torch_cuda.cuda.Stream(), torch_cuda.cuda.Stream()
+    S.eval(stream=s1)
+    S.eval(stream=s2)
+    S.eval_pareto_exact(stream=s1)
+    S.eval(stream=s2)
+    S.eval_pareto_exact(stream=s2)
+    best = S.best(0, S.n_groups)
+    assert [b["id"] for b in best] == [int(i) for i in want_best["best_id"]]
+    for g in range(0, o.n_groups, 7):
+        want = o.pareto_exact(g)
+        assert [r["id"] for r in S.pareto_exact(g)] == [int(i) for i in want["id"]], g
+    S.close()
