@@ -496,12 +496,18 @@ mist_status eval_ids_impl(mist_space* S, const uint64_t* ids, int64_t n, double*
   TempBuf dids(S, (size_t)n * sizeof(uint64_t));
   TempBuf dout(S, (size_t)n * 4 * sizeof(double));
   if (!dids.p || !dout.p) return fail(MIST_E_NOMEM, "device allocation failed: eval_ids");
+  // The temporary buffers go back to the allocator when this returns: on every path the
+  // stream is drained first.
+  auto drained = [&](mist_status code) {
+    (void)hipStreamSynchronize(st);
+    return code;
+  };
   hipError_t e = copy_async(dids.p, ids, (size_t)n * sizeof(uint64_t), hipMemcpyHostToDevice, st);
-  if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync ids");
+  if (e != hipSuccess) return drained(fail_hip(e, "hipMemcpyAsync ids"));
   const int rc = launch_eval_ids(eval_args(S), (const uint64_t*)dids.p, n, (double*)dout.p, st);
-  if (rc) return fail_hip((hipError_t)rc, "eval_ids launch");
+  if (rc) return drained(fail_hip((hipError_t)rc, "eval_ids launch"));
   e = copy_async(out, dout.p, (size_t)n * 4 * sizeof(double), hipMemcpyDeviceToHost, st);
-  if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync out");
+  if (e != hipSuccess) return drained(fail_hip(e, "hipMemcpyAsync out"));
   e = hipStreamSynchronize(st);
   if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
   return MIST_OK;
