@@ -191,6 +191,7 @@ def main() -> int:
         # configurations per second of the whole pass, and its share of the FP64 peak counts
         # the definition's FLOPs per configuration over the whole pass (sort and scan included).
         exact = {"ms_per_run": ms, "runs": len(runs), "value": S.n_configs / (ms / 1e3), "unit": "configs/s",
+                 **S.exact_info(),
                  "flops_per_config": fpc,
                  "frac": None if fpc is None else fpc * S.n_configs / (ms / 1e3) / 1e12 / FP64_VECTOR_PEAK_TFLOPS,
                  "what": "exact time-vs-memory frontier of every group after the evaluation: candidate filter, "

@@ -976,6 +976,27 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
   }
 }
 
+mist_status mist_exact_info(mist_space* S, int64_t* n_candidates, int64_t* n_kept, int32_t* n_tiles_again) {
+  if (!S) return fail(MIST_E_INVALID, "space is null");
+  if (!S->exact_done) return fail(MIST_E_STATE, "mist_eval_pareto_exact has not been called");
+  hipError_t e = hipStreamSynchronize(S->exact_stream);
+  if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+  try {
+    const size_t ng = S->groups.size();
+    std::vector<int64_t> ends(ng);
+    e = copy_sync(ends.data(), S->d_seg_end, ng * sizeof(int64_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpy segment ends");
+    int64_t kept = 0;
+    for (size_t g = 0; g < ng; ++g) kept += ends[g] - S->h_seg[g];
+    if (n_candidates) *n_candidates = S->n_cand;
+    if (n_kept) *n_kept = kept;
+    if (n_tiles_again) *n_tiles_again = S->n_rerun;
+    return MIST_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(MIST_E_NOMEM, "host allocation failed");
+  }
+}
+
 mist_status mist_get_pareto_exact(mist_space* S, int64_t g, mist_result* out, int64_t cap, int64_t* n_out) {
   if (!S || !n_out || (!out && cap > 0)) return fail(MIST_E_INVALID, "null argument");
   if (!S->exact_done) return fail(MIST_E_STATE, "mist_eval_pareto_exact has not been called");

@@ -98,6 +98,7 @@ def test_candidate_windows_do_not_change_results(name, torch_cuda):
     groups = sorted({0, o.n_groups - 1} | set(int(g) for g in rng.choice(o.n_groups, size=min(12, o.n_groups),
                                                                            replace=False)))
     want = {g: o.pareto_exact(g) for g in groups}
+    sizes = {}
     for window in (1, 0, 64, 1 << 30):
         say(name, "cand_window", window)
         w = dict(wl, space=dict(wl["space"], cand_window=window))
@@ -105,12 +106,19 @@ def test_candidate_windows_do_not_change_results(name, torch_cuda):
         for _ in range(2):
             S.eval()
             S.eval_pareto_exact()
+            info = S.exact_info()
+            say("  ", info)
+            assert 0 <= info["kept"] <= info["candidates"]
+            if window == 1:
+                assert info["tiles_again"] == 0  # a window as large as its tile never overflows
+            sizes.setdefault((info["candidates"], info["kept"]), []).append(window)
             for g in groups:
                 got = S.pareto_exact(g)
                 assert [r["id"] for r in got] == [int(i) for i in want[g]["id"]], (window, g)
                 assert [r["obj"] for r in got] == list(want[g]["obj"]), (window, g)
                 assert [r["mem"] for r in got] == list(want[g]["mem"]), (window, g)
         S.close()
+    assert len(sizes) == 1, sizes  # the same candidates and survivors whatever the windows
 
 
 def test_exact_frontier_on_several_streams(torch_cuda):
