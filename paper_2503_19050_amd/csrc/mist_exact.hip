@@ -237,9 +237,11 @@ __device__ __forceinline__ int sub_range(uint64_t key, double lo, double kap) {
 __global__ __launch_bounds__(256) void k_prefilter(uint64_t* __restrict__ key, double* __restrict__ obj,
                                                    uint64_t* __restrict__ id, const int64_t* __restrict__ seg,
                                                    int64_t* __restrict__ seg_end) {
+  constexpr int kPf = 4;               // items per thread and step: four loads in flight
+  constexpr int kPfStep = 256 * kPf;
   __shared__ unsigned long long s_min[kSub];
   __shared__ double s_lo[4], s_hi[4], s_wmin[4];
-  __shared__ int s_cnt[4];
+  __shared__ int s_cnt[4][kPf];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t g = blockIdx.x;
   const int64_t b = seg[g], e = seg[g + 1];
@@ -249,10 +251,20 @@ __global__ __launch_bounds__(256) void k_prefilter(uint64_t* __restrict__ key, d
   }
   // The group's memory range.
   double lo = __builtin_huge_val(), hi = 0.0;
-  for (int64_t i = b + tid; i < e; i += 256) {
-    const double m = __longlong_as_double((long long)key[i]);
-    lo = __builtin_fmin(lo, m);
-    hi = __builtin_fmax(hi, m);
+  for (int64_t c = b; c < e; c += kPfStep) {
+    uint64_t k[kPf];
+#pragma unroll
+    for (int q = 0; q < kPf; ++q) {
+      const int64_t i = c + q * 256 + tid;
+      k[q] = i < e ? key[i] : kNoKey;
+    }
+#pragma unroll
+    for (int q = 0; q < kPf; ++q) {
+      if (k[q] == kNoKey) continue;
+      const double m = __longlong_as_double((long long)k[q]);
+      lo = __builtin_fmin(lo, m);
+      hi = __builtin_fmax(hi, m);
+    }
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -269,8 +281,18 @@ __global__ __launch_bounds__(256) void k_prefilter(uint64_t* __restrict__ key, d
   hi = __builtin_fmax(__builtin_fmax(s_hi[0], s_hi[1]), __builtin_fmax(s_hi[2], s_hi[3]));
   const double kap = hi > lo ? (double)kSub / (hi - lo) : 0.0;
   // Minimum objective per sub-range (a non-negative double orders like its bits).
-  for (int64_t i = b + tid; i < e; i += 256)
-    atomicMin(&s_min[sub_range(key[i], lo, kap)], (unsigned long long)__double_as_longlong(obj[i]));
+  for (int64_t c = b; c < e; c += kPfStep) {
+    uint64_t k[kPf], o[kPf];
+#pragma unroll
+    for (int q = 0; q < kPf; ++q) {
+      const int64_t i = c + q * 256 + tid;
+      k[q] = i < e ? key[i] : kNoKey;
+      o[q] = i < e ? (unsigned long long)__double_as_longlong(obj[i]) : 0ull;
+    }
+#pragma unroll
+    for (int q = 0; q < kPf; ++q)
+      if (k[q] != kNoKey) atomicMin(&s_min[sub_range(k[q], lo, kap)], o[q]);
+  }
   __syncthreads();
   // Exclusive prefix minimum over the sub-ranges: thread t holds sub-ranges [16t, 16t + 16).
   constexpr int kPer = kSub / 256;
@@ -300,25 +322,44 @@ __global__ __launch_bounds__(256) void k_prefilter(uint64_t* __restrict__ key, d
   }
   __syncthreads();
   // Keep the candidates below every lower sub-range's minimum, in order, at the front.  A
-  // chunk's writes land below its own start, after every thread of the block read the chunk.
+  // step's writes land below its own start, after every thread of the block read the step.
   int64_t wp = b;
-  for (int64_t c = b; c < e; c += 256) {
-    const int64_t i = c + tid;
-    const bool valid = i < e;
-    const uint64_t k = valid ? key[i] : 0ull;
-    const double o = valid ? obj[i] : 0.0;
-    const uint64_t d = valid ? id[i] : 0ull;
-    const bool keep = valid && o < __longlong_as_double((long long)s_min[sub_range(k, lo, kap)]);
-    const unsigned long long m = __builtin_amdgcn_ballot_w64(keep);
-    if (lane == 0) s_cnt[wave] = __builtin_popcountll(m);
+  for (int64_t c = b; c < e; c += kPfStep) {
+    uint64_t k[kPf], d[kPf];
+    double o[kPf];
+    bool keep[kPf];
+#pragma unroll
+    for (int q = 0; q < kPf; ++q) {
+      const int64_t i = c + q * 256 + tid;
+      const bool valid = i < e;
+      k[q] = valid ? key[i] : 0ull;
+      o[q] = valid ? obj[i] : 0.0;
+      d[q] = valid ? id[i] : 0ull;
+      keep[q] = valid && o[q] < __longlong_as_double((long long)s_min[sub_range(k[q], lo, kap)]);
+    }
+    unsigned long long m[kPf];
+#pragma unroll
+    for (int q = 0; q < kPf; ++q) {
+      m[q] = __builtin_amdgcn_ballot_w64(keep[q]);
+      if (lane == 0) s_cnt[wave][q] = __builtin_popcountll(m[q]);
+    }
     __syncthreads();
-    int rank = __builtin_amdgcn_mbcnt_hi((unsigned int)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)m, 0u));
-    for (int w = 0; w < wave; ++w) rank += s_cnt[w];
-    const int total = s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
-    if (keep) {
-      key[wp + rank] = k;
-      obj[wp + rank] = o;
-      id[wp + rank] = d;
+    // Item (q, tid) follows every item of the steps' earlier rows q' < q, then the earlier
+    // waves' items of row q, then the earlier lanes of its wave.
+    int base = 0, total = 0;
+#pragma unroll
+    for (int q = 0; q < kPf; ++q) {
+      const int row = s_cnt[0][q] + s_cnt[1][q] + s_cnt[2][q] + s_cnt[3][q];
+      if (keep[q]) {
+        int rank = base + __builtin_amdgcn_mbcnt_hi((unsigned int)(m[q] >> 32),
+                                                    __builtin_amdgcn_mbcnt_lo((unsigned int)m[q], 0u));
+        for (int w = 0; w < wave; ++w) rank += s_cnt[w][q];
+        key[wp + rank] = k[q];
+        obj[wp + rank] = o[q];
+        id[wp + rank] = d[q];
+      }
+      base += row;
+      total += row;
     }
     wp += total;
     __syncthreads();
