@@ -87,6 +87,7 @@ struct mist_space {
   int64_t tile_configs = 0;  // configurations per full-size tile, at least
   int32_t max_blocks = 0;    // cap on the evaluation grid (0: none)
   int32_t cand_window = 0;   // exact frontier: window divisor (0: automatic)
+  int32_t max_group_tiles = 0;  // tiles (full-size and small) of the largest group
   double* d_part_obj = nullptr;
   uint64_t* d_part_id = nullptr;
   double* d_bucket_obj = nullptr;
@@ -675,6 +676,7 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
     if (!rc) {
       const int64_t waves_needed = (int64_t)(S->tiles.size() + kWaves - 1) / kWaves;
       S->eval_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>(resident_blocks, waves_needed));
+      for (const DevGroup& G : S->groups) S->max_group_tiles = std::max(S->max_group_tiles, G.n_tiles + G.n_tail);
     }
     if (!rc) rc = upload(S, &S->d_groups, S->groups, "groups");
     if (!rc) rc = upload(S, &S->d_pairs, S->pairs, "pairs");
@@ -764,6 +766,7 @@ mist_status mist_eval_space(mist_space* S, void* hip_stream) {
   r.groups = S->d_groups;
   r.n_groups = (int64_t)S->groups.size();
   r.NB = S->NB;
+  r.max_group_tiles = S->max_group_tiles;
   r.part_obj = S->d_part_obj;
   r.part_id = S->d_part_id;
   r.bucket_obj = S->d_bucket_obj;

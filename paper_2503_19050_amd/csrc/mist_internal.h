@@ -10,7 +10,7 @@ namespace mist {
 constexpr int kBlock = 256;           // threads per evaluation block
 constexpr int kWaves = kBlock / 64;   // wave64
 constexpr int kWaveTile = 64;         // threads per tile: each wave works on its own tiles
-constexpr int kReduceBlock = 256;     // group-reduction block: one wave per group
+constexpr int kReduceBlock = 256;     // filter block: one wave per group
 constexpr int kTabStride = 8;         // interference table row: phi[4], psi[4]
 constexpr int kClaimCounters = 8;     // tile counters: one per XCD (blocks are dealt in turn)
 constexpr int kCounterStride = 64;    // ints between counters (separate cache lines)
@@ -135,6 +135,7 @@ struct ReduceArgs {
   const DevGroup* groups;
   int64_t n_groups;
   int32_t NB;
+  int32_t max_group_tiles;  // tiles of the largest group (chooses the reduction's layout)
   const double* part_obj;
   const uint64_t* part_id;
   double* bucket_obj;    // [n_groups][64]
