@@ -1,0 +1,49 @@
+"""bench.py without a GPU: the single-GPU contract (more than one GPU exits with a message),
+the per-configuration FLOP counts it reads, the traffic record that is used only while the
+kernel source matches the one the counters were taken on, and the CPU baseline's record."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+@pytest.mark.parametrize("argv, env", [(["--gpus", "2"], {}), (["--gpus", "8"], {}), ([], {"WORLD_SIZE": "2"})])
+def test_more_than_one_gpu_exits_with_a_message(argv, env):
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *argv], capture_output=True, text=True,
+                       env=dict(os.environ, **env), timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_flops_per_config_come_from_the_counting_oracle():
+    with open(bench.FLOPS_FILE) as f:
+        stored = json.load(f)["workloads"]
+    for name, w in stored.items():
+        fpc, fsh = bench.flops_per_config(name)
+        assert fpc == w["flops_per_config"] and fsh == w["flops_per_config_shared_levels"]
+        assert 0 < fsh < fpc
+    assert bench.flops_per_config("no such workload") == (None, None)
+
+
+def test_traffic_is_reported_only_for_the_kernel_it_was_measured_on(monkeypatch):
+    with open(bench.TRAFFIC_FILE) as f:
+        rec = json.load(f)["gpt2.7b-d16"]
+    monkeypatch.setattr(bench, "kernel_hash", lambda: rec["kernel_sha"])
+    assert bench.traffic_record("gpt2.7b-d16", 0) == rec["bytes_per_launch"]
+    monkeypatch.setattr(bench, "kernel_hash", lambda: "0" * 16)
+    assert bench.traffic_record("gpt2.7b-d16", 0) is None
+    assert bench.traffic_record("no such workload", 0) is None
+
+
+def test_cpu_baseline_record():
+    from paper_2503_19050_amd import workloads as W
+    rec = bench.cpu_baseline(W.workload("gpt1.3b-d8"), 0.5)
+    assert rec["kind"] == "oracle" and rec["cores"] == 1 and rec["unit"] == "configs/s"
+    assert rec["value"] > 0 and "gpt1.3b-d8" in rec["sample"]
