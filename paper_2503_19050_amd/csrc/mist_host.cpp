@@ -115,16 +115,22 @@ struct mist_space {
   int64_t* d_tile_end = nullptr;
   int32_t* d_list = nullptr;
   // Candidate windows: tile t writes to slots [slab_begin[t], slab_begin[t+1]) first.
-  std::vector<int64_t> h_slab_begin, h_tile_end;
-  std::vector<int32_t> h_list;
+  std::vector<int64_t> h_slab_begin;
   int64_t* d_slab_begin = nullptr;
   uint64_t *d_slab_key = nullptr, *d_slab_id = nullptr;
   double* d_slab_obj = nullptr;
   int64_t* d_seg = nullptr;
   int64_t* d_seg_end = nullptr;  // end of each group's candidates after the pre-filter
   int64_t* d_front_cnt = nullptr;
-  std::vector<int32_t> h_cnt;
-  std::vector<int64_t> h_tile_off, h_seg;
+  // Pinned host staging of the per-tile counts and the offset tables (copies to and from it
+  // run without a staging step); allocated by the first exact frontier, freed by destroy.
+  void* h_pinned = nullptr;
+  int32_t* h_cnt = nullptr;
+  int64_t* h_tile_off = nullptr;
+  int64_t* h_tile_end = nullptr;
+  int64_t* h_seg = nullptr;
+  int32_t* h_list = nullptr;
+  int32_t n_list = 0;
   int64_t cand_cap = 0, n_cand = 0;
   int32_t n_rerun = 0;  // tiles the last call evaluated a second time
   uint64_t *d_cand_key = nullptr, *d_cand_id = nullptr, *d_key_sorted = nullptr;
@@ -843,17 +849,33 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       S->d_slab_key = (uint64_t*)dev_alloc(S, n_slab * 8);
       S->d_slab_obj = (double*)dev_alloc(S, n_slab * 8);
       S->d_slab_id = (uint64_t*)dev_alloc(S, n_slab * 8);
+      {
+        const size_t bytes = 8 * (2 * nt + ng + 1) + 4 * (2 * nt) + 64;
+        void* p = nullptr;
+        if (hipHostMalloc(&p, bytes, hipHostMallocDefault) != hipSuccess) p = nullptr;
+        S->h_pinned = p;
+        if (p) {
+          char* q = (char*)p;
+          S->h_tile_off = (int64_t*)q;
+          S->h_tile_end = S->h_tile_off + nt;
+          S->h_seg = S->h_tile_end + nt;
+          S->h_cnt = (int32_t*)(S->h_seg + ng + 1);
+          S->h_list = S->h_cnt + nt;
+        }
+      }
       void** bufs[] = {(void**)&S->d_filt,      (void**)&S->d_cnt_tile,   (void**)&S->d_tile_off,
                        (void**)&S->d_tile_end,  (void**)&S->d_list,       (void**)&S->d_seg, (void**)&S->d_seg_end,
                        (void**)&S->d_front_cnt, (void**)&S->d_slab_begin, (void**)&S->d_slab_key,
                        (void**)&S->d_slab_obj,  (void**)&S->d_slab_id};
-      bool ok = true;
+      bool ok = S->h_pinned != nullptr;
       for (void** b : bufs) ok = ok && *b;
       if (!ok) {  // free what was allocated: the next call starts over
         for (void** b : bufs) {
           dev_free_one(S, *b);
           *b = nullptr;
         }
+        if (S->h_pinned) (void)hipHostFree(S->h_pinned);
+        S->h_pinned = nullptr;
         return fail(MIST_E_NOMEM, "device allocation failed: exact frontier");
       }
       const hipError_t e = copy_sync(S->d_slab_begin, S->h_slab_begin.data(), (nt + 1) * sizeof(int64_t),
@@ -875,16 +897,12 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
     if (!k) k = launch_pairs(ea, st);  // also resets the tile counters
     if (!k) k = launch_eval(ea, mode_grid(S, kModeEmit), kModeEmit, st);
     if (k) return fail_hip((hipError_t)k, "exact frontier: candidates");
-    S->h_cnt.resize(nt);
-    hipError_t e = copy_async(S->h_cnt.data(), S->d_cnt_tile, nt * sizeof(int32_t), hipMemcpyDeviceToHost, st);
+    hipError_t e = copy_async(S->h_cnt, S->d_cnt_tile, nt * sizeof(int32_t), hipMemcpyDeviceToHost, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     if (e != hipSuccess) return fail_hip(e, "exact frontier: counts");
     // Candidate slots in group order: a group's full-size tiles, then its small ones.  Tiles
     // whose candidates overflowed their window are listed for pass 2.
-    S->h_tile_off.assign(nt, 0);
-    S->h_tile_end.assign(nt, 0);
-    S->h_seg.assign(ng + 1, 0);
-    S->h_list.clear();
+    S->n_list = 0;
     int64_t off = 0;
     for (size_t t = 0; t < nt; ++t)
       if (S->h_cnt[t] == INT32_MAX) return fail(MIST_E_RANGE, "exact frontier: 2^31 or more candidates in a tile");
@@ -892,7 +910,7 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       S->h_tile_off[t] = off;
       off += S->h_cnt[t];
       S->h_tile_end[t] = off;
-      if (S->h_cnt[t] > S->h_slab_begin[t + 1] - S->h_slab_begin[t]) S->h_list.push_back(t);
+      if (S->h_cnt[t] > S->h_slab_begin[t + 1] - S->h_slab_begin[t]) S->h_list[S->n_list++] = t;
     };
     for (size_t g = 0; g < ng; ++g) {
       const DevGroup& G = S->groups[g];
@@ -933,16 +951,16 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       S->sort_temp_bytes = S->d_sort_temp ? need : 0;
       if (!S->d_sort_temp) return fail(MIST_E_NOMEM, "device allocation failed: sort storage");
     }
-    const int32_t n_list = (int32_t)S->h_list.size();
+    const int32_t n_list = S->n_list;
     S->exact_launched = true;
     S->exact_stream = st;
-    e = copy_async(S->d_tile_off, S->h_tile_off.data(), nt * sizeof(int64_t), hipMemcpyHostToDevice, st);
+    e = copy_async(S->d_tile_off, S->h_tile_off, nt * sizeof(int64_t), hipMemcpyHostToDevice, st);
     if (e == hipSuccess)
-      e = copy_async(S->d_seg, S->h_seg.data(), (ng + 1) * sizeof(int64_t), hipMemcpyHostToDevice, st);
+      e = copy_async(S->d_seg, S->h_seg, (ng + 1) * sizeof(int64_t), hipMemcpyHostToDevice, st);
     if (e == hipSuccess && n_list > 0)
-      e = copy_async(S->d_tile_end, S->h_tile_end.data(), nt * sizeof(int64_t), hipMemcpyHostToDevice, st);
+      e = copy_async(S->d_tile_end, S->h_tile_end, nt * sizeof(int64_t), hipMemcpyHostToDevice, st);
     if (e == hipSuccess && n_list > 0)
-      e = copy_async(S->d_list, S->h_list.data(), (size_t)n_list * sizeof(int32_t), hipMemcpyHostToDevice, st);
+      e = copy_async(S->d_list, S->h_list, (size_t)n_list * sizeof(int32_t), hipMemcpyHostToDevice, st);
     if (e != hipSuccess) return fail_hip(e, "exact frontier: offsets");
     // The windows that held their tile's candidates move to group order; pass 2 evaluates the
     // listed tiles again, writing straight to their slots.
@@ -1284,6 +1302,7 @@ mist_status mist_space_destroy(mist_space* S) {
   if (S->evaluated) (void)hipStreamSynchronize(S->stream);
   // The exact frontier may run on another stream; its buffers and host tables go below.
   if (S->exact_launched && S->exact_stream != S->stream) (void)hipStreamSynchronize(S->exact_stream);
+  if (S->h_pinned) (void)hipHostFree(S->h_pinned);
   for (hipEvent_t e : S->events) (void)hipEventDestroy(e);
   dev_free_all(S);
   delete S;
