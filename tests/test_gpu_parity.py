@@ -325,21 +325,27 @@ def test_allocator_failure_is_reported(torch_cuda):
         assert not live, "buffers left behind"
 
 
-@pytest.mark.parametrize("chunk", range(4))
+@pytest.mark.parametrize("chunk", range(8))
 def test_random_small_spaces(chunk, torch_cuda):
     """Seeded random small spaces (GPT and grouped-query Llama shapes, flash or not, device counts
     1-8 including 3 and 6, random microbatch subsets, 1-6 ratios from the eighths of [0, 1], 1-64
     buckets, both layer rules, one or two hardware samples with budgets from 1 MB to 10 GB,
-    0-3 weight samples): buckets, best, frontier bits, weight samples and exact frontiers of every
-    group, and sampled per-configuration values, against the oracle."""
+    0-3 weight samples), each with a random launch geometry (tile size, grid cap) and candidate
+    window: buckets, best, frontier bits, weight samples and exact frontiers of every group, and
+    sampled per-configuration values, against the oracle."""
     from paper_2503_19050_amd import mist
     n = 0
-    for seed in range(chunk * 15, chunk * 15 + 15):
+    for seed in range(chunk * 25, chunk * 25 + 25):
         wl = W.random_space(seed)
+        rng = np.random.default_rng(seed)
+        wl["space"]["cand_window"] = int(rng.choice([0, 1, 3, 64, 1 << 30]))
+        wl["space"]["tile_configs"] = int(rng.choice([0, 0, 64, 1000, 100000]))
+        wl["space"]["max_blocks"] = int(rng.choice([0, 0, 1, 7, 37]))
         o = O.Oracle(wl)
         if o.n_configs > 1_500_000:
             continue
-        say("random space", seed, o.n_configs, "configs", o.n_groups, "groups")
+        say("random space", seed, o.n_configs, "configs", o.n_groups, "groups", "window", wl["space"]["cand_window"],
+            "tile", wl["space"]["tile_configs"], "grid cap", wl["space"]["max_blocks"])
         S = mist.from_workload(wl)
         S.eval()
         S.eval_pareto_exact()
@@ -365,4 +371,4 @@ def test_random_small_spaces(chunk, torch_cuda):
         _compare_ids(S, o, _sample_ids(o, np.random.default_rng(seed), 300))
         S.close()
         n += 1
-    assert n >= 10
+    assert n >= 15
