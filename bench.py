@@ -187,15 +187,13 @@ def main() -> int:
             runs.append((time.perf_counter() - t0) * 1e3)
         runs.sort()
         ms = runs[len(runs) // 2]
-        # Every configuration is evaluated once more (the candidate test), so the row's rate is
-        # configurations per second of the whole pass, and its share of the FP64 peak counts
-        # the definition's FLOPs per configuration over the whole pass (sort and scan included).
+        # The row's rate: configurations of the space per second of the whole pass.  Tiles that
+        # cannot hold a candidate are skipped, so it is not an evaluation rate and no FP64 peak
+        # fraction is derived from it.
         exact = {"ms_per_run": ms, "runs": len(runs), "value": S.n_configs / (ms / 1e3), "unit": "configs/s",
                  **S.exact_info(),
-                 "flops_per_config": fpc,
-                 "frac": None if fpc is None else fpc * S.n_configs / (ms / 1e3) / 1e12 / FP64_VECTOR_PEAK_TFLOPS,
                  "what": "exact time-vs-memory frontier of every group after the evaluation: candidate filter, "
-                         "one candidate pass of the evaluation kernel (plus the tiles whose candidates overflowed their "
+                         "live tiles, one candidate pass of the evaluation kernel over them (plus the tiles whose candidates overflowed their "
                          "window), exact pre-filter, segmented sort by memory, scan; host "
                          "wall time including its one synchronisation"}
 

@@ -114,6 +114,7 @@ struct mist_space {
   int64_t* d_tile_off = nullptr;
   int64_t* d_tile_end = nullptr;
   int32_t* d_list = nullptr;
+  uint8_t* d_live = nullptr;  // per tile: may hold a candidate
   // Candidate windows: tile t writes to slots [slab_begin[t], slab_begin[t+1]) first.
   std::vector<int64_t> h_slab_begin;
   int64_t* d_slab_begin = nullptr;
@@ -842,6 +843,7 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       S->d_tile_off = (int64_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int64_t));
       S->d_tile_end = (int64_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int64_t));
       S->d_list = (int32_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int32_t));
+      S->d_live = (uint8_t*)dev_alloc(S, std::max<size_t>(nt, 1));
       S->d_seg = (int64_t*)dev_alloc(S, (ng + 1) * sizeof(int64_t));
       S->d_seg_end = (int64_t*)dev_alloc(S, std::max<size_t>(ng, 1) * sizeof(int64_t));
       S->d_front_cnt = (int64_t*)dev_alloc(S, std::max<size_t>(ng, 1) * sizeof(int64_t));
@@ -864,7 +866,7 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
         }
       }
       void** bufs[] = {(void**)&S->d_filt,      (void**)&S->d_cnt_tile,   (void**)&S->d_tile_off,
-                       (void**)&S->d_tile_end,  (void**)&S->d_list,       (void**)&S->d_seg, (void**)&S->d_seg_end,
+                       (void**)&S->d_tile_end,  (void**)&S->d_list,       (void**)&S->d_seg, (void**)&S->d_seg_end, (void**)&S->d_live,
                        (void**)&S->d_front_cnt, (void**)&S->d_slab_begin, (void**)&S->d_slab_key,
                        (void**)&S->d_slab_obj,  (void**)&S->d_slab_id};
       bool ok = S->h_pinned != nullptr;
@@ -890,10 +892,12 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
     ea.win_end = S->d_slab_begin + 1;
     ea.tile_list = nullptr;
     ea.n_list = 0;
+    ea.tile_live = S->d_live;
     ea.cand_key = S->d_slab_key;
     ea.cand_obj = S->d_slab_obj;
     ea.cand_id = S->d_slab_id;
     int k = launch_filter(ea, S->d_bucket_obj, S->d_bucket_id, S->d_filt, st);
+    if (!k) k = launch_live(ea, S->d_filt, S->d_live, st);
     if (!k) k = launch_pairs(ea, st);  // also resets the tile counters
     if (!k) k = launch_eval(ea, mode_grid(S, kModeEmit), kModeEmit, st);
     if (k) return fail_hip((hipError_t)k, "exact frontier: candidates");

@@ -126,6 +126,7 @@ struct EvalArgs {
   const int64_t* win_end;    // [n_tiles]
   const int32_t* tile_list;  // nullptr: every tile
   int32_t n_list;
+  const uint8_t* tile_live;  // nullptr, or 0 for a tile that holds no candidate (skipped)
   uint64_t* cand_key;        // memory bit patterns (a non-negative double orders like its bits)
   double* cand_obj;
   uint64_t* cand_id;
@@ -156,6 +157,8 @@ int launch_eval(const EvalArgs& a, int blocks, int mode, void* stream);
 int eval_blocks_per_cu(int R, int mode);
 int launch_reduce(const ReduceArgs& a, void* stream);
 int launch_eval_ids(const EvalArgs& a, const uint64_t* ids, int64_t n, double* out, void* stream);
+// Tiles that may hold a candidate of the exact frontier, from the last evaluation's partials.
+int launch_live(const EvalArgs& a, const FiltEntry* filt, uint8_t* live, void* stream);
 int launch_filter(const EvalArgs& a, const double* bucket_obj, const uint64_t* bucket_id, FiltEntry* filt,
                   void* stream);
 // Exact frontier, mist_exact.hip: the candidates of group g are [seg[g], seg[g+1]).  The

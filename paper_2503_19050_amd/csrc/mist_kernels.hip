@@ -392,6 +392,8 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
   for (int x = (int)blockIdx.x * kWaves + wave; x < n_items;) {
     const int t = listed ? a.tile_list[x] : x;
     const DevTile tile = a.tiles[t];
+    // The exact frontier's pass skips a tile that holds no candidate (its count stays 0).
+    const int strip_end = EX && a.tile_live && !a.tile_live[t] ? tile.strip_begin : tile.strip_end;
     const DevGroup g = a.groups[tile.group];
     const DevHw& hw = a.hws[g.hw];
     if (g.hw != loaded_hw) {  // the wave's LDS copy of the hardware tables
@@ -434,7 +436,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
     const int64_t ke = g.k < g.G ? g.k : g.G;
 
 #pragma unroll 1
-    for (int s = tile.strip_begin + lane; s < tile.strip_end; s += 64) {
+    for (int s = tile.strip_begin + lane; s < strip_end; s += 64) {
       const int unit = s / SU;
       const int rem = s - unit * SU;
       const int z = rem / R2;
@@ -851,6 +853,21 @@ __global__ __launch_bounds__(256) void k_eval_ids(EvalArgs a, const uint64_t* __
   out[4 * i + 3] = v.obj;
 }
 
+// Live tiles of the exact frontier: one wave per tile, lane j = bucket j.  A candidate needs an
+// objective below every lower bucket's minimum (pm); the tile's partial for bucket j is the
+// minimum objective of its configurations in that bucket, so a tile none of whose partials is
+// below its pm holds no candidate.
+__global__ __launch_bounds__(kReduceBlock) void k_live(EvalArgs a, const FiltEntry* __restrict__ filt,
+                                                      uint8_t* __restrict__ live) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * (kReduceBlock / 64) + (threadIdx.x >> 6);
+  if (t >= a.n_tiles) return;
+  const int64_t g = a.tiles[t].group;
+  const bool may = lane < a.NB && a.part_obj[t * 64 + lane] < filt[g * 64 + lane].pm;
+  const unsigned long long m = __builtin_amdgcn_ballot_w64(may);
+  if (lane == 0) live[t] = m != 0ull ? 1 : 0;
+}
+
 // Candidate filter of the exact frontier: one wave per group, lane j = bucket j.
 __global__ __launch_bounds__(kReduceBlock) void k_filter(EvalArgs a, const double* __restrict__ bucket_obj,
                                                          const uint64_t* __restrict__ bucket_id,
@@ -958,6 +975,14 @@ int launch_reduce(const ReduceArgs& a, void* stream) {
     hipLaunchKernelGGL(k_reduce<4>, dim3((unsigned)a.n_groups), dim3(256), 0, (hipStream_t)stream, a);
   else
     hipLaunchKernelGGL(k_reduce<1>, dim3((unsigned)((a.n_groups + 3) / 4)), dim3(256), 0, (hipStream_t)stream, a);
+  return check_launch();
+}
+
+int launch_live(const EvalArgs& a, const FiltEntry* filt, uint8_t* live, void* stream) {
+  if (a.n_tiles <= 0) return 0;
+  const int per = kReduceBlock / 64;
+  const int64_t blocks = ((int64_t)a.n_tiles + per - 1) / per;
+  hipLaunchKernelGGL(k_live, dim3((unsigned)blocks), dim3(kReduceBlock), 0, (hipStream_t)stream, a, filt, live);
   return check_launch();
 }
 
