@@ -251,10 +251,12 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream);
 mist_status mist_get_pareto_exact(mist_space* S, int64_t g, mist_result* out, int64_t cap, int64_t* n_out);
 
 /* Sizes of the last exact frontier, for diagnostics and measurement: the candidates of the
- * candidate pass (all groups), those the pre-filter kept, and the tiles evaluated a second
- * time because their candidates overflowed their window.  Waits for mist_eval_pareto_exact;
- * any pointer may be NULL.  Errors: MIST_E_INVALID, MIST_E_STATE, MIST_E_DEVICE. */
-mist_status mist_exact_info(mist_space* S, int64_t* n_candidates, int64_t* n_kept, int32_t* n_tiles_again);
+ * candidate pass (all groups), those the pre-filter kept, the tiles the candidate pass
+ * evaluated (those that may hold a candidate) and the tiles evaluated a second time because
+ * their candidates overflowed their window.  Waits for mist_eval_pareto_exact; any pointer may
+ * be NULL.  Errors: MIST_E_INVALID, MIST_E_STATE, MIST_E_DEVICE, MIST_E_NOMEM. */
+mist_status mist_exact_info(mist_space* S, int64_t* n_candidates, int64_t* n_kept, int32_t* n_tiles_live,
+                            int32_t* n_tiles_again);
 
 /* Raw per-bucket table of groups g0..g0+n-1: host ids[n*NB] and objs[n*NB] (MIST_NONE /
  * +inf for empty buckets) and host frontier masks[n] (bit j = bucket j on the staircase);

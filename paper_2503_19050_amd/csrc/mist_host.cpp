@@ -1001,7 +1001,8 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
   }
 }
 
-mist_status mist_exact_info(mist_space* S, int64_t* n_candidates, int64_t* n_kept, int32_t* n_tiles_again) {
+mist_status mist_exact_info(mist_space* S, int64_t* n_candidates, int64_t* n_kept, int32_t* n_tiles_live,
+                            int32_t* n_tiles_again) {
   if (!S) return fail(MIST_E_INVALID, "space is null");
   if (!S->exact_done) return fail(MIST_E_STATE, "mist_eval_pareto_exact has not been called");
   hipError_t e = hipStreamSynchronize(S->exact_stream);
@@ -1013,8 +1014,15 @@ mist_status mist_exact_info(mist_space* S, int64_t* n_candidates, int64_t* n_kep
     if (e != hipSuccess) return fail_hip(e, "hipMemcpy segment ends");
     int64_t kept = 0;
     for (size_t g = 0; g < ng; ++g) kept += ends[g] - S->h_seg[g];
+    const size_t nt = S->tiles.size();
+    std::vector<uint8_t> live(nt);
+    e = copy_sync(live.data(), S->d_live, nt, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpy live tiles");
+    int32_t n_live = 0;
+    for (uint8_t v : live) n_live += v ? 1 : 0;
     if (n_candidates) *n_candidates = S->n_cand;
     if (n_kept) *n_kept = kept;
+    if (n_tiles_live) *n_tiles_live = n_live;
     if (n_tiles_again) *n_tiles_again = S->n_rerun;
     return MIST_OK;
   } catch (const std::bad_alloc&) {

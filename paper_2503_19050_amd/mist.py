@@ -156,7 +156,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         L.mist_space_destroy.argtypes = [vp]
         L.mist_eval_pareto_exact.argtypes = [vp, vp]
         L.mist_get_pareto_exact.argtypes = [vp, ctypes.c_int64, P(Result), ctypes.c_int64, P(ctypes.c_int64)]
-        L.mist_exact_info.argtypes = [vp, P(ctypes.c_int64), P(ctypes.c_int64), P(ctypes.c_int32)]
+        L.mist_exact_info.argtypes = [vp, P(ctypes.c_int64), P(ctypes.c_int64), P(ctypes.c_int32), P(ctypes.c_int32)]
         L.mist_plan_points.argtypes = [P(StagePoint), ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P(Plan)]
         L.mist_plan_pipeline.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, P(Plan)]
         dp = P(ctypes.c_double)
@@ -325,11 +325,12 @@ class Space:
             return [_struct_to_dict(out[i]) for i in range(n.value)]
 
     def exact_info(self) -> dict:
-        """Sizes of the last exact frontier: candidates, those the pre-filter kept, and tiles
-        evaluated a second time."""
-        c, k, t = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int32()
-        _check(self.L, self.L.mist_exact_info(self.h, ctypes.byref(c), ctypes.byref(k), ctypes.byref(t)))
-        return {"candidates": c.value, "kept": k.value, "tiles_again": t.value}
+        """Sizes of the last exact frontier: candidates, those the pre-filter kept, tiles the
+        candidate pass evaluated, and tiles evaluated a second time."""
+        c, k, v, t = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
+        _check(self.L, self.L.mist_exact_info(self.h, ctypes.byref(c), ctypes.byref(k), ctypes.byref(v),
+                                              ctypes.byref(t)))
+        return {"candidates": c.value, "kept": k.value, "tiles_live": v.value, "tiles_again": t.value}
 
     def plan(self, hw: int = 0, pp: int = 0) -> dict | None:
         """The inter-stage plan (Eq. 1-3) of hardware sample hw from this space's frontier

@@ -97,7 +97,7 @@ def test_null_arguments():
     assert L.mist_space_create(None, None, 0, None, None, None) == -1
     assert L.mist_eval_space(None, None) == -1
     assert L.mist_space_destroy(None) == 0
-    assert L.mist_exact_info(None, None, None, None) == -1
+    assert L.mist_exact_info(None, None, None, None, None) == -1
     assert L.mist_last_error() is not None
 
 

@@ -109,6 +109,7 @@ def test_candidate_windows_do_not_change_results(name, torch_cuda):
             info = S.exact_info()
             say("  ", info)
             assert 0 <= info["kept"] <= info["candidates"]
+            assert 0 <= info["tiles_again"] <= info["tiles_live"]
             if window == 1:
                 assert info["tiles_again"] == 0  # a window as large as its tile never overflows
             sizes.setdefault((info["candidates"], info["kept"]), []).append(window)
