@@ -44,7 +44,8 @@ def test_exact_frontier(name, torch_cuda):
         groups = range(o.n_groups)
     else:
         rng = np.random.default_rng(4)
-        groups = sorted({0, o.n_groups - 1} | set(int(g) for g in rng.choice(o.n_groups, size=6, replace=False)))
+        size = 100 if name == "llama7b-d32" else 6
+        groups = sorted({0, o.n_groups - 1} | set(int(g) for g in rng.choice(o.n_groups, size=size, replace=False)))
     best = S.best(0, S.n_groups)
     total = 0
     for g in groups:
