@@ -177,12 +177,15 @@ typedef struct mist_group_key {
   uint64_t size;  /* configurations in the group */
 } mist_group_key;
 
-/* Validates and copies the descriptors (the caller may free them afterwards), enumerates
- * the groups, builds the tables and uploads them to the current HIP device.  hw points to
- * n_hw >= 1 samples.  alloc may be NULL (hipMalloc/hipFree).  On success *out owns every
+/* The problem statement of Sec. 5.3: a model (m), hardware samples (hw) and a search space (s)
+ * of the per-stage tuples of Table 2.  Validates and copies the descriptors (the caller may
+ * free them afterwards), enumerates the groups (every candidate stage, the IntraStagePareto
+ * queries of Eq. 3), builds the tables and uploads them to the current HIP device.  hw points
+ * to n_hw >= 1 samples.  alloc may be NULL (hipMalloc/hipFree).  On success *out owns every
  * device and host buffer.  A space may hold no configuration (when no microbatch size and
  * parallel split fits the global batch): it has no group, and every later call succeeds with
- * empty results.  Errors: MIST_E_INVALID, MIST_E_NOMEM, MIST_E_DEVICE. */
+ * empty results.  Errors: MIST_E_INVALID (a descriptor), MIST_E_RANGE (a group of 2^32 - 1 or
+ * more configurations: local ids are 32-bit), MIST_E_NOMEM, MIST_E_DEVICE. */
 mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n_hw,
                               const mist_space_desc* s, const mist_allocator* alloc,
                               mist_space** out);
@@ -195,15 +198,18 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
  * there (the two share buffers).  Errors: MIST_E_INVALID, MIST_E_DEVICE. */
 mist_status mist_eval_space(mist_space* S, void* hip_stream);
 
-/* Waits for the last evaluation and writes, for groups g0..g0+n-1, the feasible
- * configuration of minimum obj (lowest id among equal obj) into host out[0..n-1]; a group
- * without a feasible configuration gets id MIST_NONE, obj +inf, bucket -1.
+/* The intra-stage optimum of Eq. 4 (objective G*t + d, subject to the memory budget) per
+ * candidate stage: waits for the last evaluation and writes, for groups g0..g0+n-1, the
+ * feasible configuration of minimum obj (lowest id among equal obj) into host out[0..n-1]; a
+ * group without a feasible configuration gets id MIST_NONE, obj +inf, bucket -1.
  * Errors: MIST_E_STATE (no evaluation yet), MIST_E_RANGE, MIST_E_DEVICE. */
 mist_status mist_get_best(mist_space* S, int64_t g0, int64_t n, mist_result* out);
 
-/* Waits for the last evaluation and writes the time-vs-memory staircase of group g into
- * host out[0..*n_out-1] in increasing bucket order: bucket j is on it when it holds a
- * feasible configuration whose obj is strictly below that of every lower bucket.  If cap
+/* The time-vs-memory Pareto staircase that the inter-stage partitioner consumes (Eq. 3: each
+ * stage's frontier over its memory use; here over 64 memory-budget buckets): waits for the
+ * last evaluation and writes the staircase of group g into host out[0..*n_out-1] in
+ * increasing bucket order: bucket j is on it when it holds a feasible configuration whose obj
+ * is strictly below that of every lower bucket.  If cap
  * is too small returns MIST_E_RANGE with *n_out set to the required count. */
 mist_status mist_get_pareto(mist_space* S, int64_t g, mist_result* out, int32_t cap,
                             int32_t* n_out);

@@ -279,7 +279,11 @@ bool counts_exact(const mist_model_desc& m, int64_t PP, int64_t l, int64_t b, in
   return true;
 }
 
-std::string enumerate(mist_space* S) {
+// Enumerates the space.  On failure returns the message and sets *code: MIST_E_RANGE for a
+// space beyond the sizes the kernels index (a group's local ids are 32-bit, and 0xFFFFFFFF
+// marks an empty bucket), MIST_E_INVALID otherwise.
+std::string enumerate(mist_space* S, mist_status* code) {
+  *code = MIST_E_INVALID;
   const mist_model_desc& m = S->model;
   const int64_t L = m.n_layers;
   const int64_t R = S->R;
@@ -349,9 +353,24 @@ std::string enumerate(mist_space* S) {
             g.pair_begin = pair_begin;
             g.n_pairs = (int32_t)ps.size();
             const uint64_t units = (uint64_t)ps.size() * (uint64_t)(l + 1);
-            if (units > (uint64_t)INT32_MAX / 2) return "group too large";
-            const uint64_t size = units * per_unit;
-            if (base > UINT64_MAX - size) return "space too large";
+            // Local ids are 32-bit and 0xFFFFFFFF marks an empty bucket: a group holds fewer
+            // than 2^32 - 1 configurations.
+            const bool big = units > ((uint64_t)UINT32_MAX - 1) / per_unit;
+            const uint64_t size = big ? 0 : units * per_unit;
+            if (big || size >= (uint64_t)UINT32_MAX) {
+              *code = MIST_E_RANGE;
+              char msg[200];
+              std::snprintf(msg, sizeof msg,
+                            "group too large: %llu (pair, recomputed layers) units x %llu configurations "
+                            "(PP %lld, G %lld, l %lld); a group holds at most 2^32 - 2 configurations",
+                            (unsigned long long)units, (unsigned long long)per_unit, (long long)PP,
+                            (long long)G, (long long)l);
+              return msg;
+            }
+            if (base > UINT64_MAX - size) {
+              *code = MIST_E_RANGE;
+              return "space too large: 2^64 or more configurations";
+            }
             base += size;
             S->groups.push_back(g);
           }
@@ -375,7 +394,10 @@ std::string enumerate(mist_space* S) {
   const uint64_t per_unit_strips = 4ull * (uint64_t)(R * R);
   for (const DevGroup& g : S->groups) {
     const uint64_t st = (uint64_t)g.n_pairs * (uint64_t)(g.l + 1) * per_unit_strips;
-    if (st > (uint64_t)INT32_MAX) return "group too large";
+    if (st > (uint64_t)INT32_MAX) {  // strip indices are int32 (reached only with one ratio)
+      *code = MIST_E_RANGE;
+      return "group too large: 2^31 or more strips";
+    }
   }
 
   // Per-hardware tables (host divisions, each correctly rounded).
@@ -658,10 +680,11 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
       S->alloc = *alloc;
       S->custom_alloc = true;
     }
-    const std::string err = enumerate(S);
+    mist_status ecode = MIST_E_INVALID;
+    const std::string err = enumerate(S, &ecode);
     if (!err.empty()) {
       delete S;
-      return fail(MIST_E_INVALID, err);
+      return fail(ecode, err);
     }
     mist_status rc = MIST_OK;
     // Persistent evaluation grid: as many blocks as fit on the device at once.

@@ -92,6 +92,16 @@ def test_counts_beyond_exact_range_rejected():
     assert rc == -1 and "2^53" in msg
 
 
+def test_group_beyond_32bit_local_ids_rejected():
+    """Local ids within a group are 32-bit (0xFFFFFFFF marks an empty bucket): a group of 2^32 - 1
+    or more configurations is refused with MIST_E_RANGE before the device is touched.  Here PP = 1
+    and l = L = 20,000 layers give 20,001 x (pairs) units of 4 * 16^4 configurations each."""
+    ratios = [j / 15 for j in range(16)]
+    rc, msg = _create(W.workload("tiny"), m__n_layers=20000, s__ratios=ratios, s__n_devices=1,
+                      s__global_batch=16)
+    assert rc == -5 and "group too large" in msg and "2^32 - 2" in msg
+
+
 def test_null_arguments():
     L = mist.load()
     assert L.mist_space_create(None, None, 0, None, None, None) == -1
