@@ -681,6 +681,22 @@ double orc_interference(const double* X4, const double* phi64) {
   return interference<double>(X, phi, psi);
 }
 
+// FP64 operations of Algorithm 1 alone on one stream vector (the counting build of the
+// same template), for the tests that pin the counter by hand.
+int orc_count_interference(const double* X4, const double* phi64, uint64_t* flops) {
+  double phi[16][4];
+  double psi[64];
+  for (int i = 0; i < 64; ++i) {
+    phi[i / 4][i % 4] = phi64[i];
+    psi[i] = 1.0 / phi64[i];
+  }
+  const Counted X[4] = {Counted(X4[0]), Counted(X4[1]), Counted(X4[2]), Counted(X4[3])};
+  g_flops = 0;
+  (void)interference<Counted>(X, phi, psi);
+  *flops = g_flops;
+  return 0;
+}
+
 // Every configuration of groups [g0, g1): out[5*i..] = t, d, mem, obj, bucket
 // (bucket -1 = infeasible), in id order starting at groups[g0].base.
 int orc_dump(const Model* m, const Hw* hw, int32_t n_hw, const Space* s,

@@ -68,6 +68,7 @@ def lib() -> ctypes.CDLL:
             L.orc_pareto_exact.argtypes = args + [ctypes.c_int64, P(ctypes.c_uint64), P(ctypes.c_double),
                                                   P(ctypes.c_double), ctypes.c_int64, P(ctypes.c_int64)]
             L.orc_count_flops_ids.argtypes = args + [P(ctypes.c_uint64), ctypes.c_int64, P(ctypes.c_uint64)]
+            L.orc_count_interference.argtypes = [P(ctypes.c_double), P(ctypes.c_double), P(ctypes.c_uint64)]
             L.orc_interference.argtypes = [P(ctypes.c_double), P(ctypes.c_double)]
             L.orc_interference.restype = ctypes.c_double
             _lib = L
@@ -230,7 +231,6 @@ class Oracle:
         self._check(self.L.orc_count_flops(*self._args(), g0, g1, ctypes.byref(f), ctypes.byref(c)))
         return f.value, c.value
 
-
     def count_flops_ids(self, ids) -> int:
         """FP64 operations of the definition for the given configurations, each evaluated from
         scratch (no level shared between configurations)."""
@@ -238,6 +238,17 @@ class Oracle:
         f = ctypes.c_uint64()
         self._check(self.L.orc_count_flops_ids(*self._args(), _up(a), len(a), ctypes.byref(f)))
         return f.value
+
+
+def count_interference(X, phi) -> int:
+    """FP64 operations the counting build of the oracle records for Algorithm 1 on one vector."""
+    x = np.ascontiguousarray(X, dtype=np.float64)
+    p = np.ascontiguousarray(phi, dtype=np.float64).reshape(64)
+    f = ctypes.c_uint64()
+    rc = lib().orc_count_interference(_dp(x), _dp(p), ctypes.byref(f))
+    if rc != 0:
+        raise RuntimeError("orc_count_interference failed")
+    return f.value
 
 
 def interference(X, phi) -> float:

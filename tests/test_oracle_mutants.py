@@ -19,7 +19,8 @@ from oracle import oracle as O
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PINS = ["tests/test_oracle_pins.py", "tests/test_oracle_terms.py", "tests/test_oracle_reduce.py",
-        "tests/test_oracle_alpha.py", "tests/test_oracle_pareto.py", "tests/test_oracle_calib.py"]
+        "tests/test_oracle_alpha.py", "tests/test_oracle_pareto.py", "tests/test_oracle_calib.py",
+        "tests/test_oracle_flops.py"]
 
 MUTANTS = {
     "forward peak drops the optimizer-step unit": (
@@ -75,6 +76,15 @@ MUTANTS = {
         "(int64_t)((k > 1) + (k < PP))", "(int64_t)((k > 1) || (k < PP))"),
     "measured efficiency multiplied instead of divided": (
         "ie.push_back(1.0 / h.eta_tab[i]);", "ie.push_back(h.eta_tab[i]);"),
+    "operation counter scores a fused multiply-add as one operation": (
+        "inline Counted fma3(Counted a, Counted b, Counted c) { g_flops += 2;",
+        "inline Counted fma3(Counted a, Counted b, Counted c) { g_flops += 1;"),
+    "operation counter scores a comparison (min/max) as an operation": (
+        "inline bool operator<(Counted a, Counted b) { return a.v < b.v; }",
+        "inline bool operator<(Counted a, Counted b) { ++g_flops; return a.v < b.v; }"),
+    "operation counter skips subtractions": (
+        "inline Counted operator-(Counted a, Counted b) { ++g_flops; return",
+        "inline Counted operator-(Counted a, Counted b) { return"),
     "measured efficiency of the next microbatch size": (
         "ie.push_back(1.0 / h.eta_tab[i]);", "ie.push_back(1.0 / h.eta_tab[(i + 1) % X.mb.size()]);"),
 }
