@@ -2,8 +2,9 @@
 (cost model + feasibility filter + per-bucket and per-group reductions) and the FP64
 vector roofline fraction of the evaluation kernel.
 
-One step = one mist_eval_space over the whole space of the workload (default gpt2.7b-d16: GPT
-L32 h2560, 273,952,500 configurations, 4,527 groups), inputs resident on the GPU.
+One step = one mist_eval_space over the whole space of the workload (default llama42b-d128-hw64:
+Llama L60 h8192 GQA-8, D=128, 64 hardware samples in one launch, 29,939,155,200 configurations,
+66,496 groups, the largest workload), inputs resident on the GPU.
 Prints one JSON line; its "alpha_frontier" field times the same space with weight samples of
 Eq. 4 added (the per-group (t, d) argmins), and its "exact_frontier" field the exact
 (unbucketed) time-vs-memory staircase of every group on the evaluated space.  The CPU baseline is the plain oracle timed on this host over a
@@ -39,14 +40,29 @@ def kernel_hash() -> str:
 
 
 def flops_per_config(name: str):
-    """(FP64 operations of the definition for one configuration on its own, the same with every
-    level shared among the configurations below it, as the oracle's loops evaluate it)."""
+    """(FP64 operations of the definition per configuration with every level shared among the
+    configurations below it, as the oracle's nested loops evaluate it: the algorithmic unit; the
+    same for one configuration evaluated on its own, every level repeated)."""
     try:
         with open(FLOPS_FILE) as f:
             w = json.load(f)["workloads"][name]
-            return w["flops_per_config"], w["flops_per_config_shared_levels"]
+            return w["flops_per_config_shared_levels"], w["flops_per_config"]
     except (OSError, KeyError, ValueError):
         return None, None
+
+
+def counter_record(name: str):
+    """FP64 operations the evaluation kernel executes per configuration, from the committed
+    rocprofv3 instruction counters (64 x (ADD + MUL + TRANS + 2 FMA) F64 wave instructions per
+    configuration), if they were taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)[name]
+    except (OSError, KeyError, ValueError):
+        return None
+    if rec.get("kernel_sha") != kernel_hash():
+        return None
+    return rec.get("executed_fp64_per_config")
 
 
 def traffic_record(name: str, n_launch_configs: int):
@@ -62,14 +78,14 @@ def traffic_record(name: str, n_launch_configs: int):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(wl: dict, seconds: float) -> dict:
-    """The oracle as it stands, one process, one thread, over seeded random groups until
-    about ``seconds`` of work."""
+def _oracle_for(wl: dict, seconds: float, shard: int, n_shards: int):
+    """The oracle over this shard's share of the groups (a seeded random order dealt round robin)
+    until about ``seconds`` of work: (groups, configurations, seconds)."""
     import numpy as np
     from oracle import oracle as O
 
     o = O.Oracle(wl)
-    order = np.random.default_rng(2025).permutation(o.n_groups)
+    order = np.random.default_rng(2025).permutation(o.n_groups)[shard::n_shards]
     keys = o.group_keys()
     done = configs = 0
     t0 = time.perf_counter()
@@ -79,12 +95,52 @@ def cpu_baseline(wl: dict, seconds: float) -> dict:
         configs += keys[int(g)]["size"]
         if time.perf_counter() - t0 >= seconds:
             break
-    dt = time.perf_counter() - t0
-    return {
+    return done, configs, time.perf_counter() - t0, o.n_groups
+
+
+def _oracle_shard(job):
+    return _oracle_for(*job)
+
+
+def host_cpu() -> dict:
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count() or 1
+    return {"cpu_model": model, "nproc": usable, "cpu_count": os.cpu_count()}
+
+
+def cpu_baseline(wl: dict, seconds: float, shards: int) -> dict:
+    """The oracle as it stands: one process (one thread) over seeded random groups until about
+    ``seconds`` of work; then, when ``shards`` > 1, that many single-threaded processes over
+    disjoint groups for the same time, as the parity runs over the large workloads use it."""
+    done, configs, dt, n_groups = _oracle_for(wl, seconds, 0, 1)
+    host = host_cpu()
+    rec = {
         "value": configs / dt, "unit": "configs/s", "cores": 1, "kind": "oracle",
         "sample": "%d of %d groups of %s in seeded random order, %d configs, %.1f s" % (
-            done, o.n_groups, wl["name"], configs, dt),
+            done, n_groups, wl["name"], configs, dt),
+        **host,
     }
+    if shards > 1:
+        import multiprocessing as mp
+        with mp.get_context("spawn").Pool(shards) as pool:
+            parts = pool.map(_oracle_shard, [(wl, seconds, i, shards) for i in range(shards)], chunksize=1)
+        total = sum(p[1] for p in parts)
+        wall = max(p[2] for p in parts)
+        rec["sharded"] = {"value": total / wall, "unit": "configs/s", "processes": shards,
+                          "sample": "%d groups, %d configs over %d single-threaded oracle processes, "
+                                    "%.1f s" % (sum(p[0] for p in parts), total, shards, wall)}
+    return rec
 
 
 def main() -> int:
@@ -92,8 +148,12 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="gpt2.7b-d16", choices=["gpt1.3b-d8", "gpt2.7b-d16", "llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"])
+    ap.add_argument("--workload", default="llama42b-d128-hw64",
+                    choices=["gpt1.3b-d8", "gpt2.7b-d16", "llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-shards", type=int, default=0,
+                    help="single-threaded oracle processes of the sharded CPU baseline (0: the usable "
+                         "CPUs, at most 16; 1: none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--alphas", type=int, default=8,
                     help="after the headline run, also time the space with this many weight samples of "
@@ -101,6 +161,10 @@ def main() -> int:
     ap.add_argument("--exact-runs", type=int, default=10,
                     help="after the headline run, time this many exact (non-bucketed) frontier passes "
                          "(mist_eval_pareto_exact) on the evaluated space; 0 skips them")
+    ap.add_argument("--probe-fp64", action="store_true",
+                    help="instead of the benchmark, run the FP64 instruction-mix probe (one kernel per "
+                         "instruction kind with a known count, for reading the profiler's FP64 counters) "
+                         "and print the expected counts")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="after the timed region, copy a buffer of this many MiB on the device "
                          "(a plain copy kernel of known size, to scale the HBM byte counters)")
@@ -117,6 +181,14 @@ def main() -> int:
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.probe_fp64:
+        n_threads, reps = 256 * 1024, 64
+        want = {}
+        for kind in mist.PROBE_KINDS:
+            want[kind] = mist.probe_fp64(kind, n_threads, reps)
+        print(json.dumps({"probe": "fp64 instruction mix", "kernel": "k_probe<kind>",
+                          "kinds": mist.PROBE_KINDS, "wave_instructions_per_dispatch": want}))
+        return 0
     props = torch.cuda.get_device_properties(0)
     wl = W.workload(args.workload)
 
@@ -163,17 +235,26 @@ def main() -> int:
     value = S.n_configs / (ms_per_step / 1e3)
     k1_avg = k1_ms / n
     k2_avg = k2_ms / n
-    fpc, fsh = flops_per_config(wl["name"])
+    fpc, fscratch = flops_per_config(wl["name"])
     roofline = None
     if fpc is not None:
+        # Algorithmic FLOPs: the definition's FP64 operations as the oracle's nested loops
+        # perform them (each level once per combination of the digits it depends on).
         achieved = fpc * S.n_configs / (k1_avg / 1e3) / 1e12
-        shared = fsh * S.n_configs / (k1_avg / 1e3) / 1e12
         traffic = traffic_record(wl["name"], S.n_configs)
         roofline = {"bound": "alu", "achieved": achieved, "peak": FP64_VECTOR_PEAK_TFLOPS,
                     "unit": "TFLOP/s", "frac": achieved / FP64_VECTOR_PEAK_TFLOPS, "traffic": traffic,
                     "kernel": "k_eval", "flops_per_config": fpc,
-                    "flops_per_config_shared_levels": fsh,
-                    "frac_shared_levels": shared / FP64_VECTOR_PEAK_TFLOPS}
+                    "flops_unit": "FP64 operations of the cost model per configuration with every loop level "
+                                  "shared, as the oracle evaluates it (fma = 2)",
+                    # Labelled extras: the same definition with every level repeated per
+                    # configuration, and what the kernel executes by the instruction counters.
+                    "flops_per_config_from_scratch": fscratch,
+                    "frac_from_scratch": fscratch * S.n_configs / (k1_avg / 1e3) / 1e12 / FP64_VECTOR_PEAK_TFLOPS}
+        executed = counter_record(wl["name"])
+        if executed is not None:
+            roofline["executed_fp64_per_config"] = executed
+            roofline["frac_executed"] = executed * S.n_configs / (k1_avg / 1e3) / 1e12 / FP64_VECTOR_PEAK_TFLOPS
 
     exact = None
     if args.exact_runs > 0:
@@ -215,7 +296,7 @@ def main() -> int:
         a_total = start.elapsed_time(end)
         a_k1, a_k2, a_n = SA.read_timing()
         SA.set_timing(False)
-        a_fpc = None if fpc is None else fpc + 3.0 * A   # + per sample: (1-alpha)*d and one fma
+        a_fpc = None if fpc is None else fpc + 3.0 * A   # + per sample: (1-alpha)*d and one fma (shared levels)
         a_k1_avg = a_k1 / a_n
         alpha = {"n_alphas": A, "value": S.n_configs / (a_total / args.steps / 1e3), "unit": "configs/s",
                  "ms_per_step": a_total / args.steps, "eval_kernel_ms": a_k1_avg, "reduce_kernel_ms": a_k2 / a_n,
@@ -226,7 +307,8 @@ def main() -> int:
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline: oracle for about %.0f s" % args.cpu_seconds)
-        cpu = cpu_baseline(wl, args.cpu_seconds)
+        shards = args.cpu_shards or min(16, host_cpu()["nproc"])
+        cpu = cpu_baseline(wl, args.cpu_seconds, shards)
 
     rec = {
         "metric": METRIC, "value": value, "unit": "configs/s", "n_gpus": 1, "steps": args.steps,

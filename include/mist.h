@@ -398,6 +398,25 @@ mist_status mist_interference(const double* phi, const double* x, double* out);
 mist_status mist_measure_eta(const mist_model_desc* m, const int32_t* mb, int32_t n_mb, int32_t tp,
                              double peak_flops, int32_t reps, double* eta, double* sec);
 
+/* ---------------------------------------------------------------------------------------
+ * Measurement support: an FP64 instruction-mix probe for reading the profiler's per-type FP64
+ * instruction counters (which of them counts FP64 min, max and compare) against known counts.
+ * --------------------------------------------------------------------------------------- */
+#define MIST_PROBE_ADD 0
+#define MIST_PROBE_MUL 1
+#define MIST_PROBE_FMA 2
+#define MIST_PROBE_MIN 3
+#define MIST_PROBE_MAX 4
+#define MIST_PROBE_CMP 5 /* v_cmp_lt_f64 */
+
+/* Enqueues on hip_stream one kernel of n_threads threads (a positive multiple of 256) each of
+ * which issues reps x 8 FP64 instructions of the given kind and no other FP64 arithmetic; it
+ * reads device in[2 * n_threads] (operands; any finite values) and writes device
+ * out[n_threads].  *n_instructions (may be NULL) receives the wave-level count of the probed
+ * instruction: n_threads / 64 x reps x 8.  Errors: MIST_E_INVALID, MIST_E_DEVICE. */
+mist_status mist_probe_fp64(int32_t kind, const double* in, uint64_t* out, int64_t n_threads, int32_t reps,
+                            uint64_t* n_instructions, void* hip_stream);
+
 /* Frees every buffer of the space (through its allocator).  NULL is accepted. */
 mist_status mist_space_destroy(mist_space* S);
 

@@ -27,8 +27,10 @@ EXPORTS = [
     "mist_read_timing", "mist_launch_info", "mist_space_destroy", "mist_last_error",
     "mist_plan_points", "mist_plan_pipeline", "mist_eval_pareto_exact", "mist_get_pareto_exact", "mist_exact_info",
     "mist_corun_create", "mist_corun_run", "mist_corun_reduce", "mist_corun_measure", "mist_corun_destroy",
-    "mist_fit_phi", "mist_interference", "mist_measure_eta",
+    "mist_fit_phi", "mist_interference", "mist_measure_eta", "mist_probe_fp64",
 ]
+
+PROBE_KINDS = {"add": 0, "mul": 1, "fma": 2, "min": 3, "max": 4, "cmp": 5}
 
 
 class MistError(RuntimeError):
@@ -171,6 +173,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         L.mist_interference.argtypes = [dp, dp, dp]
         L.mist_measure_eta.argtypes = [P(ModelDesc), ip, ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
                                        ctypes.c_int32, dp, dp]
+        L.mist_probe_fp64.argtypes = [ctypes.c_int32, vp, vp, ctypes.c_int64, ctypes.c_int32, P(ctypes.c_uint64), vp]
         L.mist_last_error.restype = ctypes.c_char_p
         for name in EXPORTS:
             if name != "mist_last_error":
@@ -466,6 +469,20 @@ def interference(phi, x) -> float:
     out = ctypes.c_double()
     _check(L, L.mist_interference(_dptr(p), _dptr(xx), ctypes.byref(out)))
     return out.value
+
+
+def probe_fp64(kind: str, n_threads: int, reps: int, stream=None) -> int:
+    """Enqueues the FP64 instruction-mix probe of one kind (add, mul, fma, min, max, cmp) on the
+    current (or given) stream; returns the wave-level count of the probed instruction."""
+    import torch
+    L = load()
+    inp = torch.rand(2 * n_threads, dtype=torch.float64, device="cuda") + 0.5
+    out = torch.empty(n_threads, dtype=torch.int64, device="cuda")
+    n = ctypes.c_uint64()
+    _check(L, L.mist_probe_fp64(PROBE_KINDS[kind], ctypes.c_void_p(inp.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                                n_threads, reps, ctypes.byref(n), _stream_handle(stream)))
+    torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
+    return n.value
 
 
 def measure_eta(model: dict, mb, tp: int, peak_flops: float, reps: int = 5) -> tuple[np.ndarray, np.ndarray]:

@@ -18,7 +18,7 @@ HEADER = os.path.join(ROOT, "include", "mist.h")
 def _declared():
     with open(HEADER) as f:
         text = f.read()
-    return sorted(set(re.findall(r"\b(mist_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(mist_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_header_declares_the_boundary():

@@ -26,7 +26,9 @@ def test_flops_per_config_come_from_the_counting_oracle():
     with open(bench.FLOPS_FILE) as f:
         stored = json.load(f)["workloads"]
     for name, w in stored.items():
-        fpc, fsh = bench.flops_per_config(name)
+        # The algorithmic unit is the shared-level count (the oracle's nested loops); the
+        # from-scratch count is reported beside it.
+        fsh, fpc = bench.flops_per_config(name)
         assert fpc == w["flops_per_config"] and fsh == w["flops_per_config_shared_levels"]
         assert 0 < fsh < fpc
     assert bench.flops_per_config("no such workload") == (None, None)
@@ -44,6 +46,20 @@ def test_traffic_is_reported_only_for_the_kernel_it_was_measured_on(monkeypatch)
 
 def test_cpu_baseline_record():
     from paper_2503_19050_amd import workloads as W
-    rec = bench.cpu_baseline(W.workload("gpt1.3b-d8"), 0.5)
+    rec = bench.cpu_baseline(W.workload("gpt1.3b-d8"), 0.5, 2)
     assert rec["kind"] == "oracle" and rec["cores"] == 1 and rec["unit"] == "configs/s"
     assert rec["value"] > 0 and "gpt1.3b-d8" in rec["sample"]
+    assert rec["nproc"] >= 1 and isinstance(rec["cpu_model"], str)
+    sh = rec["sharded"]
+    assert sh["processes"] == 2 and sh["value"] > 0 and sh["unit"] == "configs/s"
+
+
+def test_counter_record_only_for_the_kernel_it_was_measured_on(monkeypatch, tmp_path):
+    rec = {"w": {"kernel_sha": "abc", "executed_fp64_per_config": 50.0}}
+    p = tmp_path / "t.json"
+    p.write_text(json.dumps(rec))
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(p))
+    monkeypatch.setattr(bench, "kernel_hash", lambda: "abc")
+    assert bench.counter_record("w") == 50.0
+    monkeypatch.setattr(bench, "kernel_hash", lambda: "abd")
+    assert bench.counter_record("w") is None

@@ -20,7 +20,7 @@ pytestmark = pytest.mark.skipif(shutil.which("gcc") is None, reason="no gcc")
 
 def _declared():
     with open(HEADER) as f:
-        return sorted(set(re.findall(r"\b(mist_[a-z_]+)\s*\(", f.read())))
+        return sorted(set(re.findall(r"\b(mist_[a-z0-9_]+)\s*\(", f.read())))
 
 
 def test_header_is_c99():
