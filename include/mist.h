@@ -81,20 +81,22 @@ typedef struct mist_model_desc {
  * operator database, communication as bytes / bandwidth) and of the interference model
  * (Sec. 5.2.2: one slowdown factor per co-running combination and stream). */
 typedef struct mist_hw_desc {
-  double flops;      /* peak FLOP/s, > 0 */
+  double flops;      /* peak FLOP/s, in [2^-200, 2^200] */
   double mem_bytes;  /* memory budget in bytes, > 0 (the Mem_Budget of Eq. 4) */
-  double pcie_bw;    /* host<->device bytes/s, > 0 */
-  double link_bw;    /* device<->device bytes/s, > 0 */
-  double eta_max;    /* compute efficiency eta(b) = eta_max*b*s/(b*s + n_half); 0 selects
-                        eta_tab */
-  double n_half;
+  double pcie_bw;    /* host<->device bytes/s, in [2^-200, 2^200] */
+  double link_bw;    /* device<->device bytes/s, in [2^-200, 2^200] */
+  double eta_max;    /* compute efficiency eta(b) = eta_max*b*s/(b*s + n_half), in [2^-100,
+                        2^100]; 0 selects eta_tab */
+  double n_half;     /* in [0, 2^100] */
   double phi[16][4]; /* phi[mask][j]: slowdown of stream j (0 compute, 1 GPU-GPU, 2 host->
-                        device, 3 device->host) when the streams of mask co-run; >= 1 and
-                        finite; entries of absent streams and single-stream masks unused */
+                        device, 3 device->host) when the streams of mask co-run; in [1, 2^100];
+                        entries of absent streams and single-stream masks unused */
   double eta_tab[MIST_MAX_MB]; /* with eta_max = 0: measured efficiency of the space's i-th
-                        microbatch size (positive, finite), e.g. from mist_measure_eta (the
+                        microbatch size, in [2^-100, 2^100], e.g. from mist_measure_eta (the
                         operator database of Sec. 5.2.1); unused otherwise */
 } mist_hw_desc;
+/* The magnitude bounds lie far beyond any physical value; they keep every non-zero stream time
+ * of the runtime model within [2^-363, 2^500], so that no step of Algorithm 1 underflows. */
 
 /* The search space of Table 2 for every candidate stage. */
 typedef struct mist_space_desc {
@@ -102,7 +104,8 @@ typedef struct mist_space_desc {
   int64_t global_batch;  /* B */
   const int32_t* mb;     /* host: microbatch sizes, strictly ascending, >= 1 */
   int32_t n_mb;          /* 1..MIST_MAX_MB */
-  const double* ratios;  /* host: offload ratios, strictly ascending in [0, 1] */
+  const double* ratios;  /* host: offload ratios, strictly ascending in [0, 1]; a non-zero ratio
+                            is at least 2^-100 */
   int32_t n_ratios;      /* R, 1..MIST_MAX_RATIOS */
   int32_t n_buckets;     /* NB, 1..MIST_MAX_BUCKETS; bucket edges E_j = M*(j+1)/NB */
   int32_t l_rule;        /* MIST_L_FULL or MIST_L_BALANCED */
@@ -295,6 +298,22 @@ mist_status mist_eval_ids(mist_space* S, const uint64_t* ids, int64_t n, double*
  * MIST_E_DEVICE. */
 mist_status mist_set_timing(mist_space* S, int32_t on);
 mist_status mist_read_timing(mist_space* S, double* eval_ms, double* reduce_ms, int64_t* n_evals);
+
+/* Tile t of the evaluation kernel: its group, the global id of its first configuration and its
+ * configuration count (a tile covers consecutive ids of one group).  Errors: MIST_E_RANGE. */
+mist_status mist_tile_info(const mist_space* S, int32_t t, int64_t* group, uint64_t* first_id, int64_t* n_configs);
+
+/* Parity checks of the evaluation kernel itself (the cost model of Eq. 4-6 with Algorithm 1,
+ * Sec. 5.2): runs the evaluation kernel's own per-configuration path (not the per-id path of
+ * mist_eval_ids) over the listed tiles and writes, for every configuration of tiles[0..n-1] in
+ * that order and in id order within a tile, five doubles into host out: t, d, mem, obj and the
+ * bucket entry the kernel chose (0..NB-1 for a feasible configuration; NB..64 for an infeasible
+ * one, which the reduction ignores).  cap is the capacity of out in configurations.
+ * Synchronous on hip_stream; allocates temporary device memory through the space's allocator.
+ * Errors: MIST_E_INVALID, MIST_E_RANGE (a tile index, or cap too small), MIST_E_NOMEM,
+ * MIST_E_DEVICE. */
+mist_status mist_debug_eval_tiles(mist_space* S, const int32_t* tiles, int32_t n, double* out, int64_t cap,
+                                  void* hip_stream);
 
 /* Launch geometry of the evaluation kernel: tiles (work items, one wave each), threads per
  * tile, strips per full-size tile (a strip is the R^2 configurations sharing pair,

@@ -215,22 +215,35 @@ std::string validate(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n
   if (m->flash != 0 && m->flash != 1) return "flash must be 0 or 1";
   if (m->hidden % m->heads) return "hidden must be a multiple of heads";
   if (m->heads % m->kv_heads) return "heads must be a multiple of kv_heads";
+  // Magnitude bounds (far beyond any physical value) under which every non-zero stream time is
+  // at least 2^-363 and at most 2^500: a difference of two distinct scaled times then exceeds
+  // 2^-415, and dividing it by a factor of at most 2^100 cannot round to zero, which the
+  // evaluation kernel's second interference round relies on (a stream keeps running exactly when
+  // its scaled time exceeds the overlap).
+  const double lo_rate = 0x1p-200, hi_rate = 0x1p200, lo_eff = 0x1p-100, hi_eff = 0x1p100;
   for (int32_t i = 0; i < n_hw; ++i) {
     const mist_hw_desc& h = hw[i];
     const double v[4] = {h.flops, h.mem_bytes, h.pcie_bw, h.link_bw};
     for (double x : v)
       if (!(x > 0.0) || !std::isfinite(x)) return "hardware rates and memory must be positive and finite";
+    if (!(h.flops >= lo_rate && h.flops <= hi_rate && h.pcie_bw >= lo_rate && h.pcie_bw <= hi_rate &&
+          h.link_bw >= lo_rate && h.link_bw <= hi_rate))
+      return "flops, pcie_bw and link_bw must lie in [2^-200, 2^200]";
     if (!(h.eta_max >= 0.0) || !std::isfinite(h.eta_max) || !(h.n_half >= 0.0) || !std::isfinite(h.n_half))
       return "eta_max and n_half must be non-negative and finite";
+    if (h.eta_max != 0.0 && !(h.eta_max >= lo_eff && h.eta_max <= hi_eff)) return "eta_max must be 0 or in [2^-100, 2^100]";
+    if (!(h.n_half <= hi_eff)) return "n_half must be at most 2^100";
     if (h.eta_max == 0.0 && s && s->mb && s->n_mb >= 1 && s->n_mb <= MIST_MAX_MB)
       for (int32_t j = 0; j < s->n_mb; ++j)
-        if (!(h.eta_tab[j] > 0.0) || !std::isfinite(h.eta_tab[j]))
-          return "with eta_max = 0 every eta_tab entry of the microbatch list must be positive and finite";
+        if (!(h.eta_tab[j] >= lo_eff && h.eta_tab[j] <= hi_eff))
+          return "with eta_max = 0 every eta_tab entry of the microbatch list must lie in [2^-100, 2^100]";
     for (int mask = 0; mask < 16; ++mask) {
       if (popcount4(mask) < 2) continue;
       for (int j = 0; j < 4; ++j)
         if ((mask >> j & 1) && !(h.phi[mask][j] >= 1.0 && std::isfinite(h.phi[mask][j])))
           return "slowdown factors must be finite and >= 1";
+        else if ((mask >> j & 1) && !(h.phi[mask][j] <= hi_eff))
+          return "slowdown factors must be at most 2^100";
     }
   }
   if (s->n_devices < 1 || s->global_batch < 1) return "n_devices and global_batch must be positive";
@@ -241,6 +254,8 @@ std::string validate(const mist_model_desc* m, const mist_hw_desc* hw, int32_t n
   for (int32_t i = 0; i < s->n_ratios; ++i)
     if (!(s->ratios[i] >= 0.0 && s->ratios[i] <= 1.0) || (i && !(s->ratios[i] > s->ratios[i - 1])))
       return "ratios must be strictly ascending in [0, 1]";
+    else if (s->ratios[i] != 0.0 && !(s->ratios[i] >= 0x1p-100))
+      return "a non-zero ratio must be at least 2^-100";
   if (s->n_buckets < 1 || s->n_buckets > MIST_MAX_BUCKETS) return "n_buckets out of range";
   if (s->l_rule != MIST_L_FULL && s->l_rule != MIST_L_BALANCED) return "unknown l_rule";
   if (s->n_alphas < 0 || s->n_alphas > MIST_MAX_ALPHAS || (s->n_alphas > 0 && !s->alphas))
@@ -1322,6 +1337,70 @@ mist_status mist_read_timing(mist_space* S, double* eval_ms, double* reduce_ms, 
   if (reduce_ms) *reduce_ms = b;
   if (n_evals) *n_evals = (int64_t)n;
   return MIST_OK;
+}
+
+mist_status mist_tile_info(const mist_space* S, int32_t t, int64_t* group, uint64_t* first_id, int64_t* n_configs) {
+  if (!S) return fail(MIST_E_INVALID, "space is null");
+  if (t < 0 || (size_t)t >= S->tiles.size()) return fail(MIST_E_RANGE, "tile out of range");
+  const DevTile& T = S->tiles[t];
+  const uint64_t R2 = (uint64_t)S->R * (uint64_t)S->R;
+  if (group) *group = T.group;
+  if (first_id) *first_id = S->groups[T.group].base + (uint64_t)T.strip_begin * R2;
+  if (n_configs) *n_configs = (int64_t)((uint64_t)(T.strip_end - T.strip_begin) * R2);
+  return MIST_OK;
+}
+
+mist_status mist_debug_eval_tiles(mist_space* S, const int32_t* tiles, int32_t n, double* out, int64_t cap,
+                                  void* hip_stream) {
+  if (!S) return fail(MIST_E_INVALID, "space is null");
+  if (n < 0 || (n > 0 && (!tiles || !out))) return fail(MIST_E_INVALID, "tiles and out must be given");
+  if (n == 0) return MIST_OK;
+  try {
+    hipStream_t st = (hipStream_t)hip_stream;
+    const int64_t R2 = (int64_t)S->R * S->R;
+    std::vector<int64_t> off((size_t)n);
+    int64_t total = 0;
+    for (int32_t i = 0; i < n; ++i) {
+      if (tiles[i] < 0 || (size_t)tiles[i] >= S->tiles.size()) return fail(MIST_E_RANGE, "tile out of range");
+      off[(size_t)i] = total;
+      total += (int64_t)(S->tiles[tiles[i]].strip_end - S->tiles[tiles[i]].strip_begin) * R2;
+    }
+    if (total > cap) return fail(MIST_E_RANGE, "cap is smaller than the listed tiles' configurations");
+    // Work of this space queued on other streams shares the tile counters: it finishes first.
+    if (S->evaluated && S->stream != st) {
+      const hipError_t e = hipStreamSynchronize(S->stream);
+      if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+    }
+    if (S->exact_launched && S->exact_stream != st) {
+      const hipError_t e = hipStreamSynchronize(S->exact_stream);
+      if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+    }
+    TempBuf dlist(S, (size_t)n * sizeof(int32_t));
+    TempBuf doff(S, (size_t)n * sizeof(int64_t));
+    TempBuf dout(S, (size_t)std::max<int64_t>(total, 1) * 5 * sizeof(double));
+    if (!dlist.p || !doff.p || !dout.p) return fail(MIST_E_NOMEM, "device allocation failed: debug tiles");
+    auto drained = [&](mist_status code) {
+      (void)hipStreamSynchronize(st);
+      return code;
+    };
+    hipError_t e = copy_async(dlist.p, tiles, (size_t)n * sizeof(int32_t), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess) e = copy_async(doff.p, off.data(), (size_t)n * sizeof(int64_t), hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return drained(fail_hip(e, "debug tiles: upload"));
+    EvalArgs ea = eval_args(S);
+    ea.tile_list = (const int32_t*)dlist.p;
+    ea.n_list = n;
+    ea.dump = (double*)dout.p;
+    ea.dump_off = (const int64_t*)doff.p;
+    int k = launch_pairs(ea, st);  // pair constants, and the tile counters' reset
+    if (!k) k = launch_eval(ea, mode_grid(S, kModeDump), kModeDump, st);
+    if (k) return drained(fail_hip((hipError_t)k, "debug tiles: launch"));
+    e = copy_async(out, dout.p, (size_t)total * 5 * sizeof(double), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return drained(fail_hip(e, "debug tiles: results"));
+    return MIST_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(MIST_E_NOMEM, "host allocation failed");
+  }
 }
 
 mist_status mist_launch_info(const mist_space* S, int64_t* n_tiles, int32_t* block, int32_t* strips_per_tile) {

@@ -90,6 +90,7 @@ struct FiltEntry {
 constexpr int kModeBuckets = 0;  // bucket minima (and per-tile partials)
 constexpr int kModeAlpha = 1;    // bucket minima and the weight-sampled argmins
 constexpr int kModeEmit = 2;     // exact frontier: write and count each tile's candidates
+constexpr int kModeDump = 3;     // per-configuration values of listed tiles (parity checks)
 
 struct EvalArgs {
   DevModel m;
@@ -130,6 +131,11 @@ struct EvalArgs {
   uint64_t* cand_key;        // memory bit patterns (a non-negative double orders like its bits)
   double* cand_obj;
   uint64_t* cand_id;
+  // Dump variant (parity checks): listed item x writes, for every configuration of its tile in
+  // local-id order, t, d, mem, obj and the bucket entry the kernel chose (as a double; NB..64
+  // are the sinks of infeasible configurations) to dump[5 * (dump_off[x] + i)..].
+  double* dump;
+  const int64_t* dump_off;   // [n_list]
 };
 
 struct ReduceArgs {

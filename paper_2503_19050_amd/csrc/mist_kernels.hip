@@ -233,30 +233,53 @@ __device__ __forceinline__ double interference(double c, double g, double h, dou
   return T + remaining(x);
 }
 
-// First round with a pattern known in advance (row at e), then two looked-up rounds.
-__device__ __forceinline__ double interference_first(const double* __restrict__ e, double c, double g,
-                                                     double h, double d, const double* __restrict__ tab) {
-  Streams x{c, g, h, d};
-  double T = round_row(x, e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]);
-  T = T + round_lookup<kLdsRow>(x, tab);
-  T = T + round_lookup<kLdsRow>(x, tab);
-  return T + remaining(x);
-}
-
-// The first-microbatch streams of a strip: compute and GPU-GPU times (and their scaled
-// values under the strip's first-round row) are fixed, the host streams vary.
-struct FirstRow {
-  double s0, s1, m01;   // C * phi0, G2G * phi1, min of the two
+// Calls whose first round uses a row known in advance: every configuration of a strip whose host
+// streams both run (pattern 15, or 13 without GPU-GPU traffic), with compute c and GPU-GPU g fixed
+// per strip.  The strip precomputes the scaled c and g, their minimum m01, and what streams 0 and 1
+// contribute to the second round's row.  After the first round a member keeps running exactly
+// when its scaled time exceeds the overlap (s_j - ov > 0, and (s_j - ov) * psi_j cannot round to
+// zero: the host's input bounds keep every non-zero stream time and difference far above the
+// subnormal range), so the second row follows from three comparisons instead of four on the
+// updated times: streams 0 and 1 both keep running when ov < m01, and those above m01 when
+// ov == m01 (ov <= m01 always).
+struct KnownRow {
+  double s0, s1, m01;   // c * phi0, g * phi1 (NaN when GPU-GPU is no member), min of the two
   double f2, f3, p0, p1, p2, p3;
+  const char* row_lt;   // the table plus the second-row offset of streams 0 and 1 for ov < m01
+  const char* row_eq;   // and for ov == m01
 };
 
-__device__ __forceinline__ double interference_strip(const FirstRow& r, double h, double d,
+__device__ __forceinline__ KnownRow known_row(const double* __restrict__ tab, int pattern, double c, double g) {
+  const double* e = tab + pattern * kLdsRow;
+  KnownRow r;
+  r.s0 = c * e[0];
+  r.s1 = g * e[1];
+  r.m01 = __builtin_fmin(r.s0, r.s1);
+  r.f2 = e[2];
+  r.f3 = e[3];
+  r.p0 = e[4];
+  r.p1 = e[5];
+  r.p2 = e[6];
+  r.p3 = e[7];
+  constexpr int kRowBytes = kLdsRow * (int)sizeof(double);
+  const char* t = reinterpret_cast<const char*>(tab);
+  r.row_lt = t + (pattern & 3) * kRowBytes;
+  r.row_eq = t + ((pattern & 1) && r.s0 > r.m01 ? kRowBytes : 0) + ((pattern & 2) && r.s1 > r.m01 ? 2 * kRowBytes : 0);
+  return r;
+}
+
+// Host streams h, d > 0 of such a call: first round with the known row, second with the row
+// derived above, third looked up.
+__device__ __forceinline__ double interference_known(const KnownRow& r, double h, double d,
                                                      const double* __restrict__ tab) {
   const double s2 = h * r.f2, s3 = d * r.f3;
   const double ov = __builtin_fmin(r.m01, __builtin_fmin(s2, s3));
   Streams x{(r.s0 - ov) * r.p0, (r.s1 - ov) * r.p1, (s2 - ov) * r.p2, (s3 - ov) * r.p3};
+  constexpr int kRowBytes = kLdsRow * (int)sizeof(double);
+  const double* e = reinterpret_cast<const double*>((ov < r.m01 ? r.row_lt : r.row_eq) + (s2 > ov ? 4 * kRowBytes : 0) +
+                                                    (s3 > ov ? 8 * kRowBytes : 0));
   double T = ov;
-  T = T + round_lookup<kLdsRow>(x, tab);
+  T = T + round_row(x, e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]);
   T = T + round_lookup<kLdsRow>(x, tab);
   return T + remaining(x);
 }
@@ -320,6 +343,19 @@ struct AlphaEntry {
   unsigned int pad;
 };
 
+// Reads a table entry at a wave-uniform index through the constant address space, so that it
+// arrives in scalar registers (scalar loads; the tables are read-only during the kernel).
+template <class T>
+__device__ __forceinline__ T load_uniform(const T* p) {
+  static_assert(sizeof(T) % 4 == 0, "whole dwords");
+  const __attribute__((address_space(4))) uint32_t* q = (const __attribute__((address_space(4))) uint32_t*)p;
+  T v;
+  uint32_t* d = reinterpret_cast<uint32_t*>(&v);
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 4); ++i) d[i] = q[i];
+  return v;
+}
+
 // A 64-bit key that orders like the double (neither -0 nor NaN occurs as a key).
 __device__ __forceinline__ unsigned long long order_key(double v) {
   const unsigned long long b = (unsigned long long)__double_as_longlong(v);
@@ -355,6 +391,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
                                                                  const PairK* __restrict__ pk) {
   constexpr bool AL = MODE == kModeAlpha;
   constexpr bool EX = MODE == kModeEmit;
+  constexpr bool DM = MODE == kModeDump;
   constexpr int R2 = R * R;
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
   constexpr int IB = ia_block<R>();
@@ -367,7 +404,9 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  // The wave index is uniform across the wave: stated, so that the tile, group and hardware
+  // values derived from it live in scalar registers (scalar loads) rather than in every lane.
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int NB = a.NB;
   const double* __restrict__ rr = ratio;  // read-only and uniform: scalar loads
   const double* __restrict__ om = ratio + R;
@@ -382,7 +421,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
   // runs out, until all have.  When the grid has at least as many waves as there are items
   // no claim is made.  Item x is tile x, or tile tile_list[x] when the emit variant runs a
   // list.
-  const bool listed = EX && a.tile_list != nullptr;
+  const bool listed = (EX || DM) && a.tile_list != nullptr;
   const int n_items = listed ? a.n_list : a.n_tiles;
   const int n_waves = (int)gridDim.x * kWaves;
   const bool claims = n_items > n_waves;
@@ -390,11 +429,11 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
   int exhausted = 0;
   int loaded_hw = -1;
   for (int x = (int)blockIdx.x * kWaves + wave; x < n_items;) {
-    const int t = listed ? a.tile_list[x] : x;
-    const DevTile tile = a.tiles[t];
+    const int t = listed ? load_uniform(a.tile_list + x) : x;
+    const DevTile tile = load_uniform(a.tiles + t);
     // The exact frontier's pass skips a tile that holds no candidate (its count stays 0).
     const int strip_end = EX && a.tile_live && !a.tile_live[t] ? tile.strip_begin : tile.strip_end;
-    const DevGroup g = a.groups[tile.group];
+    const DevGroup g = load_uniform(a.groups + tile.group);
     const DevHw& hw = a.hws[g.hw];
     if (g.hw != loaded_hw) {  // the wave's LDS copy of the hardware tables
       for (int i = lane; i < 16 * kTabStride; i += 64)
@@ -431,7 +470,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
     }
     wave_sync();
 
-    const double iP = hw.iP, kNB = hw.kNB, M = hw.M;
+    const double iP = load_uniform(&hw.iP), kNB = load_uniform(&hw.kNB), M = load_uniform(&hw.M);
     const int l = g.l;
     const int64_t ke = g.k < g.G ? g.k : g.G;
 
@@ -453,17 +492,8 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
 
       // First microbatch: every configuration of the strip with a non-zero offload ratio
       // starts with compute, both host streams and (if it carries traffic) GPU-GPU.
-      const double* e1 = tab + (Z.G2Gf > 0.0 ? 15 : 13) * kLdsRow;
-      FirstRow fr;
-      fr.s0 = K.C * e1[0];
-      fr.s1 = Z.G2Gf * e1[1];
-      fr.m01 = __builtin_fmin(fr.s0, fr.s1);
-      fr.f2 = e1[2];
-      fr.f3 = e1[3];
-      fr.p0 = e1[4];
-      fr.p1 = e1[5];
-      fr.p2 = e1[6];
-      fr.p3 = e1[7];
+      const int pat1 = Z.G2Gf > 0.0 ? 15 : 13;
+      const KnownRow fr = known_row(tab, pat1, K.C, Z.G2Gf);
       const bool zero_strip = r0_zero && rw == 0.0 && rg == 0.0;
       // First-microbatch time of the strip's all-zero configuration (no host streams).
       const double T1z = interference_zero(K.C, Z.G2Gf, tab);
@@ -473,7 +503,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
       // With a positive activation ratio both host streams run, so the stable microbatch's
       // first round has the pattern compute + both host streams (+ GPU-GPU when it carries
       // traffic).
-      const double* es = tab + (Z.G2Gs > 0.0 ? 15 : 13) * kLdsRow;
+      const int pats = Z.G2Gs > 0.0 ? 15 : 13;
 
       // Activation ratios in blocks of IB: the values a block keeps across the optimizer
       // ratios fit the registers, at the price of one more optimizer-level evaluation per
@@ -481,6 +511,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
 #pragma unroll
       for (int ib = 0; ib < R; ib += IB) {
         // Stable time per activation ratio (it does not depend on the optimizer ratio).
+        const KnownRow sr = known_row(tab, pats, K.C, Z.G2Gs);
         double tt[IB];
 #pragma unroll
         for (int c = 0; c < IB; ++c) {
@@ -489,7 +520,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
           const double H2Ds = __builtin_fma(rr[ia], K.A, W.HW) * iP;
           const double D2Hs = __builtin_fma(rr[ia], K.A, W.DG) * iP;
           if (ia == 0 && r0_zero) tt[c] = interference(K.C, Z.G2Gs, H2Ds, D2Hs, tab);
-          else tt[c] = interference_first(es, K.C, Z.G2Gs, H2Ds, D2Hs, tab);
+          else tt[c] = interference_known(sr, H2Ds, D2Hs, tab);
         }
 
 #pragma unroll 1
@@ -508,7 +539,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             const double mem = O.Bmax + SO;
             const double H2Df = __builtin_fma(ra, A, HW) * iP + O.H2Dx;
             const double D2Hf = __builtin_fma(ra, A, DG) * iP + O.D2Hx;
-            double T1 = interference_strip(fr, H2Df, D2Hf, tab);
+            double T1 = interference_known(fr, H2Df, D2Hf, tab);
             if (ia == 0) T1 = zero_oo ? T1z : T1;
             const double tv = tt[c];
             const double d = T1 - tv;
@@ -522,6 +553,15 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             const unsigned int off0 = __umul24((unsigned int)j0, (unsigned int)sizeof(BucketEntry));
             char* const b0 = reinterpret_cast<char*>(bucket) + off0;
             const double e0 = reinterpret_cast<const BucketEntry*>(b0)->edge;
+            if constexpr (DM) {
+              double* o = a.dump + 5 * (a.dump_off[x] + (int64_t)(s - tile.strip_begin) * R2 + io * R + ia);
+              o[0] = tv;
+              o[1] = d;
+              o[2] = mem;
+              o[3] = obj;
+              o[4] = (double)(j0 + (mem > e0 ? 1 : 0));
+              continue;
+            }
             if constexpr (EX) {
               // Exact frontier candidates: feasible, below every lower bucket's minimum, and not
               // dominated by the bucket's winner (no more memory and no smaller objective, not
@@ -545,7 +585,6 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
               continue;
             }
             const bool up = mem > e0;
-            BucketEntry* const be = reinterpret_cast<BucketEntry*>(b0 + (up ? sizeof(BucketEntry) : 0));
 
             // Lexicographic (obj, id) minimum per bucket without a serial loop: the lanes
             // that beat their bucket's entry lower the objective bits with an LDS atomic
@@ -558,10 +597,16 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             // Both candidate entries' keys in one LDS round trip (entry 64 exists: a sink).
             const unsigned long long k_lo = reinterpret_cast<const BucketEntry*>(b0)->key;
             const unsigned long long k_hi = reinterpret_cast<const BucketEntry*>(b0 + sizeof(BucketEntry))->key;
-            const unsigned long long k_old = up ? k_hi : k_lo;
             // A candidate beats the entry: key < k_old, or an equal key with a lower id.  No
             // lane with key > k_old is one, so the exact test waits for a lane with key <= k_old.
-            if (__builtin_amdgcn_ballot_w64(key <= k_old)) {
+            // The two comparisons and the edge test are combined as wave masks (scalar ALU)
+            // instead of selecting k_old first.
+            const unsigned long long m_up = __builtin_amdgcn_ballot_w64(up);
+            const unsigned long long m_lo = __builtin_amdgcn_ballot_w64(key <= k_lo);
+            const unsigned long long m_hi = __builtin_amdgcn_ballot_w64(key <= k_hi);
+            if ((m_lo & ~m_up) | (m_hi & m_up)) {
+              const unsigned long long k_old = up ? k_hi : k_lo;
+              BucketEntry* const be = reinterpret_cast<BucketEntry*>(b0 + (up ? sizeof(BucketEntry) : 0));
               const unsigned int lid = lid_oo + (unsigned int)ia;
               const unsigned int i_old = be->lid;
               const bool cand = (key < k_old) | ((key == k_old) & (lid < i_old));
@@ -631,7 +676,8 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
       }
     }
     // The tile's partials: lane j = bucket j.
-    if constexpr (EX) {
+    if constexpr (DM) {
+    } else if constexpr (EX) {
       // Saturated at 2^31 - 1, which the host rejects (no tile of a space with fewer than
       // 2^32 candidates reaches it).
       if (lane == 0) a.cnt_tile[t] = (int32_t)min(n_cand - n_beg, (int64_t)0x7FFFFFFF);
@@ -907,6 +953,7 @@ void launch_eval_r(const EvalArgs& a, int blocks, int mode, hipStream_t st) {
   switch (mode) {
     case kModeAlpha: launch_eval_rm<R, kModeAlpha>(a, blocks, st); break;
     case kModeEmit: launch_eval_rm<R, kModeEmit>(a, blocks, st); break;
+    case kModeDump: launch_eval_rm<R, kModeDump>(a, blocks, st); break;
     default: launch_eval_rm<R, kModeBuckets>(a, blocks, st); break;
   }
 }
@@ -922,6 +969,7 @@ int blocks_per_cu_r(int mode) {
   switch (mode) {
     case kModeAlpha: return blocks_per_cu_rm<R, kModeAlpha>();
     case kModeEmit: return blocks_per_cu_rm<R, kModeEmit>();
+    case kModeDump: return blocks_per_cu_rm<R, kModeDump>();
     default: return blocks_per_cu_rm<R, kModeBuckets>();
   }
 }

@@ -28,6 +28,7 @@ EXPORTS = [
     "mist_plan_points", "mist_plan_pipeline", "mist_eval_pareto_exact", "mist_get_pareto_exact", "mist_exact_info",
     "mist_corun_create", "mist_corun_run", "mist_corun_reduce", "mist_corun_measure", "mist_corun_destroy",
     "mist_fit_phi", "mist_interference", "mist_measure_eta", "mist_probe_fp64",
+    "mist_tile_info", "mist_debug_eval_tiles",
 ]
 
 PROBE_KINDS = {"add": 0, "mul": 1, "fma": 2, "min": 3, "max": 4, "cmp": 5}
@@ -173,6 +174,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         L.mist_interference.argtypes = [dp, dp, dp]
         L.mist_measure_eta.argtypes = [P(ModelDesc), ip, ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
                                        ctypes.c_int32, dp, dp]
+        L.mist_tile_info.argtypes = [vp, ctypes.c_int32, P(ctypes.c_int64), P(ctypes.c_uint64), P(ctypes.c_int64)]
+        L.mist_debug_eval_tiles.argtypes = [vp, P(ctypes.c_int32), ctypes.c_int32, P(ctypes.c_double),
+                                            ctypes.c_int64, vp]
         L.mist_probe_fp64.argtypes = [ctypes.c_int32, vp, vp, ctypes.c_int64, ctypes.c_int32, P(ctypes.c_uint64), vp]
         L.mist_last_error.restype = ctypes.c_char_p
         for name in EXPORTS:
@@ -371,6 +375,24 @@ class Space:
                                             len(ids), out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
                                             ctypes.c_void_p(_stream_handle(stream))))
         return out
+
+    def tile_info(self, t: int) -> dict:
+        g = ctypes.c_int64()
+        f = ctypes.c_uint64()
+        n = ctypes.c_int64()
+        _check(self.L, self.L.mist_tile_info(self.h, t, ctypes.byref(g), ctypes.byref(f), ctypes.byref(n)))
+        return {"group": g.value, "first_id": f.value, "n_configs": n.value}
+
+    def debug_eval_tiles(self, tiles, stream=None) -> np.ndarray:
+        """The evaluation kernel's own per-configuration values over the listed tiles: rows of
+        (t, d, mem, obj, bucket entry) in tile order, id order within a tile."""
+        tl = np.ascontiguousarray(tiles, dtype=np.int32)
+        total = sum(self.tile_info(int(t))["n_configs"] for t in tl)
+        out = np.empty((max(total, 1), 5), dtype=np.float64)
+        _check(self.L, self.L.mist_debug_eval_tiles(self.h, tl.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                                    len(tl), out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                                    total, _stream_handle(stream)))
+        return out[:total]
 
     def decode(self, cid: int) -> dict:
         c = Config()

@@ -73,6 +73,10 @@ def _create(wl, **over):
     {"s__alphas": [0.5, 1.5]}, {"s__alphas": [-0.25]}, {"s__alphas": [float("nan")]},
     {"s__alphas": [0.5] * 17}, {"s__n_alphas": 2}, {"s__n_alphas": -1},
     {"s__tile_configs": -1}, {"s__max_blocks": -4}, {"s__cand_window": -1},
+    # magnitude bounds: rates in [2^-200, 2^200], efficiencies in [2^-100, 2^100], non-zero
+    # ratios at least 2^-100
+    {"h__flops": 2.0 ** 201}, {"h__pcie_bw": 2.0 ** -201}, {"h__link_bw": 1e300},
+    {"h__eta_max": 2.0 ** -101}, {"h__n_half": 2.0 ** 101}, {"s__ratios": [0.0, 2.0 ** -101, 1.0]},
 ])
 def test_invalid_descriptors_are_rejected(over):
     rc, msg = _create(W.workload("tiny"), **over)
@@ -85,6 +89,14 @@ def test_bad_slowdown_factor_rejected():
     wl["hws"][0]["phi"][15][2] = 0.5
     rc, msg = _create(wl)
     assert rc == -1 and "slowdown" in msg
+
+
+def test_slowdown_factor_above_bound_rejected():
+    wl = W.workload("tiny")
+    wl["hws"][0]["phi"] = [list(r) for r in wl["hws"][0]["phi"]]
+    wl["hws"][0]["phi"][15][1] = 2.0 ** 101
+    rc, msg = _create(wl)
+    assert rc == -1 and "2^100" in msg
 
 
 def test_counts_beyond_exact_range_rejected():

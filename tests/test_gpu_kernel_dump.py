@@ -1,0 +1,134 @@
+"""The evaluation kernel's own per-configuration path against the oracle, configuration by
+configuration (GPU, through the C ABI).
+
+mist_eval_ids evaluates ids one by one with the generic form of Algorithm 1; the evaluation kernel
+instead shares work across a strip (the stable time across optimizer ratios, the first round of
+each call with a row known per strip, the second round's row derived from the strip's scaled
+compute and GPU-GPU times, the closed form of the all-zero configuration).  mist_debug_eval_tiles
+runs that kernel path over listed tiles and returns t, d, mem, obj and the bucket entry it chose
+for every configuration; here they are compared bit for bit with the oracle's per-configuration
+dump (Eq. 4-6, Algorithm 1, Sec. 5.2), and the bucket with the oracle's (an infeasible
+configuration must land on a sink entry, NB..64).
+"""
+
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2503_19050_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "a GPU is required"
+    torch.cuda.init()
+    return torch
+
+
+def _check_tiles(S, o, wl, tiles, group_cache=None):
+    """Compares the kernel's values over the listed tiles with the oracle's dump of their groups."""
+    got = S.debug_eval_tiles(tiles)
+    nb = wl["space"]["n_buckets"]
+    keys = o.group_keys()
+    row = 0
+    cache = {} if group_cache is None else group_cache
+    for t in tiles:
+        info = S.tile_info(int(t))
+        g = info["group"]
+        if g not in cache:
+            if len(cache) >= 4:
+                cache.clear()
+            cache[g] = o.dump(g, g + 1)
+        ref = cache[g]
+        lo = info["first_id"] - keys[g]["base"]
+        n = info["n_configs"]
+        want = ref[lo:lo + n]
+        have = got[row:row + n]
+        row += n
+        bad = np.flatnonzero(np.any(have[:, :4] != want[:, :4], axis=1))
+        assert bad.size == 0, "tile %d, config %d: kernel %s, oracle %s" % (
+            t, info["first_id"] + bad[0], have[bad[0]].tolist(), want[bad[0]].tolist())
+        feasible = want[:, 4] >= 0
+        assert np.array_equal(have[feasible, 4], want[feasible, 4]), "tile %d: buckets differ" % t
+        assert np.all((have[~feasible, 4] >= nb) & (have[~feasible, 4] <= 64)), "tile %d: infeasible off sink" % t
+    assert row == len(got)
+
+
+def _unit_factors(wl):
+    for h in wl["hws"]:
+        h["phi"] = [[1.0] * 4 for _ in range(16)]
+    return wl
+
+
+def _large_factors(wl, seed):
+    """Slowdown factors up to 50 (far above the seeded ones), for rounds whose scaled times
+    cross differently."""
+    rng = np.random.default_rng(seed)
+    for h in wl["hws"]:
+        h["phi"] = [[float(x) for x in 1.0 + 49.0 * rng.random(4) ** 3] for _ in range(16)]
+    return wl
+
+
+@pytest.mark.parametrize("name, mod", [
+    ("tiny", None), ("tiny_llama", None), ("tiny", "unit"), ("tiny_llama", "unit"),
+    ("tiny", "large"), ("tiny_llama", "large"), ("gpt1.3b-d8", None), ("gpt1.3b-d8", "unit"),
+])
+def test_every_tile_small(name, mod, torch_cuda):
+    from paper_2503_19050_amd import mist
+    wl = W.workload(name)
+    if mod == "unit":
+        wl = _unit_factors(wl)
+    elif mod == "large":
+        wl = _large_factors(wl, 7)
+    say("kernel dump", name, mod)
+    S = mist.from_workload(wl)
+    o = O.Oracle(wl)
+    n_tiles = S.launch_info()["tiles"]
+    cache = {}
+    for lo in range(0, n_tiles, 512):
+        _check_tiles(S, o, wl, list(range(lo, min(n_tiles, lo + 512))), cache)
+    S.close()
+
+
+@pytest.mark.parametrize("name, n", [("gpt2.7b-d16", 160), ("llama7b-d32", 24), ("llama42b-d128-hw64", 24)])
+def test_sampled_tiles_full_size(name, n, torch_cuda):
+    """Full-size spaces in the benchmark's launch configuration: the first and the last tile (a
+    small tail tile) and seeded random ones."""
+    from paper_2503_19050_amd import mist
+    wl = W.workload(name)
+    say("kernel dump", name)
+    S = mist.from_workload(wl)
+    o = O.Oracle(wl)
+    n_tiles = S.launch_info()["tiles"]
+    rng = np.random.default_rng(11)
+    # Full-size tiles come first in the tile table, then every group's small tail tiles.
+    picks = {0, n_tiles - 1} | set(int(t) for t in rng.integers(0, n_tiles, size=n))
+    tiles = sorted(picks, key=lambda t: (S.tile_info(t)["group"], t))   # one oracle group dump at a time
+    _check_tiles(S, o, wl, tiles)
+    S.close()
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_spaces(seed, torch_cuda):
+    from paper_2503_19050_amd import mist
+    wl = W.random_space(seed)
+    o = O.Oracle(wl)
+    if o.n_configs == 0 or o.n_configs > 400_000:
+        pytest.skip("empty or large random space")
+    if seed % 3 == 1:
+        wl = _unit_factors(wl)
+        o = O.Oracle(wl)
+    say("kernel dump random", seed, o.n_configs)
+    S = mist.from_workload(wl)
+    n_tiles = S.launch_info()["tiles"]
+    _check_tiles(S, o, wl, list(range(n_tiles)), {})
+    S.close()
