@@ -370,6 +370,20 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
+// Words that other lanes of the wave update with atomics are read and written with relaxed
+// wavefront-scope atomics: a plain load after a lane's own atomic update could otherwise be
+// answered from a value the compiler already holds (for an entry at a wave-uniform address the
+// compiler combines the lanes' atomic minima into one update by one lane).
+template <class T>
+__device__ __forceinline__ T lds_load(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
+
+template <class T>
+__device__ __forceinline__ void lds_store(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
+
 // Activation ratios per block of the strip loop: a block keeps its stable times and the
 // per-ratio terms of its configurations in registers across the optimizer ratios.
 template <int R>
@@ -608,11 +622,11 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
               const unsigned long long k_old = up ? k_hi : k_lo;
               BucketEntry* const be = reinterpret_cast<BucketEntry*>(b0 + (up ? sizeof(BucketEntry) : 0));
               const unsigned int lid = lid_oo + (unsigned int)ia;
-              const unsigned int i_old = be->lid;
+              const unsigned int i_old = lds_load(&be->lid);
               const bool cand = (key < k_old) | ((key == k_old) & (lid < i_old));
               if (cand) atomicMin(&be->key, key);
-              const unsigned long long k_new = cand ? be->key : 0ull;
-              if (cand && k_new < k_old) be->lid = 0xFFFFFFFFu;
+              const unsigned long long k_new = cand ? lds_load(&be->key) : 0ull;
+              if (cand && k_new < k_old) lds_store(&be->lid, 0xFFFFFFFFu);
               if (cand && key == k_new) atomicMin(&be->lid, lid);
             }
 
@@ -632,7 +646,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
 #pragma unroll 1
             for (int q = 0; q < a.n_alpha; ++q) {
               const double2 ab = s_ab[wave][q];
-              const double cur = s_aent[wave][q].val;
+              const double cur = lds_load(&s_aent[wave][q].val);
               bool any = false;
 #pragma unroll
               for (int c = 0; c < IB; ++c) {
@@ -653,19 +667,19 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
                   if (ia >= R) break;
                   const double v = __builtin_fma(ab.x, tt[c], ab.y * dn_blk[c]);
                   wave_sync();
-                  const double cur = e->val;
+                  const double cur = lds_load(&e->val);
                   if (__builtin_amdgcn_ballot_w64(v <= cur)) {
                     const unsigned int lid = lid_oo + (unsigned int)ia;
                     const unsigned long long ak = order_key(v);
-                    const unsigned long long ak_old = e->key;
-                    const unsigned int ai_old = e->lid;
+                    const unsigned long long ak_old = lds_load(&e->key);
+                    const unsigned int ai_old = lds_load(&e->lid);
                     const bool cand = (v <= cur) & ((ak < ak_old) | ((ak == ak_old) & (lid < ai_old)));
                     if (cand) atomicMin(&e->key, ak);
-                    const unsigned long long ak_new = cand ? e->key : 0ull;
-                    if (cand && ak_new < ak_old) e->lid = 0xFFFFFFFFu;
+                    const unsigned long long ak_new = cand ? lds_load(&e->key) : 0ull;
+                    if (cand && ak_new < ak_old) lds_store(&e->lid, 0xFFFFFFFFu);
                     if (cand && ak == ak_new) {
                       atomicMin(&e->lid, lid);
-                      e->val = v;
+                      lds_store(&e->val, v);
                     }
                   }
                 }
