@@ -324,12 +324,12 @@ __global__ __launch_bounds__(256) void k_pairs(EvalArgs a) {
 // as the tile's partials.
 // ---------------------------------------------------------------------------------------
 struct BucketEntry {
+  double edge;             // the bucket's upper memory edge E_j (+inf past NB - 1): the edge
+                           // and the key are adjacent, read together
   unsigned long long key;  // bits of the minimum objective (a non-negative double orders like
                            // its bit pattern)
   unsigned int lid;        // lowest local id (id - group base, < 2^32) reaching it
   unsigned int pad;
-  double edge;             // the bucket's upper memory edge E_j (+inf past NB - 1): one
-                           // address serves the edge test and the entry
 };
 static_assert(sizeof(BucketEntry) == 24, "24-byte entries: the entry offset is one multiply-add");
 
@@ -461,6 +461,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
     bucket[lane].key = lane < NB ? kEmpty : 0ull;
     bucket[lane].lid = lane < NB ? 0xFFFFFFFFu : 0u;
     if (lane == 0) {
+      bucket[64].edge = __builtin_huge_val();
       bucket[64].key = 0ull;
       bucket[64].lid = 0u;
     }
@@ -562,11 +563,16 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             // Bucket j = min{j : mem <= E_j}: floor(mem * kNB) is j or j - 1 (kNB carries a
             // 2^-40 margin), so one comparison with E settles it.  An infeasible
             // configuration (Eq. 4: mem > M = E_{NB-1}) has floor(mem * kNB) >= NB - 1 and
-            // lands on a sink: past NB - 1 the edges are +inf.
-            const int j0 = (int)__builtin_fmin(mem * kNB, 63.0);
+            // lands on a sink: past NB - 1 the edges are +inf.  j0 = j - 1 needs mem within a
+            // relative 2^-40 above an edge, or an infeasible mem just above M: rare, so only
+            // entry j0's edge and key are read, and entry j0 + 1 (<= 64: entry 64's edge is
+            // +inf) only by lanes whose mem exceeds E_j0.
+            const int j0 = (int)__builtin_fmin(mem * kNB, 64.0);
             const unsigned int off0 = __umul24((unsigned int)j0, (unsigned int)sizeof(BucketEntry));
             char* const b0 = reinterpret_cast<char*>(bucket) + off0;
+            wave_sync();  // read the entry after every earlier update of the wave
             const double e0 = reinterpret_cast<const BucketEntry*>(b0)->edge;
+            const unsigned long long k_lo = reinterpret_cast<const BucketEntry*>(b0)->key;
             if constexpr (DM) {
               double* o = a.dump + 5 * (a.dump_off[x] + (int64_t)(s - tile.strip_begin) * R2 + io * R + ia);
               o[0] = tv;
@@ -607,20 +613,14 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             // of a wave execute in program order and each step addresses the same words as
             // the one before, so each step sees the previous one's result.
             const unsigned long long key = (unsigned long long)__double_as_longlong(obj);
-            wave_sync();  // read the entry after every earlier update of the wave
-            // Both candidate entries' keys in one LDS round trip (entry 64 exists: a sink).
-            const unsigned long long k_lo = reinterpret_cast<const BucketEntry*>(b0)->key;
-            const unsigned long long k_hi = reinterpret_cast<const BucketEntry*>(b0 + sizeof(BucketEntry))->key;
             // A candidate beats the entry: key < k_old, or an equal key with a lower id.  No
-            // lane with key > k_old is one, so the exact test waits for a lane with key <= k_old.
-            // The two comparisons and the edge test are combined as wave masks (scalar ALU)
-            // instead of selecting k_old first.
+            // lane with key > k_old is one, so the exact test waits for a lane with key <= k_old
+            // or a lane in entry j0 + 1 (combined as wave masks by the scalar ALU).
             const unsigned long long m_up = __builtin_amdgcn_ballot_w64(up);
             const unsigned long long m_lo = __builtin_amdgcn_ballot_w64(key <= k_lo);
-            const unsigned long long m_hi = __builtin_amdgcn_ballot_w64(key <= k_hi);
-            if ((m_lo & ~m_up) | (m_hi & m_up)) {
-              const unsigned long long k_old = up ? k_hi : k_lo;
+            if (m_lo | m_up) {
               BucketEntry* const be = reinterpret_cast<BucketEntry*>(b0 + (up ? sizeof(BucketEntry) : 0));
+              const unsigned long long k_old = up ? lds_load(&be->key) : k_lo;
               const unsigned int lid = lid_oo + (unsigned int)ia;
               const unsigned int i_old = lds_load(&be->lid);
               const bool cand = (key < k_old) | ((key == k_old) & (lid < i_old));
