@@ -290,6 +290,17 @@ mist_status mist_decode(const mist_space* S, uint64_t id, mist_config* out);
 mist_status mist_eval_ids(mist_space* S, const uint64_t* ids, int64_t n, double* out,
                           void* hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): mist_eval_ids without any allocation.  The ids and
+ * results pass through a fixed 4 MiB device array of the library (one per GPU, held until the
+ * process ends), so n is at most 104,857 per call; the space's device must be current.  It
+ * calls no hipMalloc or hipFree (the host-to-device and device-to-host copies use the HIP
+ * runtime's own staging for pageable host memory).  Calls that overlap on one GPU share the
+ * array and race: issue them one at a time per GPU.  Synchronous on hip_stream.
+ * Errors: MIST_E_INVALID (null argument, another device current), MIST_E_RANGE (more ids than
+ * the array holds, or an id >= the number of configurations), MIST_E_DEVICE. */
+mist_status mist_eval_ids_noalloc(mist_space* S, const uint64_t* ids, int64_t n, double* out, void* hip_stream);
+
 /* Kernel timing.  mist_set_timing(S, 1) waits for pending work and starts recording HIP
  * events around the two kernels of every later mist_eval_space, on the evaluation stream;
  * mist_read_timing waits for the recorded evaluations and returns the summed durations (ms)

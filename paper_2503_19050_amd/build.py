@@ -16,7 +16,7 @@ LIB = os.path.join(PKG, "libmist.so")
 SOURCES = [os.path.join(CSRC, "mist_host.cpp"), os.path.join(CSRC, "mist_plan.cpp"),
            os.path.join(CSRC, "mist_calib.cpp"), os.path.join(CSRC, "mist_kernels.hip"),
            os.path.join(CSRC, "mist_exact.hip"), os.path.join(CSRC, "mist_corun.hip"),
-           os.path.join(CSRC, "mist_probe.hip")]
+           os.path.join(CSRC, "mist_probe.hip"), os.path.join(CSRC, "mist_noalloc.hip")]
 LIBS = ["-lrocblas"]  # the calibration's GEMMs
 HEADERS = [os.path.join(CSRC, "mist_internal.h"), os.path.join(INCLUDE, "mist.h")]
 

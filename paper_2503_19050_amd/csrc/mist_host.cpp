@@ -105,6 +105,7 @@ struct mist_space {
   double* d_alpha_obj = nullptr;
   uint64_t* d_alpha_id = nullptr;
   int32_t cus = 0;
+  int32_t device = 0;  // the HIP device the space was created on
   // exact frontier (mist_eval_pareto_exact)
   bool exact_done = false;
   bool exact_launched = false;  // some call enqueued uploads of the host offset tables
@@ -713,6 +714,7 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
       resident_blocks = std::max<int64_t>(1, (int64_t)cus * (per_cu > 0 ? per_cu : 1));
       if (S->max_blocks > 0) resident_blocks = std::min<int64_t>(resident_blocks, S->max_blocks);
       S->cus = cus;
+      S->device = dev;
     }
     if (!rc) {
       const std::string terr = build_tiles(S, resident_blocks * kWaves);
@@ -1302,6 +1304,39 @@ mist_status mist_eval_ids(mist_space* S, const uint64_t* ids, int64_t n, double*
   } catch (const std::bad_alloc&) {
     return fail(MIST_E_NOMEM, "host allocation failed");
   }
+}
+
+mist_status mist_eval_ids_noalloc(mist_space* S, const uint64_t* ids, int64_t n, double* out, void* hip_stream) {
+  if (!S || ((!ids || !out) && n > 0) || n < 0) return fail(MIST_E_INVALID, "null argument");
+  if (n > kNoAllocMaxIds)
+    return fail(MIST_E_RANGE, "mist_eval_ids_noalloc: at most " + std::to_string(kNoAllocMaxIds) +
+                                  " ids per call (a fixed 4 MiB device scratch)");
+  if (n == 0) return MIST_OK;
+  for (int64_t i = 0; i < n; ++i)
+    if (ids[i] >= S->n_configs) return fail(MIST_E_RANGE, "id out of range");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+  if (dev != S->device) return fail(MIST_E_INVALID, "the space's device must be the current device");
+  void* scratch = nullptr;
+  const int rc = noalloc_scratch(&scratch);
+  if (rc) return fail_hip((hipError_t)rc, "device scratch address");
+  // Layout: ids [n] uint64, then results [n][4] doubles (8-byte aligned).  Both are written in
+  // full before they are read, so nothing needs clearing.
+  uint64_t* d_ids = (uint64_t*)scratch;
+  double* d_out = (double*)((char*)scratch + (size_t)n * sizeof(uint64_t));
+  hipStream_t st = (hipStream_t)hip_stream;
+  e = copy_async(d_ids, ids, (size_t)n * sizeof(uint64_t), hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync ids");
+  const int k = launch_eval_ids(eval_args(S), d_ids, n, d_out, st);
+  if (k) {
+    (void)hipStreamSynchronize(st);
+    return fail_hip((hipError_t)k, "eval_ids launch");
+  }
+  e = copy_async(out, d_out, (size_t)n * 4 * sizeof(double), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return fail_hip(e, "mist_eval_ids_noalloc results");
+  return MIST_OK;
 }
 
 mist_status mist_set_timing(mist_space* S, int32_t on) {

@@ -157,6 +157,13 @@ struct ReduceArgs {
   uint64_t* alpha_id;    // [n_groups][n_alpha]
 };
 
+// Allocation-free per-id evaluation (mist_eval_ids_noalloc): a fixed device scratch array of
+// this many bytes holds the ids and the results of one call (40 bytes per id).
+constexpr size_t kNoAllocScratchBytes = (size_t)4 << 20;
+constexpr int64_t kNoAllocMaxIds = (int64_t)(kNoAllocScratchBytes / (sizeof(uint64_t) + 4 * sizeof(double)));
+// The current device's address of that array (mist_noalloc.hip); 0 or a hipError_t.
+int noalloc_scratch(void** ptr);
+
 // Kernel launchers (mist_kernels.hip).
 int launch_pairs(const EvalArgs& a, void* stream);
 int launch_eval(const EvalArgs& a, int blocks, int mode, void* stream);

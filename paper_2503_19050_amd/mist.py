@@ -28,7 +28,7 @@ EXPORTS = [
     "mist_plan_points", "mist_plan_pipeline", "mist_eval_pareto_exact", "mist_get_pareto_exact", "mist_exact_info",
     "mist_corun_create", "mist_corun_run", "mist_corun_reduce", "mist_corun_measure", "mist_corun_destroy",
     "mist_fit_phi", "mist_interference", "mist_measure_eta", "mist_probe_fp64",
-    "mist_tile_info", "mist_debug_eval_tiles",
+    "mist_tile_info", "mist_debug_eval_tiles", "mist_eval_ids_noalloc",
 ]
 
 PROBE_KINDS = {"add": 0, "mul": 1, "fma": 2, "min": 3, "max": 4, "cmp": 5}
@@ -153,6 +153,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         L.mist_get_group_key.argtypes = [vp, ctypes.c_int64, P(GroupKey)]
         L.mist_decode.argtypes = [vp, ctypes.c_uint64, P(Config)]
         L.mist_eval_ids.argtypes = [vp, P(ctypes.c_uint64), ctypes.c_int64, P(ctypes.c_double), vp]
+        L.mist_eval_ids_noalloc.argtypes = [vp, P(ctypes.c_uint64), ctypes.c_int64, P(ctypes.c_double), vp]
         L.mist_set_timing.argtypes = [vp, ctypes.c_int32]
         L.mist_read_timing.argtypes = [vp, P(ctypes.c_double), P(ctypes.c_double), P(ctypes.c_int64)]
         L.mist_launch_info.argtypes = [vp, P(ctypes.c_int64), P(ctypes.c_int32), P(ctypes.c_int32)]
@@ -374,6 +375,15 @@ class Space:
         _check(self.L, self.L.mist_eval_ids(self.h, ids.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)),
                                             len(ids), out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
                                             ctypes.c_void_p(_stream_handle(stream))))
+        return out
+
+    def eval_ids_noalloc(self, ids, stream=None) -> np.ndarray:
+        """eval_ids through the allocation-free entry point (at most 104,857 ids per call)."""
+        ids = np.ascontiguousarray(ids, dtype=np.uint64)
+        out = np.empty((len(ids), 4), dtype=np.float64)
+        _check(self.L, self.L.mist_eval_ids_noalloc(self.h, ids.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)),
+                                                    len(ids), out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                                    ctypes.c_void_p(_stream_handle(stream))))
         return out
 
     def tile_info(self, t: int) -> dict:
