@@ -118,8 +118,10 @@ typedef struct mist_space_desc {
                             device at once) */
   int32_t cand_window;   /* exact frontier, results do not depend on it: each tile first writes
                             its candidates to a window of ceil(configurations / cand_window)
-                            slots, and a tile with more is evaluated a second time (0: 8, raised
-                            as needed to keep all windows within 2^27 slots) */
+                            slots (0: 8, raised as needed to keep all windows within 2^27 slots),
+                            the rest to an overflow pool of half as many slots as all windows
+                            (at most 2^26); a tile with a candidate that finds no place is
+                            evaluated a second time */
 } mist_space_desc;
 
 /* Device memory provider, e.g. PyTorch's caching allocator.  alloc returns NULL on
@@ -246,9 +248,9 @@ mist_status mist_plan_pipeline(mist_space* S, int32_t hw, int32_t pp, mist_plan*
  * mist_eval_space, finds for each group the feasible configurations whose obj is strictly
  * below that of every configuration before them in (mem, obj, id) order.  A candidate pass
  * keeps only configurations that beat every lower bucket's minimum and are not dominated by
- * their bucket's winner (each tile writes them to a window of its own and counts them; tiles
- * with more than their window holds are evaluated a second time, see cand_window); they are
- * sorted by memory per group and scanned.  Waits for the evaluation and once more for the
+ * their bucket's winner (each tile writes them to a window of its own, the rest to a shared
+ * overflow pool, and counts them; a tile whose candidates do not all find a place is evaluated
+ * a second time, see cand_window); they are sorted by memory per group and scanned.  Waits for the evaluation and once more for the
  * candidate counts, then enqueues the rest on hip_stream.
  * Errors: MIST_E_STATE (no evaluation yet), MIST_E_RANGE (2^32 candidates or more),
  * MIST_E_NOMEM, MIST_E_DEVICE. */
@@ -262,10 +264,16 @@ mist_status mist_get_pareto_exact(mist_space* S, int64_t g, mist_result* out, in
 /* Sizes of the last exact frontier, for diagnostics and measurement: the candidates of the
  * candidate pass (all groups), those the pre-filter kept, the tiles the candidate pass
  * evaluated (those that may hold a candidate) and the tiles evaluated a second time because
- * their candidates overflowed their window.  Waits for mist_eval_pareto_exact; any pointer may
+ * a candidate found no place in its window or the overflow pool.  Waits for mist_eval_pareto_exact; any pointer may
  * be NULL.  Errors: MIST_E_INVALID, MIST_E_STATE, MIST_E_DEVICE, MIST_E_NOMEM. */
 mist_status mist_exact_info(mist_space* S, int64_t* n_candidates, int64_t* n_kept, int32_t* n_tiles_live,
                             int32_t* n_tiles_again);
+
+/* Per-group sizes of the last exact frontier, groups g0..g0+n-1: host candidates[i] (the
+ * candidate pass's configurations of the group) and host kept[i] (those the pre-filter kept for
+ * the sort and scan); either pointer may be NULL.  Waits for mist_eval_pareto_exact.
+ * Errors: MIST_E_INVALID, MIST_E_STATE, MIST_E_RANGE, MIST_E_DEVICE, MIST_E_NOMEM. */
+mist_status mist_exact_group_sizes(mist_space* S, int64_t g0, int64_t n, int64_t* candidates, int64_t* kept);
 
 /* Raw per-bucket table of groups g0..g0+n-1: host ids[n*NB] and objs[n*NB] (MIST_NONE /
  * +inf for empty buckets) and host frontier masks[n] (bit j = bucket j on the staircase);

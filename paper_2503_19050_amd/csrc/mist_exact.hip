@@ -367,25 +367,49 @@ __global__ __launch_bounds__(256) void k_prefilter(uint64_t* __restrict__ key, d
   if (tid == 0) seg_end[g] = wp;
 }
 
-// One wave per tile: its window's candidates, in order, to the tile's place in group order.
+// One wave per tile: its window's candidates (its first ones, in order) to the tile's place in
+// group order; the rest of an overflowing tile comes from the pool.
 __global__ __launch_bounds__(256) void k_compact(const uint64_t* __restrict__ slab_key,
                                                  const double* __restrict__ slab_obj,
                                                  const uint64_t* __restrict__ slab_id,
                                                  const int64_t* __restrict__ slab_begin,
                                                  const int32_t* __restrict__ cnt,
+                                                 const uint8_t* __restrict__ tile_drop,
                                                  const int64_t* __restrict__ tile_off, int32_t n_tiles,
                                                  uint64_t* __restrict__ cand_key, double* __restrict__ cand_obj,
                                                  uint64_t* __restrict__ cand_id) {
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= n_tiles) return;
-  const int64_t src = slab_begin[t], n = cnt[t], dst = tile_off[t];
-  if (n > slab_begin[t + 1] - src) return;  // overflowed: the tile is evaluated again
+  if (tile_drop[t]) return;  // a candidate found no place: the tile is evaluated again
+  const int64_t src = slab_begin[t], dst = tile_off[t];
+  const int64_t win = slab_begin[t + 1] - src;
+  const int64_t n = cnt[t] < win ? (int64_t)cnt[t] : win;
   for (int64_t i = lane; i < n; i += 64) {
     cand_key[dst + i] = slab_key[src + i];
     cand_obj[dst + i] = slab_obj[src + i];
     cand_id[dst + i] = slab_id[src + i];
   }
+}
+
+// One thread per pool slot: the overflowing candidate to its tile's place plus its rank.
+__global__ __launch_bounds__(256) void k_pool_place(const uint64_t* __restrict__ pool_key,
+                                                    const double* __restrict__ pool_obj,
+                                                    const uint64_t* __restrict__ pool_id,
+                                                    const int32_t* __restrict__ pool_tile,
+                                                    const int32_t* __restrict__ pool_rank, int64_t n,
+                                                    const uint8_t* __restrict__ tile_drop,
+                                                    const int64_t* __restrict__ tile_off,
+                                                    uint64_t* __restrict__ cand_key, double* __restrict__ cand_obj,
+                                                    uint64_t* __restrict__ cand_id) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= n) return;
+  const int32_t t = pool_tile[p];
+  if (tile_drop[t]) return;
+  const int64_t dst = tile_off[t] + pool_rank[p];
+  cand_key[dst] = pool_key[p];
+  cand_obj[dst] = pool_obj[p];
+  cand_id[dst] = pool_id[p];
 }
 
 int last_error() {
@@ -417,11 +441,21 @@ int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_in, ui
 }
 
 int launch_compact(const uint64_t* slab_key, const double* slab_obj, const uint64_t* slab_id,
-                   const int64_t* slab_begin, const int32_t* cnt, const int64_t* tile_off, int32_t n_tiles,
-                   uint64_t* cand_key, double* cand_obj, uint64_t* cand_id, void* stream) {
+                   const int64_t* slab_begin, const int32_t* cnt, const uint8_t* tile_drop, const int64_t* tile_off,
+                   int32_t n_tiles, uint64_t* cand_key, double* cand_obj, uint64_t* cand_id, void* stream) {
   if (n_tiles <= 0) return 0;
   hipLaunchKernelGGL(k_compact, dim3((unsigned)((n_tiles + 3) / 4)), dim3(256), 0, (hipStream_t)stream, slab_key,
-                     slab_obj, slab_id, slab_begin, cnt, tile_off, n_tiles, cand_key, cand_obj, cand_id);
+                     slab_obj, slab_id, slab_begin, cnt, tile_drop, tile_off, n_tiles, cand_key, cand_obj, cand_id);
+  return last_error();
+}
+
+int launch_pool_place(const uint64_t* pool_key, const double* pool_obj, const uint64_t* pool_id,
+                      const int32_t* pool_tile, const int32_t* pool_rank, int64_t n, const uint8_t* tile_drop,
+                      const int64_t* tile_off, uint64_t* cand_key, double* cand_obj, uint64_t* cand_id,
+                      void* stream) {
+  if (n <= 0) return 0;
+  hipLaunchKernelGGL(k_pool_place, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, (hipStream_t)stream, pool_key,
+                     pool_obj, pool_id, pool_tile, pool_rank, n, tile_drop, tile_off, cand_key, cand_obj, cand_id);
   return last_error();
 }
 

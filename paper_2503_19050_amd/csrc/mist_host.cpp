@@ -47,6 +47,7 @@ constexpr int64_t kMaxTiles = 131072;         // and tiles per space, at most
 constexpr int64_t kWindowDiv = 8;             // exact frontier: candidate window of a tile,
                                               // 1/kWindowDiv of its configurations
 constexpr int64_t kWindowSlots = (int64_t)1 << 27;  // and all windows together, at most
+constexpr int64_t kPoolSlots = (int64_t)1 << 26;    // overflow pool of the candidate pass, at most
 constexpr int64_t kTailPercent = 10;          // share of each group's strips in small tiles
 constexpr int64_t kStripAlign = kWaveTile;    // strips per tile: a multiple of the wave
 
@@ -116,6 +117,16 @@ struct mist_space {
   int64_t* d_tile_end = nullptr;
   int32_t* d_list = nullptr;
   uint8_t* d_live = nullptr;  // per tile: may hold a candidate
+  // Overflow pool of the candidate pass: candidates past their tile's window.
+  unsigned long long* d_pool_count = nullptr;
+  int64_t pool_cap = 0;
+  uint64_t *d_pool_key = nullptr, *d_pool_id = nullptr;
+  double* d_pool_obj = nullptr;
+  int32_t *d_pool_tile = nullptr, *d_pool_rank = nullptr;
+  uint8_t* d_tile_drop = nullptr;  // per tile: a candidate found no place (evaluated again)
+  uint8_t* h_drop = nullptr;
+  unsigned long long* h_pool_count = nullptr;
+  int64_t n_pooled = 0;  // candidates the last call placed through the pool
   // Candidate windows: tile t writes to slots [slab_begin[t], slab_begin[t+1]) first.
   std::vector<int64_t> h_slab_begin;
   int64_t* d_slab_begin = nullptr;
@@ -891,8 +902,18 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       S->d_slab_key = (uint64_t*)dev_alloc(S, n_slab * 8);
       S->d_slab_obj = (double*)dev_alloc(S, n_slab * 8);
       S->d_slab_id = (uint64_t*)dev_alloc(S, n_slab * 8);
+      // The pool holds half as many slots as all windows together (at most kPoolSlots).
+      S->pool_cap = std::min<int64_t>(kPoolSlots, std::max<int64_t>((int64_t)n_slab / 2, 1));
+      const size_t n_pool = (size_t)S->pool_cap;
+      S->d_pool_count = (unsigned long long*)dev_alloc(S, 256);
+      S->d_pool_key = (uint64_t*)dev_alloc(S, n_pool * 8);
+      S->d_pool_obj = (double*)dev_alloc(S, n_pool * 8);
+      S->d_pool_id = (uint64_t*)dev_alloc(S, n_pool * 8);
+      S->d_pool_tile = (int32_t*)dev_alloc(S, n_pool * 4);
+      S->d_pool_rank = (int32_t*)dev_alloc(S, n_pool * 4);
+      S->d_tile_drop = (uint8_t*)dev_alloc(S, std::max<size_t>(nt, 1));
       {
-        const size_t bytes = 8 * (2 * nt + ng + 1) + 4 * (2 * nt) + 64;
+        const size_t bytes = 8 * (2 * nt + ng + 1) + 4 * (2 * nt) + 64 + 8 + nt;
         void* p = nullptr;
         if (hipHostMalloc(&p, bytes, hipHostMallocDefault) != hipSuccess) p = nullptr;
         S->h_pinned = p;
@@ -903,12 +924,16 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
           S->h_seg = S->h_tile_end + nt;
           S->h_cnt = (int32_t*)(S->h_seg + ng + 1);
           S->h_list = S->h_cnt + nt;
+          S->h_pool_count = (unsigned long long*)(S->h_list + nt + 16);  // 8-byte aligned: nt ints + 64 B
+          S->h_drop = (uint8_t*)(S->h_pool_count + 1);
         }
       }
       void** bufs[] = {(void**)&S->d_filt,      (void**)&S->d_cnt_tile,   (void**)&S->d_tile_off,
                        (void**)&S->d_tile_end,  (void**)&S->d_list,       (void**)&S->d_seg, (void**)&S->d_seg_end, (void**)&S->d_live,
                        (void**)&S->d_front_cnt, (void**)&S->d_slab_begin, (void**)&S->d_slab_key,
-                       (void**)&S->d_slab_obj,  (void**)&S->d_slab_id};
+                       (void**)&S->d_slab_obj,  (void**)&S->d_slab_id,    (void**)&S->d_pool_count,
+                       (void**)&S->d_pool_key,  (void**)&S->d_pool_obj,   (void**)&S->d_pool_id,
+                       (void**)&S->d_pool_tile, (void**)&S->d_pool_rank,  (void**)&S->d_tile_drop};
       bool ok = S->h_pinned != nullptr;
       for (void** b : bufs) ok = ok && *b;
       if (!ok) {  // free what was allocated: the next call starts over
@@ -936,16 +961,27 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
     ea.cand_key = S->d_slab_key;
     ea.cand_obj = S->d_slab_obj;
     ea.cand_id = S->d_slab_id;
+    ea.pool_count = S->d_pool_count;
+    ea.pool_cap = S->pool_cap;
+    ea.pool_key = S->d_pool_key;
+    ea.pool_obj = S->d_pool_obj;
+    ea.pool_id = S->d_pool_id;
+    ea.pool_tile = S->d_pool_tile;
+    ea.pool_rank = S->d_pool_rank;
+    ea.tile_drop = S->d_tile_drop;
     int k = launch_filter(ea, S->d_bucket_obj, S->d_bucket_id, S->d_filt, st);
     if (!k) k = launch_live(ea, S->d_filt, S->d_live, st);
-    if (!k) k = launch_pairs(ea, st);  // also resets the tile counters
+    if (!k) k = launch_pairs(ea, st);  // also resets the tile counters and the pool
     if (!k) k = launch_eval(ea, mode_grid(S, kModeEmit), kModeEmit, st);
     if (k) return fail_hip((hipError_t)k, "exact frontier: candidates");
     hipError_t e = copy_async(S->h_cnt, S->d_cnt_tile, nt * sizeof(int32_t), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = copy_async(S->h_drop, S->d_tile_drop, nt, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = copy_async(S->h_pool_count, S->d_pool_count, 8, hipMemcpyDeviceToHost, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     if (e != hipSuccess) return fail_hip(e, "exact frontier: counts");
-    // Candidate slots in group order: a group's full-size tiles, then its small ones.  Tiles
-    // whose candidates overflowed their window are listed for pass 2.
+    const int64_t n_pool = std::min<int64_t>((int64_t)*S->h_pool_count, S->pool_cap);
+    // Candidate slots in group order: a group's full-size tiles, then its small ones.  Tiles with
+    // a candidate that found no place (its window and the pool full) are listed for pass 2.
     S->n_list = 0;
     int64_t off = 0;
     for (size_t t = 0; t < nt; ++t)
@@ -954,7 +990,7 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       S->h_tile_off[t] = off;
       off += S->h_cnt[t];
       S->h_tile_end[t] = off;
-      if (S->h_cnt[t] > S->h_slab_begin[t + 1] - S->h_slab_begin[t]) S->h_list[S->n_list++] = t;
+      if (S->h_drop[t]) S->h_list[S->n_list++] = t;
     };
     for (size_t g = 0; g < ng; ++g) {
       const DevGroup& G = S->groups[g];
@@ -1008,9 +1044,14 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
     if (e != hipSuccess) return fail_hip(e, "exact frontier: offsets");
     // The windows that held their tile's candidates move to group order; pass 2 evaluates the
     // listed tiles again, writing straight to their slots.
-    k = launch_compact(S->d_slab_key, S->d_slab_obj, S->d_slab_id, S->d_slab_begin, S->d_cnt_tile, S->d_tile_off,
-                       (int32_t)nt, S->d_cand_key, S->d_cand_obj, S->d_cand_id, st);
+    k = launch_compact(S->d_slab_key, S->d_slab_obj, S->d_slab_id, S->d_slab_begin, S->d_cnt_tile, S->d_tile_drop,
+                       S->d_tile_off, (int32_t)nt, S->d_cand_key, S->d_cand_obj, S->d_cand_id, st);
+    if (!k)
+      k = launch_pool_place(S->d_pool_key, S->d_pool_obj, S->d_pool_id, S->d_pool_tile, S->d_pool_rank, n_pool,
+                            S->d_tile_drop, S->d_tile_off, S->d_cand_key, S->d_cand_obj, S->d_cand_id, st);
     if (!k && n_list > 0) {
+      ea.pool_count = nullptr;  // exact slots: nothing overflows
+      ea.tile_drop = nullptr;
       ea.win_begin = S->d_tile_off;
       ea.win_end = S->d_tile_end;
       ea.tile_list = S->d_list;
@@ -1033,6 +1074,7 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
     if (k) return fail_hip((hipError_t)k, "exact frontier");
     S->n_cand = off;
     S->n_rerun = n_list;
+    S->n_pooled = n_pool;
     S->exact_done = true;
     S->exact_stream = st;
     return MIST_OK;
@@ -1064,6 +1106,27 @@ mist_status mist_exact_info(mist_space* S, int64_t* n_candidates, int64_t* n_kep
     if (n_kept) *n_kept = kept;
     if (n_tiles_live) *n_tiles_live = n_live;
     if (n_tiles_again) *n_tiles_again = S->n_rerun;
+    return MIST_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(MIST_E_NOMEM, "host allocation failed");
+  }
+}
+
+mist_status mist_exact_group_sizes(mist_space* S, int64_t g0, int64_t n, int64_t* candidates, int64_t* kept) {
+  if (!S) return fail(MIST_E_INVALID, "space is null");
+  if (!S->exact_done) return fail(MIST_E_STATE, "mist_eval_pareto_exact has not been called");
+  if (g0 < 0 || n < 0 || g0 + n > (int64_t)S->groups.size()) return fail(MIST_E_RANGE, "group range");
+  if (n == 0) return MIST_OK;
+  try {
+    std::vector<int64_t> seg((size_t)n + 1), end((size_t)n);
+    hipError_t e = hipStreamSynchronize(S->exact_stream);
+    if (e == hipSuccess) e = copy_sync(seg.data(), S->d_seg + g0, ((size_t)n + 1) * sizeof(int64_t), hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = copy_sync(end.data(), S->d_seg_end + g0, (size_t)n * sizeof(int64_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_hip(e, "exact frontier: group sizes");
+    for (int64_t i = 0; i < n; ++i) {
+      if (candidates) candidates[i] = seg[(size_t)i + 1] - seg[(size_t)i];
+      if (kept) kept[i] = end[(size_t)i] - seg[(size_t)i];
+    }
     return MIST_OK;
   } catch (const std::bad_alloc&) {
     return fail(MIST_E_NOMEM, "host allocation failed");

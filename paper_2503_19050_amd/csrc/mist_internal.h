@@ -131,6 +131,18 @@ struct EvalArgs {
   uint64_t* cand_key;        // memory bit patterns (a non-negative double orders like its bits)
   double* cand_obj;
   uint64_t* cand_id;
+  // Overflow pool of the first candidate pass (pool_count = nullptr: none).  A candidate past its
+  // tile's window takes the next pool slot from *pool_count (reset by the pair kernel) and
+  // stores itself with its tile and its rank among the tile's candidates; past pool_cap it is
+  // dropped and tile_drop[t] = 1 marks the tile for a second evaluation.
+  unsigned long long* pool_count;
+  int64_t pool_cap;
+  uint64_t* pool_key;
+  double* pool_obj;
+  uint64_t* pool_id;
+  int32_t* pool_tile;
+  int32_t* pool_rank;
+  uint8_t* tile_drop;        // [n_tiles]
   // Dump variant (parity checks): listed item x writes, for every configuration of its tile in
   // local-id order, t, d, mem, obj and the bucket entry the kernel chose (as a double; NB..64
   // are the sinks of infeasible configurations) to dump[5 * (dump_off[x] + i)..].
@@ -184,11 +196,16 @@ int launch_prefilter(uint64_t* cand_key, double* cand_obj, uint64_t* cand_id, co
 int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_in, uint32_t* idx_out, int64_t n,
                int64_t n_groups, const int64_t* seg_begin, const int64_t* seg_end, void* temp, size_t* temp_bytes,
                void* stream);
-// Moves each tile's candidates from its window [slab_begin[t], slab_begin[t+1]) to
-// [tile_off[t], tile_off[t] + cnt[t]); tiles whose count exceeds the window are skipped.
+// Moves each tile's window [slab_begin[t], slab_begin[t+1]) (its first candidates, at most
+// cnt[t]) to [tile_off[t], ...); tiles with tile_drop[t] set are skipped (evaluated again).
 int launch_compact(const uint64_t* slab_key, const double* slab_obj, const uint64_t* slab_id,
-                   const int64_t* slab_begin, const int32_t* cnt, const int64_t* tile_off, int32_t n_tiles,
-                   uint64_t* cand_key, double* cand_obj, uint64_t* cand_id, void* stream);
+                   const int64_t* slab_begin, const int32_t* cnt, const uint8_t* tile_drop, const int64_t* tile_off,
+                   int32_t n_tiles, uint64_t* cand_key, double* cand_obj, uint64_t* cand_id, void* stream);
+// Moves pool slots [0, n) to tile_off[pool_tile] + pool_rank (tiles with tile_drop set skipped).
+int launch_pool_place(const uint64_t* pool_key, const double* pool_obj, const uint64_t* pool_id,
+                      const int32_t* pool_tile, const int32_t* pool_rank, int64_t n, const uint8_t* tile_drop,
+                      const int64_t* tile_off, uint64_t* cand_key, double* cand_obj, uint64_t* cand_id,
+                      void* stream);
 int launch_front_scan(const uint32_t* order, const uint64_t* sorted_key, const double* cand_obj,
                       const uint64_t* cand_id, const int64_t* seg_begin, const int64_t* seg_end, int64_t n_groups,
                       uint64_t* front_key, double* front_obj, uint64_t* front_id, int64_t* front_cnt, void* stream);

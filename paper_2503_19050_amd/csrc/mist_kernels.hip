@@ -301,6 +301,7 @@ __global__ __launch_bounds__(256) void k_pairs(EvalArgs a) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < kClaimCounters) a.work[i * kCounterStride] = 0;  // the evaluation kernel's tile
                                                            // counters (it runs after this one)
+  if (i == 0 && a.pool_count) *a.pool_count = 0ull;       // and its candidate overflow pool
   if (i >= a.n_pk) return;
   const DevGroup g = a.groups[a.pk_group[i]];
   const int p = i - g.pk_begin;
@@ -469,6 +470,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
     int64_t n_cand = 0;  // exact frontier: the next candidate's slot
     int64_t n_beg = 0;   // and the tile's window of slots
     int64_t n_end = 0;
+    bool dropped = false;  // and whether a candidate of this lane found no place
     if constexpr (EX) {
       s_filt[wave][lane] = a.filt[(size_t)tile.group * 64 + lane];
       n_beg = a.win_begin[t];
@@ -591,14 +593,39 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
               const bool cand = (mem <= M) & (obj < f.pm) &
                                 !(((obj > f.bobj) & (mem >= f.bmem)) | ((obj >= f.bobj) & (mem > f.bmem)));
               const unsigned long long m = __builtin_amdgcn_ballot_w64(cand);
+              int64_t slot = 0;
+              const uint64_t cid = g.base + (uint64_t)(lid_oo + (unsigned int)ia);
               if (cand) {
                 const unsigned int below = __builtin_amdgcn_mbcnt_hi(
                     (unsigned int)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)m, 0u));
-                const int64_t slot = n_cand + below;
-                if (slot < n_end) {  // past the window: counted only
+                slot = n_cand + below;
+                if (slot < n_end) {
                   a.cand_key[slot] = (unsigned long long)__double_as_longlong(mem);
                   a.cand_obj[slot] = obj;
-                  a.cand_id[slot] = g.base + (uint64_t)(lid_oo + (unsigned int)ia);
+                  a.cand_id[slot] = cid;
+                }
+              }
+              // Past the window: the overflow pool (one device-wide atomic per wave and step),
+              // else counted only and the tile is evaluated again.
+              const bool over = cand && slot >= n_end;
+              const unsigned long long mo = __builtin_amdgcn_ballot_w64(over);
+              if (mo) {
+                const int leader = __builtin_ctzll(mo);
+                unsigned long long pbase = 0;
+                if (a.pool_count && lane == leader) pbase = atomicAdd(a.pool_count, (unsigned long long)__builtin_popcountll(mo));
+                pbase = __shfl(pbase, leader, 64);
+                if (over) {
+                  const unsigned long long pos = pbase + __builtin_amdgcn_mbcnt_hi(
+                      (unsigned int)(mo >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)mo, 0u));
+                  if (a.pool_count && pos < (unsigned long long)a.pool_cap) {
+                    a.pool_key[pos] = (unsigned long long)__double_as_longlong(mem);
+                    a.pool_obj[pos] = obj;
+                    a.pool_id[pos] = cid;
+                    a.pool_tile[pos] = t;
+                    a.pool_rank[pos] = (int32_t)(slot - n_beg);
+                  } else {
+                    dropped = true;
+                  }
                 }
               }
               n_cand += __builtin_popcountll(m);
@@ -695,6 +722,8 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
       // Saturated at 2^31 - 1, which the host rejects (no tile of a space with fewer than
       // 2^32 candidates reaches it).
       if (lane == 0) a.cnt_tile[t] = (int32_t)min(n_cand - n_beg, (int64_t)0x7FFFFFFF);
+      const unsigned long long md = __builtin_amdgcn_ballot_w64(dropped);
+      if (lane == 0 && a.tile_drop) a.tile_drop[t] = md ? 1 : 0;
     } else {
       wave_sync();
       const unsigned int bl = bucket[lane].lid;

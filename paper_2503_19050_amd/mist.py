@@ -28,7 +28,7 @@ EXPORTS = [
     "mist_plan_points", "mist_plan_pipeline", "mist_eval_pareto_exact", "mist_get_pareto_exact", "mist_exact_info",
     "mist_corun_create", "mist_corun_run", "mist_corun_reduce", "mist_corun_measure", "mist_corun_destroy",
     "mist_fit_phi", "mist_interference", "mist_measure_eta", "mist_probe_fp64",
-    "mist_tile_info", "mist_debug_eval_tiles", "mist_eval_ids_noalloc",
+    "mist_tile_info", "mist_debug_eval_tiles", "mist_eval_ids_noalloc", "mist_exact_group_sizes",
 ]
 
 PROBE_KINDS = {"add": 0, "mul": 1, "fma": 2, "min": 3, "max": 4, "cmp": 5}
@@ -160,6 +160,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         L.mist_space_destroy.argtypes = [vp]
         L.mist_eval_pareto_exact.argtypes = [vp, vp]
         L.mist_get_pareto_exact.argtypes = [vp, ctypes.c_int64, P(Result), ctypes.c_int64, P(ctypes.c_int64)]
+        L.mist_exact_group_sizes.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, P(ctypes.c_int64), P(ctypes.c_int64)]
         L.mist_exact_info.argtypes = [vp, P(ctypes.c_int64), P(ctypes.c_int64), P(ctypes.c_int32), P(ctypes.c_int32)]
         L.mist_plan_points.argtypes = [P(StagePoint), ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P(Plan)]
         L.mist_plan_pipeline.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, P(Plan)]
@@ -331,6 +332,15 @@ class Space:
                 continue
             _check(self.L, rc)
             return [_struct_to_dict(out[i]) for i in range(n.value)]
+
+    def exact_group_sizes(self, g0: int = 0, n: int | None = None) -> tuple[np.ndarray, np.ndarray]:
+        """Per-group candidates and pre-filter survivors of the last exact frontier."""
+        n = self.n_groups - g0 if n is None else n
+        c = np.zeros(max(n, 1), dtype=np.int64)
+        k = np.zeros(max(n, 1), dtype=np.int64)
+        P = ctypes.POINTER(ctypes.c_int64)
+        _check(self.L, self.L.mist_exact_group_sizes(self.h, g0, n, c.ctypes.data_as(P), k.ctypes.data_as(P)))
+        return c[:n], k[:n]
 
     def exact_info(self) -> dict:
         """Sizes of the last exact frontier: candidates, those the pre-filter kept, tiles the
