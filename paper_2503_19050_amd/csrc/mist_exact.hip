@@ -392,7 +392,8 @@ __global__ __launch_bounds__(256) void k_compact(const uint64_t* __restrict__ sl
   }
 }
 
-// One thread per pool slot: the overflowing candidate to its tile's place plus its rank.
+// One thread per pool slot: the overflowing candidate to its tile's place plus its rank (slots
+// that a wave's chunk left unused hold tile -1).
 __global__ __launch_bounds__(256) void k_pool_place(const uint64_t* __restrict__ pool_key,
                                                     const double* __restrict__ pool_obj,
                                                     const uint64_t* __restrict__ pool_id,
@@ -405,7 +406,7 @@ __global__ __launch_bounds__(256) void k_pool_place(const uint64_t* __restrict__
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= n) return;
   const int32_t t = pool_tile[p];
-  if (tile_drop[t]) return;
+  if (t < 0 || tile_drop[t]) return;  // an unused slot of a chunk, or a tile evaluated again
   const int64_t dst = tile_off[t] + pool_rank[p];
   cand_key[dst] = pool_key[p];
   cand_obj[dst] = pool_obj[p];

@@ -385,6 +385,23 @@ __device__ __forceinline__ void lds_store(T* p, T v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
 }
 
+// Overflow pool of the exact frontier's candidate pass: each wave takes chunks of kPoolChunk
+// slots; the slots of a chunk it leaves unused are marked (tile -1) so that the placement skips
+// them.
+constexpr int kPoolChunk = 256;
+
+__device__ __forceinline__ void pool_holes(const EvalArgs& a, unsigned long long base, int used, int lane) {
+  // The active lanes share the work (lanes past a ragged tile's last strip are inactive).
+  const unsigned long long ex = __builtin_amdgcn_read_exec();
+  const int n_act = __builtin_popcountll(ex);
+  const int r = (int)__builtin_amdgcn_mbcnt_hi((unsigned int)(ex >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)ex, 0u));
+  (void)lane;
+  for (int i = used + r; i < kPoolChunk; i += n_act) {
+    const unsigned long long pos = base + (unsigned long long)i;
+    if (pos < (unsigned long long)a.pool_cap) a.pool_tile[pos] = -1;
+  }
+}
+
 // Activation ratios per block of the strip loop: a block keeps its stable times and the
 // per-ratio terms of its configurations in registers across the optimizer ratios.
 template <int R>
@@ -443,6 +460,9 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
   int counter = (int)(blockIdx.x % kClaimCounters);
   int exhausted = 0;
   int loaded_hw = -1;
+  // Exact frontier: the wave's current chunk of overflow-pool slots (none yet: used = chunk).
+  unsigned long long pool_base = 0;
+  int pool_used = kPoolChunk;
   for (int x = (int)blockIdx.x * kWaves + wave; x < n_items;) {
     const int t = listed ? load_uniform(a.tile_list + x) : x;
     const DevTile tile = load_uniform(a.tiles + t);
@@ -605,19 +625,26 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
                   a.cand_id[slot] = cid;
                 }
               }
-              // Past the window: the overflow pool (one device-wide atomic per wave and step),
-              // else counted only and the tile is evaluated again.
+              // Past the window: the overflow pool, in chunks of kPoolChunk slots per wave (one
+              // device-wide atomic per chunk), else counted only and the tile is evaluated again.
               const bool over = cand && slot >= n_end;
               const unsigned long long mo = __builtin_amdgcn_ballot_w64(over);
-              if (mo) {
-                const int leader = __builtin_ctzll(mo);
-                unsigned long long pbase = 0;
-                if (a.pool_count && lane == leader) pbase = atomicAdd(a.pool_count, (unsigned long long)__builtin_popcountll(mo));
-                pbase = __shfl(pbase, leader, 64);
+              if (mo && a.pool_count) {
+                const int k = __builtin_popcountll(mo);
+                if (pool_used + k > kPoolChunk) {
+                  pool_holes(a, pool_base, pool_used, lane);
+                  const int leader = __builtin_ctzll(mo);
+                  unsigned long long b = 0;
+                  if (lane == leader) b = atomicAdd(a.pool_count, (unsigned long long)kPoolChunk);
+                  const unsigned long long bb = __shfl(b, leader, 64);
+                  pool_base = ((unsigned long long)__builtin_amdgcn_readfirstlane((unsigned int)(bb >> 32)) << 32) |
+                              (unsigned long long)__builtin_amdgcn_readfirstlane((unsigned int)bb);
+                  pool_used = 0;
+                }
                 if (over) {
-                  const unsigned long long pos = pbase + __builtin_amdgcn_mbcnt_hi(
+                  const unsigned long long pos = pool_base + (unsigned long long)pool_used + __builtin_amdgcn_mbcnt_hi(
                       (unsigned int)(mo >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)mo, 0u));
-                  if (a.pool_count && pos < (unsigned long long)a.pool_cap) {
+                  if (pos < (unsigned long long)a.pool_cap) {
                     a.pool_key[pos] = (unsigned long long)__double_as_longlong(mem);
                     a.pool_obj[pos] = obj;
                     a.pool_id[pos] = cid;
@@ -627,6 +654,9 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
                     dropped = true;
                   }
                 }
+                pool_used += k;
+              } else if (mo) {
+                dropped = dropped | over;
               }
               n_cand += __builtin_popcountll(m);
               continue;
@@ -753,6 +783,9 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
       }
       counter = counter + 1 == kClaimCounters ? 0 : counter + 1;
     }
+  }
+  if constexpr (EX) {
+    if (a.pool_count) pool_holes(a, pool_base, pool_used, lane);
   }
 }
 
