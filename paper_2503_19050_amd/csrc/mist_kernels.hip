@@ -749,6 +749,14 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
     // The tile's partials: lane j = bucket j.
     if constexpr (DM) {
     } else if constexpr (EX) {
+      // The wave's pool chunk is updated inside the strip loop, which lanes past a ragged
+      // tile's last strip leave early: lane 0 stays to the end and holds the current chunk.
+      {
+        const unsigned long long b = __shfl(pool_base, 0, 64);
+        pool_base = ((unsigned long long)__builtin_amdgcn_readfirstlane((unsigned int)(b >> 32)) << 32) |
+                    (unsigned long long)__builtin_amdgcn_readfirstlane((unsigned int)b);
+        pool_used = __builtin_amdgcn_readfirstlane(__shfl(pool_used, 0, 64));
+      }
       // Saturated at 2^31 - 1, which the host rejects (no tile of a space with fewer than
       // 2^32 candidates reaches it).
       if (lane == 0) a.cnt_tile[t] = (int32_t)min(n_cand - n_beg, (int64_t)0x7FFFFFFF);
