@@ -119,8 +119,8 @@ typedef struct mist_space_desc {
   int32_t cand_window;   /* exact frontier, results do not depend on it: each tile first writes
                             its candidates to a window of ceil(configurations / cand_window)
                             slots (0: 8, raised as needed to keep all windows within 2^27 slots),
-                            the rest to an overflow pool of half as many slots as all windows
-                            (at most 2^26); a tile with a candidate that finds no place is
+                            the rest to an overflow pool of as many slots as all windows (at
+                            most 2^27); a tile with a candidate that finds no place is
                             evaluated a second time */
 } mist_space_desc;
 

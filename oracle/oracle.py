@@ -279,6 +279,23 @@ def _worker_run_alpha(job):
     return g0, _worker_oracle.run_alpha(alphas, g0, g1)
 
 
+def _worker_pareto(g):
+    return g, _worker_oracle.pareto_exact(g)
+
+
+def pareto_exact_groups(wl: dict, groups, procs: int = 1) -> dict:
+    """Oracle.pareto_exact of each listed group (in fresh single-threaded processes when procs > 1):
+    {group: result}."""
+    groups = [int(g) for g in groups]
+    if procs <= 1:
+        o = Oracle(wl)
+        return {g: o.pareto_exact(g) for g in groups}
+    import multiprocessing as mp
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(procs, initializer=_worker_init, initargs=(wl,)) as pool:
+        return dict(pool.map(_worker_pareto, groups, chunksize=max(1, len(groups) // (8 * procs))))
+
+
 def run_alpha_groups(wl: dict, alphas, groups, procs: int = 1) -> dict:
     """Oracle.run_alpha on the listed group indices; arrays in that order."""
     groups = [int(g) for g in groups]

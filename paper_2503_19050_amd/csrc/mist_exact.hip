@@ -1,14 +1,14 @@
 // Exact time-vs-memory frontier (the staircase without memory buckets), second stage.  The
-// candidates of every group are sorted by memory with one segmented radix sort (rocPRIM; a
-// non-negative double orders like its bit pattern).  In (mem, obj, id) order a candidate is on the
-// frontier exactly when its objective is below that of every candidate before it; within a run of
-// equal memory only the run's (obj, id) minimum can be, and it is when its objective is below the
-// minima of every earlier run.  So the sort by memory alone suffices: one wave per group walks
-// its candidates in chunks of 64, reduces each run to its minimum (a segmented scan across the
-// lanes, carried over chunk boundaries) and keeps the runs that lower the running minimum.
+// candidates of every group are sorted by memory (a non-negative double orders like its bit
+// pattern) by a segmented sort of this file: a block per group sorts up to kSortCap candidates
+// in LDS (bitonic), and a larger group as sorted chunks merged pairwise (merge path).  In
+// (mem, obj, id) order a candidate is on the frontier exactly when its objective is below that of
+// every candidate before it; within a run of equal memory only the run's (obj, id) minimum can be,
+// and it is when its objective is below the minima of every earlier run.  So the sort by memory
+// alone suffices (the order inside a run of equal memory does not matter): one wave per group
+// walks its candidates in chunks of 64, reduces each run to its minimum (a segmented scan across
+// the lanes, carried over chunk boundaries) and keeps the runs that lower the running minimum.
 #include <hip/hip_runtime.h>
-
-#include <rocprim/device/device_segmented_radix_sort.hpp>
 
 #include <utility>
 
@@ -17,12 +17,124 @@
 namespace mist {
 namespace {
 
-__global__ __launch_bounds__(256) void k_iota(uint32_t* __restrict__ idx, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) idx[i] = (uint32_t)i;
+constexpr uint64_t kNoKey = ~0ull;  // no memory value has this bit pattern (it is a NaN)
+
+// ---------------------------------------------------------------------------------------
+// Segmented sort by memory key: keys [b, e) of cand_key, one block of kSortBlock threads per
+// group.  Output: key_out[b..e) ascending and idx_out[b..e) = the slots the keys came from.
+// ---------------------------------------------------------------------------------------
+constexpr int kSortBlock = 256;
+constexpr int kSortCap = 4096;  // keys sorted in LDS at once (48 KB with their slots)
+
+// Bitonic sort of the block's LDS keys [0, N) (N a power of two, padding keys kNoKey) with
+// their slots.
+__device__ __forceinline__ void lds_bitonic(uint64_t* sk, uint32_t* si, int N) {
+  for (int k = 2; k <= N; k <<= 1)
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = (int)threadIdx.x; i < N / 2; i += kSortBlock) {
+        const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1));
+        const int hi = lo + j;
+        const bool asc = (lo & k) == 0;
+        const uint64_t a = sk[lo], c = sk[hi];
+        if ((a > c) == asc) {
+          sk[lo] = c;
+          sk[hi] = a;
+          const uint32_t t = si[lo];
+          si[lo] = si[hi];
+          si[hi] = t;
+        }
+      }
+      __syncthreads();
+    }
 }
 
-constexpr uint64_t kNoKey = ~0ull;  // no memory value has this bit pattern (it is a NaN)
+// Sorts keys [b, b + n) (n <= kSortCap) in LDS and writes them with their slots at out + b.
+__device__ __forceinline__ void sort_chunk(const uint64_t* __restrict__ key, int64_t b, int n, uint64_t* sk,
+                                           uint32_t* si, uint64_t* __restrict__ key_out, uint32_t* __restrict__ idx_out) {
+  int N = 1;
+  while (N < n) N <<= 1;
+  for (int i = (int)threadIdx.x; i < N; i += kSortBlock) {
+    sk[i] = i < n ? key[b + i] : kNoKey;
+    si[i] = (uint32_t)i;
+  }
+  __syncthreads();
+  lds_bitonic(sk, si, N);
+  for (int i = (int)threadIdx.x; i < n; i += kSortBlock) {
+    key_out[b + i] = sk[i];
+    idx_out[b + i] = (uint32_t)(b + si[i]);
+  }
+  __syncthreads();
+}
+
+// Merges the sorted runs A = [a0, a1) and B = [a1, b1) of (ks, is) into (kd, id) at a0, by the
+// whole block: thread t produces its share of the output from the split of its diagonal
+// (merge path: the number of A's keys among the first d outputs, ties taken from A first).
+__device__ __forceinline__ void merge_runs(const uint64_t* __restrict__ ks, const uint32_t* __restrict__ is,
+                                           uint64_t* __restrict__ kd, uint32_t* __restrict__ id, int64_t a0,
+                                           int64_t a1, int64_t b1) {
+  const int64_t na = a1 - a0, nb = b1 - a1, L = na + nb;
+  const int64_t per = (L + kSortBlock - 1) / kSortBlock;
+  const int64_t d0 = min((int64_t)threadIdx.x * per, L), d1 = min(d0 + per, L);
+  if (d0 >= d1) return;
+  // i = keys of A among the first d0 outputs: the largest i with A[i-1] <= B[d0-i].
+  int64_t lo = max((int64_t)0, d0 - nb), hi = min(d0, na);
+  while (lo < hi) {
+    const int64_t i = (lo + hi) / 2;  // is A[i] <= B[d0-i-1]?  then more of A comes first
+    if (ks[a0 + i] <= ks[a1 + d0 - i - 1]) lo = i + 1;
+    else hi = i;
+  }
+  int64_t i = lo, j = d0 - lo;
+  for (int64_t d = d0; d < d1; ++d) {
+    const bool take_a = j >= nb || (i < na && ks[a0 + i] <= ks[a1 + j]);
+    const int64_t src = take_a ? a0 + i : a1 + j;
+    kd[a0 + d] = ks[src];
+    id[a0 + d] = is[src];
+    if (take_a) ++i;
+    else ++j;
+  }
+}
+
+__global__ __launch_bounds__(kSortBlock) void k_seg_sort(const uint64_t* __restrict__ key, const int64_t* __restrict__ seg,
+                                                        const int64_t* __restrict__ seg_end, uint64_t* __restrict__ key_out,
+                                                        uint32_t* __restrict__ idx_out, uint64_t* __restrict__ key_tmp,
+                                                        uint32_t* __restrict__ idx_tmp) {
+  __shared__ uint64_t sk[kSortCap];
+  __shared__ uint32_t si[kSortCap];
+  const int64_t g = blockIdx.x;
+  const int64_t b = seg[g], e = seg_end[g], n = e - b;
+  if (n <= 0) return;
+  if (n <= kSortCap) {
+    sort_chunk(key, b, (int)n, sk, si, key_out, idx_out);
+    return;
+  }
+  // Sorted chunks of kSortCap, then pairwise merges, alternating between (key_out, idx_out)
+  // and (key_tmp, idx_tmp) (both indexed by slot).
+  for (int64_t c0 = 0; c0 < n; c0 += kSortCap)
+    sort_chunk(key, b + c0, (int)min((int64_t)kSortCap, n - c0), sk, si, key_out, idx_out);
+  uint64_t* ks = key_out;
+  uint32_t* is = idx_out;
+  uint64_t* kd = key_tmp;
+  uint32_t* id = idx_tmp;
+  for (int64_t w = kSortCap; w < n; w <<= 1) {
+    for (int64_t s0 = 0; s0 < n; s0 += 2 * w) {
+      const int64_t a1 = min(s0 + w, n), b1 = min(s0 + 2 * w, n);
+      merge_runs(ks, is, kd, id, b + s0, b + a1, b + b1);
+    }
+    __syncthreads();
+    uint64_t* const tk = ks;
+    ks = kd;
+    kd = tk;
+    uint32_t* const ti = is;
+    is = id;
+    id = ti;
+  }
+  if (ks != key_out) {
+    for (int64_t i = threadIdx.x; i < n; i += kSortBlock) {
+      key_out[b + i] = ks[b + i];
+      idx_out[b + i] = is[b + i];
+    }
+  }
+}
 
 __device__ __forceinline__ bool lex_less(double o1, uint64_t i1, double o2, uint64_t i2) {
   return o1 < o2 || (o1 == o2 && i1 < i2);
@@ -420,25 +532,12 @@ int last_error() {
 
 }  // namespace
 
-int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_in, uint32_t* idx_out, int64_t n,
-               int64_t n_groups, const int64_t* seg_begin, const int64_t* seg_end, void* temp, size_t* temp_bytes,
-               void* stream) {
-  hipStream_t st = (hipStream_t)stream;
-  const unsigned int un = (unsigned int)n, ug = (unsigned int)n_groups;
-  if (!temp) {  // storage query
-    const hipError_t e = rocprim::segmented_radix_sort_pairs(nullptr, *temp_bytes, cand_key, key_out, idx_in,
-                                                             idx_out, un, ug, seg_begin, seg_end, 0, 64, st);
-    return e == hipSuccess ? 0 : (int)e;
-  }
-  if (n == 0) return 0;
-  hipLaunchKernelGGL(k_iota, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, idx_in, n);
-  int rc = last_error();
-  if (!rc) {
-    const hipError_t e = rocprim::segmented_radix_sort_pairs(temp, *temp_bytes, cand_key, key_out, idx_in, idx_out,
-                                                             un, ug, seg_begin, seg_end, 0, 64, st);
-    if (e != hipSuccess) rc = (int)e;
-  }
-  return rc;
+int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_out, uint64_t* key_tmp, uint32_t* idx_tmp,
+               int64_t n_groups, const int64_t* seg_begin, const int64_t* seg_end, void* stream) {
+  if (n_groups <= 0) return 0;
+  hipLaunchKernelGGL(k_seg_sort, dim3((unsigned)n_groups), dim3(kSortBlock), 0, (hipStream_t)stream, cand_key,
+                     seg_begin, seg_end, key_out, idx_out, key_tmp, idx_tmp);
+  return last_error();
 }
 
 int launch_compact(const uint64_t* slab_key, const double* slab_obj, const uint64_t* slab_id,

@@ -47,7 +47,7 @@ constexpr int64_t kMaxTiles = 131072;         // and tiles per space, at most
 constexpr int64_t kWindowDiv = 8;             // exact frontier: candidate window of a tile,
                                               // 1/kWindowDiv of its configurations
 constexpr int64_t kWindowSlots = (int64_t)1 << 27;  // and all windows together, at most
-constexpr int64_t kPoolSlots = (int64_t)1 << 26;    // overflow pool of the candidate pass, at most
+constexpr int64_t kPoolSlots = (int64_t)1 << 27;    // overflow pool of the candidate pass, at most
 constexpr int64_t kTailPercent = 10;          // share of each group's strips in small tiles
 constexpr int64_t kStripAlign = kWaveTile;    // strips per tile: a multiple of the wave
 
@@ -151,8 +151,6 @@ struct mist_space {
   uint32_t *d_idx_in = nullptr, *d_idx_out = nullptr;
   uint64_t *d_front_key = nullptr, *d_front_id = nullptr;
   double* d_front_obj = nullptr;
-  void* d_sort_temp = nullptr;
-  size_t sort_temp_bytes = 0;
   // state
   bool evaluated = false;
   hipStream_t stream = nullptr;
@@ -902,8 +900,9 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       S->d_slab_key = (uint64_t*)dev_alloc(S, n_slab * 8);
       S->d_slab_obj = (double*)dev_alloc(S, n_slab * 8);
       S->d_slab_id = (uint64_t*)dev_alloc(S, n_slab * 8);
-      // The pool holds half as many slots as all windows together (at most kPoolSlots).
-      S->pool_cap = std::min<int64_t>(kPoolSlots, std::max<int64_t>((int64_t)n_slab / 2, 1));
+      // The pool holds as many slots as all windows together (at most kPoolSlots): the windows
+      // of tiles that hold no candidate stay empty, so the overflow of the others can be large.
+      S->pool_cap = std::min<int64_t>(kPoolSlots, std::max<int64_t>((int64_t)n_slab, 1));
       const size_t n_pool = (size_t)S->pool_cap;
       S->d_pool_count = (unsigned long long*)dev_alloc(S, 256);
       S->d_pool_key = (uint64_t*)dev_alloc(S, n_pool * 8);
@@ -1021,16 +1020,6 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
         return fail(MIST_E_NOMEM, "device allocation failed: exact frontier candidates");
       }
     }
-    size_t need = 0;
-    k = exact_sort(S->d_cand_key, S->d_key_sorted, S->d_idx_in, S->d_idx_out, off, (int64_t)ng, S->d_seg,
-                   S->d_seg_end, nullptr, &need, st);
-    if (k) return fail_hip((hipError_t)k, "exact frontier: sort storage");
-    if (need > S->sort_temp_bytes) {
-      dev_free_one(S, S->d_sort_temp);
-      S->d_sort_temp = dev_alloc(S, need);
-      S->sort_temp_bytes = S->d_sort_temp ? need : 0;
-      if (!S->d_sort_temp) return fail(MIST_E_NOMEM, "device allocation failed: sort storage");
-    }
     const int32_t n_list = S->n_list;
     S->exact_launched = true;
     S->exact_stream = st;
@@ -1063,11 +1052,11 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
       if (!k) k = launch_eval(ea, mode_grid(S, kModeEmit), kModeEmit, st);
     }
     if (!k) k = launch_prefilter(S->d_cand_key, S->d_cand_obj, S->d_cand_id, S->d_seg, (int64_t)ng, S->d_seg_end, st);
-    if (!k) {
-      size_t bytes = S->sort_temp_bytes;
-      k = exact_sort(S->d_cand_key, S->d_key_sorted, S->d_idx_in, S->d_idx_out, off, (int64_t)ng, S->d_seg,
-                     S->d_seg_end, S->d_sort_temp, &bytes, st);
-    }
+    // The frontier's key array and the slot array d_idx_in serve as the sort's scratch (the scan
+    // writes the frontier after the sort).
+    if (!k)
+      k = exact_sort(S->d_cand_key, S->d_key_sorted, S->d_idx_out, S->d_front_key, S->d_idx_in, (int64_t)ng,
+                     S->d_seg, S->d_seg_end, st);
     if (!k)
       k = launch_front_scan(S->d_idx_out, S->d_key_sorted, S->d_cand_obj, S->d_cand_id, S->d_seg, S->d_seg_end,
                             (int64_t)ng, S->d_front_key, S->d_front_obj, S->d_front_id, S->d_front_cnt, st);

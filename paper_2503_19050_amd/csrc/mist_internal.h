@@ -189,13 +189,13 @@ int launch_filter(const EvalArgs& a, const double* bucket_obj, const uint64_t* b
 // Exact frontier, mist_exact.hip: the candidates of group g are [seg[g], seg[g+1]).  The
 // pre-filter drops, per group, candidates that one of strictly smaller memory dominates and
 // moves the rest to the front (their end in seg_end); one segmented sort by memory over
-// [seg[g], seg_end[g]) leaves the sorted keys in key_out and the candidates' slots in idx_out,
-// and the per-group scan keeps the staircase.
+// [seg[g], seg_end[g]) leaves the sorted keys in key_out and the candidates' slots in idx_out
+// (key_tmp, idx_tmp: scratch of the same slots for large groups), and the per-group scan keeps
+// the staircase.
 int launch_prefilter(uint64_t* cand_key, double* cand_obj, uint64_t* cand_id, const int64_t* seg,
                      int64_t n_groups, int64_t* seg_end, void* stream);
-int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_in, uint32_t* idx_out, int64_t n,
-               int64_t n_groups, const int64_t* seg_begin, const int64_t* seg_end, void* temp, size_t* temp_bytes,
-               void* stream);
+int exact_sort(const uint64_t* cand_key, uint64_t* key_out, uint32_t* idx_out, uint64_t* key_tmp, uint32_t* idx_tmp,
+               int64_t n_groups, const int64_t* seg_begin, const int64_t* seg_end, void* stream);
 // Moves each tile's window [slab_begin[t], slab_begin[t+1]) (its first candidates, at most
 // cnt[t]) to [tile_off[t], ...); tiles with tile_drop[t] set are skipped (evaluated again).
 int launch_compact(const uint64_t* slab_key, const double* slab_obj, const uint64_t* slab_id,

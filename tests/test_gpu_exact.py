@@ -1,6 +1,7 @@
 """GPU exact (non-bucketed) time-vs-memory frontier against the oracle's sort-and-scan, through
 the C ABI: the same ids, objectives and memory, in the same order, for every checked group."""
 
+import os
 import sys
 
 import numpy as np
@@ -31,8 +32,14 @@ def _tight():
     return wl
 
 
+PROCS = max(1, min(16, os.cpu_count() or 1))
+
+
 @pytest.mark.parametrize("name", ["tiny", "tiny_llama", "tight", "gpt1.3b-d8", "gpt2.7b-d16", "llama7b-d32", "llama13b-d64", "llama42b-d128-hw64"])
 def test_exact_frontier(name, torch_cuda):
+    """Every group of the small spaces and of gpt2.7b-d16; for the Llama workloads seeded random
+    groups plus the groups with the most candidates and the most pre-filter survivors (those past
+    the sort's in-LDS capacity of 4,096 take its merge path)."""
     from paper_2503_19050_amd import mist
     wl = _tight() if name == "tight" else W.workload(name)
     S = mist.from_workload(wl)
@@ -40,17 +47,26 @@ def test_exact_frontier(name, torch_cuda):
     S.eval_pareto_exact()
     torch_cuda.cuda.synchronize()
     o = O.Oracle(wl)
-    if name in ("tiny", "tiny_llama", "tight", "gpt1.3b-d8"):
-        groups = range(o.n_groups)
+    if name in ("tiny", "tiny_llama", "tight", "gpt1.3b-d8", "gpt2.7b-d16"):
+        groups = list(range(o.n_groups))
     else:
         rng = np.random.default_rng(4)
         size = 100 if name == "llama7b-d32" else 6
-        groups = sorted({0, o.n_groups - 1} | set(int(g) for g in rng.choice(o.n_groups, size=size, replace=False)))
+        cand, kept = S.exact_group_sizes()
+        top = set(int(g) for g in np.argsort(-cand, kind="stable")[:4]) | \
+            set(int(g) for g in np.argsort(-kept, kind="stable")[:4])
+        big = np.flatnonzero(kept > 4096)
+        if big.size:
+            top |= set(int(g) for g in rng.choice(big, size=min(4, big.size), replace=False))
+        say(name, "largest groups", sorted(top), "kept", [int(kept[g]) for g in sorted(top)])
+        groups = sorted({0, o.n_groups - 1} | top |
+                        set(int(g) for g in rng.choice(o.n_groups, size=size, replace=False)))
+    ref = O.pareto_exact_groups(wl, groups, procs=PROCS if len(groups) > 16 else 1)
     best = S.best(0, S.n_groups)
     total = 0
     for g in groups:
         got = S.pareto_exact(g)
-        want = o.pareto_exact(g)
+        want = ref[g]
         assert [r["id"] for r in got] == [int(i) for i in want["id"]], g
         assert [r["obj"] for r in got] == list(want["obj"]) and [r["mem"] for r in got] == list(want["mem"]), g
         if got:
