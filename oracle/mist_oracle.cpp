@@ -300,50 +300,51 @@ bool build_ctx(Ctx& X, const Model* m, const Hw* hw, int32_t n_hw, const Space* 
 }
 
 // ---------------------------------------------------------------------------
-// Algorithm 1 (Sec. 5.2.2): interference between the four co-running streams
-// X = [C (compute), G2G (GPU<->GPU), C2G (host->device), G2C (device->host)].
-// For n = 4 down to 2, for every n-stream combination (masks in ascending
-// order) whose streams are exactly the ones still running, every member's
-// remaining time is scaled by its slowdown factor, the smallest scaled time
-// overlaps all of them, and the members' remaining standalone times are
-// updated; finally the leftover standalone times are added.  The division by
-// the factor is a multiplication by the host reciprocal psi = 1/phi.
+// Interference model of Sec. 5.2.2 (Algorithm 1) for the four streams
+// X = [C (compute), G2G (GPU<->GPU), C2G (host->device), G2C (device->host)],
+// written as a simulation of phases.  X[j] is the time stream j needs alone.
+// While two or more streams still have work, they all run together and stream
+// j progresses phi[set][j] times slower than alone, set being the bit mask of
+// the running streams; a phase lasts until the first of them completes.  In a
+// phase each member's co-run time is its remaining standalone time times its
+// factor, the phase length is the smallest co-run time, and a member's
+// standalone time left afterwards is its unused co-run time divided by its
+// factor.  The division is a multiplication by the host reciprocal
+// psi = 1/phi.  Once at most one stream is left it runs alone; the answer is
+// the sum of the phase lengths and that last stream's time.
+//
+// Each phase ends at least one stream (the shortest co-run time minus itself
+// is exactly zero), so there are at most three phases (sets of 4, 3, 2 or
+// fewer streams); the loop bound only guards against non-finite input.
+// Members are visited in increasing stream index, which fixes the rounding
+// order of the minimum and of the final sum.
 // ---------------------------------------------------------------------------
 inline int popcount4(int v) { return (v & 1) + ((v >> 1) & 1) + ((v >> 2) & 1) + ((v >> 3) & 1); }
 
 template <class R>
 R interference(const R Xin[4], const double phi[16][4], const double* psi /*[16][4]*/) {
-  R X[4] = {Xin[0], Xin[1], Xin[2], Xin[3]};
-  R T = R(0.0);
-  for (int n = 4; n >= 2; --n) {
-    for (int mask = 0; mask < 16; ++mask) {
-      if (popcount4(mask) != n) continue;
-      int pattern = 0;
-      for (int j = 0; j < 4; ++j)
-        if (X[j] != R(0.0)) pattern |= 1 << j;
-      if (pattern != mask) continue;
-      // Update(X, T, mask, factors)
-      R sc[4];
-      bool have = false;
-      R ov = R(0.0);
-      for (int j = 0; j < 4; ++j) {
-        if (!(mask >> j & 1)) continue;
-        sc[j] = X[j] * R(phi[mask][j]);
-        ov = have ? min2(ov, sc[j]) : sc[j];
-        have = true;
+  R alone[4] = {Xin[0], Xin[1], Xin[2], Xin[3]};  // standalone time still needed per stream
+  R elapsed = R(0.0);
+  for (int phase = 0; phase < 3; ++phase) {
+    int set = 0;
+    for (int j = 0; j < 4; ++j)
+      if (alone[j] != R(0.0)) set |= 1 << j;
+    if (popcount4(set) < 2) break;
+    R corun[4];
+    R len = R(0.0);
+    bool first = true;
+    for (int j = 0; j < 4; ++j)
+      if (set >> j & 1) {
+        corun[j] = alone[j] * R(phi[set][j]);
+        len = first ? corun[j] : min2(len, corun[j]);
+        first = false;
       }
-      for (int j = 0; j < 4; ++j) {
-        if (!(mask >> j & 1)) continue;
-        X[j] = (sc[j] - ov) * R(psi[mask * 4 + j]);
-      }
-      T = T + ov;
-    }
+    for (int j = 0; j < 4; ++j)
+      if (set >> j & 1) alone[j] = (corun[j] - len) * R(psi[set * 4 + j]);
+    elapsed = elapsed + len;
   }
-  T = T + X[0];
-  T = T + X[1];
-  T = T + X[2];
-  T = T + X[3];
-  return T;
+  for (int j = 0; j < 4; ++j) elapsed = elapsed + alone[j];
+  return elapsed;
 }
 
 // ---------------------------------------------------------------------------

@@ -34,9 +34,12 @@ MUTANTS = {
     "first microbatch uses the stable ZeRO traffic": (
         "const R G2Gf = fma3(R(mf_tab[z]), r_, p2p);", "const R G2Gf = fma3(R(ms_tab[z]), r_, p2p);"),
     "interference divides by a neighbour's factor": (
-        "X[j] = (sc[j] - ov) * R(psi[mask * 4 + j]);", "X[j] = (sc[j] - ov) * R(psi[mask * 4 + (j ^ 1)]);"),
-    "interference levels in ascending order": (
-        "for (int n = 4; n >= 2; --n) {", "for (int n = 2; n <= 4; ++n) {"),
+        "alone[j] = (corun[j] - len) * R(psi[set * 4 + j]);",
+        "alone[j] = (corun[j] - len) * R(psi[set * 4 + (j ^ 1)]);"),
+    "interference phase lasts until the last stream ends": (
+        "len = first ? corun[j] : min2(len, corun[j]);", "len = first ? corun[j] : max2(len, corun[j]);"),
+    "interference keeps the all-stream factors after a stream ends": (
+        "corun[j] = alone[j] * R(phi[set][j]);", "corun[j] = alone[j] * R(phi[15][j]);"),
     "activation swap-in uses the kept fraction": (
         "const R H2Ds = fma3(ra, A, HW) * iP;", "const R H2Ds = fma3(qa, A, HW) * iP;"),
     "recomputation counted twice": ("R(exact(3 * l + c))", "R(exact(3 * l + 2 * c))"),
