@@ -231,9 +231,14 @@ mist_status mist_get_alpha(mist_space* S, int64_t g0, int64_t n, mist_result* ou
 /* Inter-stage planner (Sec. 5.3, Eq. 1-3), host only: among the candidate points pts[0..n-1]
  * of one hardware sample, chooses G, PP, the layer counts l_1..l_PP (summing to n_layers; stage
  * i draws from the points of group (G, PP, k = PP - i + 1, l_i)) and one point per stage so
- * that Eq. 2 is minimal, exactly (a dominance-pruned dynamic program over stages).  pp = 0
- * allows every PP, otherwise only plans with PP = pp (<= MIST_MAX_STAGES; points of larger PP
- * are ignored).  Writes *out (found = 0 when no plan exists).  Errors: MIST_E_INVALID. */
+ * that Eq. 2 is minimal (a dominance-pruned dynamic program over stages).  The plan chosen is
+ * the exact minimum of Eq. 2 evaluated as (G-1)*max t_i + max_i (d_i + sum_{j>=i} t_j), the sums
+ * taken from the last stage to the first (the form whose rounding the pruning respects; among
+ * equal values, the smallest G, then PP).  out->F is that plan's value in stage order (the
+ * field's form), which can differ from the stage-order minimum by the rounding of the two
+ * sums, a few ulps.  pp = 0 allows every PP, otherwise only plans with PP = pp
+ * (<= MIST_MAX_STAGES; points of larger PP are ignored).  Writes *out (found = 0 when no plan
+ * exists).  Errors: MIST_E_INVALID. */
 mist_status mist_plan_points(const mist_stage_point* pts, int64_t n, int32_t n_layers, int32_t pp,
                              mist_plan* out);
 

@@ -14,6 +14,11 @@ objective of Eq. 2 with the inner sum read as the time of the stages before i:
     F = (G - 1) * max_i t_i + sum_i t_i + max_i (d_i - sum_{j<i} t_j),
 
 evaluated in stage order: the sums left to right, F = ((G-1)*t_max + t_sum) + m.
+
+The same objective regrouped, F = (G - 1) * max_i t_i + max_i (d_i + sum_{j>=i} t_j), is equal in
+real arithmetic; evaluated with the sums taken from the last stage to the first it can differ in
+the last bits.  plan_value_suffix is that form (the one in which a stage-by-stage search from the
+last stage prunes exactly).
 """
 
 from __future__ import annotations
@@ -38,6 +43,17 @@ def plan_value(G: int, ts, ds) -> float:
     return (float(G - 1) * t_max + t_sum) + m
 
 
+def plan_value_suffix(G: int, ts, ds) -> float:
+    """Eq. 2 as (G - 1) * max t + max_i (d_i + T_i), T_i = t_i + T_{i+1} summed from the last
+    stage to the first."""
+    T = 0.0
+    h = None
+    for t, d in zip(reversed(ts), reversed(ds)):
+        T = t + T
+        h = d + T if h is None else max(h, d + T)
+    return float(G - 1) * max(ts) + h
+
+
 def candidates(wl: dict, alphas=()) -> dict:
     """{hw: {(G, PP, k, l): [(t, d, id), ...]}} from the oracle's own results: each group's best
     configuration and the one each weight sample selects."""
@@ -60,10 +76,35 @@ def candidates(wl: dict, alphas=()) -> dict:
     return out
 
 
-def best_plan(cand: dict, n_layers: int, pp: int = 0):
+def candidates_groups(wl: dict, alphas, groups, procs: int = 1) -> dict:
+    """candidates() restricted to the listed groups (process-parallel oracle runs):
+    {hw: {(G, PP, k, l): [(t, d, id), ...]}}."""
+    groups = sorted(int(g) for g in groups)
+    o = O.Oracle(wl)
+    keys = o.group_keys()
+    best = O.run_groups(wl, groups, procs)
+    ids = {g: [int(i)] for g, i in zip(groups, best["best_id"])}
+    if len(alphas):
+        al = O.run_alpha_groups(wl, alphas, groups, procs)
+        for r, g in enumerate(groups):
+            ids[g] += [int(i) for i in al["id"][r]]
+    out = {}
+    for g in groups:
+        uniq = sorted(set(i for i in ids[g] if i != int(O.NONE)))
+        if not uniq:
+            continue
+        k = keys[g]
+        vals = o.eval_ids(np.array(uniq, dtype=np.uint64))
+        out.setdefault(k["hw"], {})[(k["G"], k["PP"], k["k"], k["l"])] = [
+            (float(v[0]), float(v[1]), i) for v, i in zip(vals, uniq)]
+    return out
+
+
+def best_plan(cand: dict, n_layers: int, pp: int = 0, value=plan_value):
     """Exhaustive minimum of Eq. 2 over (G, PP, layer counts, one point per stage) for one
     hardware sample's candidates {(G, PP, k, l): [(t, d, id)]}; stage i draws from group
-    (G, PP, PP - i + 1, l_i).  Returns (F, G, PP, [l_i], [id_i]) or None."""
+    (G, PP, PP - i + 1, l_i).  `value` evaluates a plan (plan_value or plan_value_suffix).
+    Returns (F, G, PP, [l_i], [id_i]) or None; the first minimum found on ties."""
     lsets = {}
     for (G, PP, k, l) in cand:
         lsets.setdefault((G, PP), set()).add(l)
@@ -78,7 +119,7 @@ def best_plan(cand: dict, n_layers: int, pp: int = 0):
             if any(len(p) == 0 for p in pts):
                 continue
             for choice in itertools.product(*pts):
-                F = plan_value(G, [c[0] for c in choice], [c[1] for c in choice])
+                F = value(G, [c[0] for c in choice], [c[1] for c in choice])
                 if best is None or F < best[0]:
                     best = (F, G, PP, list(parts), [c[2] for c in choice])
     return best

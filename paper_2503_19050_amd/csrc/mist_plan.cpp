@@ -10,8 +10,16 @@
 // (t_i + T, max(H, d_i + t_i + T), max(M, t_i)).  A partial plan whose (T, H, M) is no smaller
 // in all three than another's with the same stages and layer count can never finish better, so
 // a dynamic program over (stage, layers used) keeps only the non-dominated triples and is exact;
-// no MILP solver is needed.  The winner's F is then re-evaluated in stage order (sums left to
-// right), the form the paper writes.
+// no MILP solver is needed.
+//
+// Exact also in floating point: every step above (a rounded sum, a maximum) and the final
+// (G - 1) * M + H are non-decreasing in T, H and M, so a pruned state's completions never round
+// below its dominator's.  Finished plans are therefore ranked by that same suffix-form value,
+// fl((G - 1) * M + H), and the winner is its exact minimum over all plans.  The reported F is the
+// winner re-evaluated in stage order (sums left to right), the form the paper writes; the two
+// forms agree in real arithmetic, so against the minimum of the stage-order form the reported F
+// is off by at most the rounding of the two evaluations (a few ulps of the summed stage times per
+// stage).
 
 #include <algorithm>
 #include <cmath>
@@ -90,6 +98,7 @@ extern "C" mist_status mist_plan_points(const mist_stage_point* pts, int64_t n, 
   try {
     std::memset(out, 0, sizeof(*out));
     out->F = std::numeric_limits<double>::infinity();
+    double best_Fs = std::numeric_limits<double>::infinity();  // suffix-form value of *out
     // candidates per (G, PP) -> per k -> per l
     std::map<std::pair<int32_t, int32_t>, std::map<int32_t, std::map<int32_t, std::vector<Pt>>>> cand;
     for (int64_t i = 0; i < n; ++i) {
@@ -142,6 +151,9 @@ extern "C" mist_status mist_plan_points(const mist_stage_point* pts, int64_t n, 
       // the finished plans: stage 1 placed, all layers used
       const auto& fin = states[1][n_layers];
       for (int s = 0; s < (int)fin.size(); ++s) {
+        const double Fs = (double)(G - 1) * fin[s].M + fin[s].H;
+        if (!(Fs < best_Fs)) continue;
+        best_Fs = Fs;
         std::vector<double> tv, dv;
         mist_plan cand_plan;
         std::memset(&cand_plan, 0, sizeof(cand_plan));
@@ -164,14 +176,11 @@ extern "C" mist_status mist_plan_points(const mist_stage_point* pts, int64_t n, 
           cur = st.prev;
           u -= st.l;
         }
-        const double F = plan_value(G, tv, dv);
-        if (F < out->F) {
-          cand_plan.G = G;
-          cand_plan.PP = PP;
-          cand_plan.found = 1;
-          cand_plan.F = F;
-          *out = cand_plan;
-        }
+        cand_plan.G = G;
+        cand_plan.PP = PP;
+        cand_plan.found = 1;
+        cand_plan.F = plan_value(G, tv, dv);
+        *out = cand_plan;
       }
     }
     return MIST_OK;

@@ -44,3 +44,22 @@ def test_digest_sees_every_word():
         d = group_digests(m["bucket_id"], m["bucket_obj"], m["frontier"], m["best_id"], m["best_obj"])
         assert d[g] != base[g], key
         assert np.array_equal(np.delete(d, g), np.delete(base, g)), key
+
+
+def test_stored_plan_points_are_the_oracles():
+    """tests/golden/plan_llama13b-d64.npz: every stored point decodes to its group's key and
+    carries the oracle's own t and d; every group with PP = 1 or 2 and a feasible configuration
+    has at least one point."""
+    z = np.load(os.path.join(GOLDEN, "plan_llama13b-d64.npz"))
+    wl = W.workload("llama13b-d64")
+    wl["space"] = dict(wl["space"], alphas=[float(a) for a in z["alphas"]])
+    o = O.Oracle(wl)
+    ids = z["id"]
+    vals = o.eval_ids(ids)
+    assert np.array_equal(vals[:, 0], z["t"]) and np.array_equal(vals[:, 1], z["d"])
+    for r in range(0, len(ids), 7):
+        c = o.decode(int(ids[r]))
+        assert (c["hw"], c["G"], c["PP"], c["k"], c["l"]) == (z["hw"][r], z["G"][r], z["PP"][r], z["k"][r], z["l"][r])
+    keys = {(k["hw"], k["G"], k["PP"], k["k"], k["l"]) for k in o.group_keys() if k["PP"] in (1, 2)}
+    have = set(zip(z["hw"].tolist(), z["G"].tolist(), z["PP"].tolist(), z["k"].tolist(), z["l"].tolist()))
+    assert have <= keys and len(have) > 0.5 * len(keys)
