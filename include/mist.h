@@ -125,9 +125,14 @@ typedef struct mist_space_desc {
 } mist_space_desc;
 
 /* Device memory provider, e.g. PyTorch's caching allocator.  alloc returns NULL on
- * failure; free receives exactly the pointers alloc returned. */
+ * failure; free receives exactly the pointers alloc returned.  hip_stream (a hipStream_t) is
+ * the stream on which the library first uses the block, so that a stream-ordered allocator can
+ * hand out a block whose earlier users were on that same stream: the null stream for the
+ * space's own buffers (mist_space_create waits for the null stream before it returns, and later
+ * calls may use them on any stream), the call's stream for the exact frontier's buffers and
+ * for temporaries.  The library frees a block only after its own work on it has finished. */
 typedef struct mist_allocator {
-  void* (*alloc)(size_t bytes, void* ctx);
+  void* (*alloc)(size_t bytes, void* hip_stream, void* ctx);
   void (*free)(void* ptr, void* ctx);
   void* ctx;
 } mist_allocator;

@@ -161,11 +161,12 @@ struct mist_space {
 
 namespace {
 
-void* dev_alloc(mist_space* S, size_t bytes) {
+// A device buffer owned by the space; `st` is the stream of its first use (see mist_allocator).
+void* dev_alloc(mist_space* S, size_t bytes, hipStream_t st) {
   if (bytes == 0) bytes = 256;
   void* p = nullptr;
   if (S->custom_alloc) {
-    p = S->alloc.alloc(bytes, S->alloc.ctx);
+    p = S->alloc.alloc(bytes, (void*)st, S->alloc.ctx);
   } else if (hipMalloc(&p, bytes) != hipSuccess) {
     p = nullptr;
   }
@@ -196,9 +197,9 @@ void dev_free_all(mist_space* S) {
 struct TempBuf {
   mist_space* S;
   void* p = nullptr;
-  TempBuf(mist_space* s, size_t bytes) : S(s) {
+  TempBuf(mist_space* s, size_t bytes, hipStream_t st) : S(s) {
     if (bytes == 0) bytes = 256;
-    if (S->custom_alloc) p = S->alloc.alloc(bytes, S->alloc.ctx);
+    if (S->custom_alloc) p = S->alloc.alloc(bytes, (void*)st, S->alloc.ctx);
     else if (hipMalloc(&p, bytes) != hipSuccess) p = nullptr;
   }
   ~TempBuf() {
@@ -475,7 +476,7 @@ std::string enumerate(mist_space* S, mist_status* code) {
 
 template <class T>
 mist_status upload(mist_space* S, T** dst, const std::vector<T>& src, const char* what) {
-  *dst = (T*)dev_alloc(S, src.size() * sizeof(T));
+  *dst = (T*)dev_alloc(S, src.size() * sizeof(T), nullptr);
   if (!*dst) return fail(MIST_E_NOMEM, std::string("device allocation failed: ") + what);
   if (src.empty()) return MIST_OK;
   const hipError_t e = copy_sync(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
@@ -548,8 +549,8 @@ mist_status eval_ids_impl(mist_space* S, const uint64_t* ids, int64_t n, double*
   if (n == 0) return MIST_OK;
   for (int64_t i = 0; i < n; ++i)
     if (ids[i] >= S->n_configs) return fail(MIST_E_RANGE, "id out of range");
-  TempBuf dids(S, (size_t)n * sizeof(uint64_t));
-  TempBuf dout(S, (size_t)n * 4 * sizeof(double));
+  TempBuf dids(S, (size_t)n * sizeof(uint64_t), st);
+  TempBuf dout(S, (size_t)n * 4 * sizeof(double), st);
   if (!dids.p || !dout.p) return fail(MIST_E_NOMEM, "device allocation failed: eval_ids");
   // The temporary buffers go back to the allocator when this returns: on every path the
   // stream is drained first.
@@ -743,31 +744,37 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
     if (!rc && S->A > 0) rc = upload(S, &S->d_alpha, S->alphas, "weight samples");
     if (!rc && S->A > 0) rc = upload(S, &S->d_beta, S->betas, "weight samples");
     if (!rc) {
-      S->d_pk = (PairK*)dev_alloc(S, S->pk_group.size() * sizeof(PairK));
-      S->d_work = (int32_t*)dev_alloc(S, sizeof(int32_t) * kClaimCounters * kCounterStride);
+      S->d_pk = (PairK*)dev_alloc(S, S->pk_group.size() * sizeof(PairK), nullptr);
+      S->d_work = (int32_t*)dev_alloc(S, sizeof(int32_t) * kClaimCounters * kCounterStride, nullptr);
       if (!S->d_pk || !S->d_work) rc = fail(MIST_E_NOMEM, "device allocation failed: pair constants");
     }
     const size_t nt = S->tiles.size(), ng = S->groups.size();
     if (!rc) {
-      S->d_part_obj = (double*)dev_alloc(S, nt * 64 * sizeof(double));
-      S->d_part_id = (uint64_t*)dev_alloc(S, nt * 64 * sizeof(uint64_t));
-      S->d_bucket_obj = (double*)dev_alloc(S, ng * 64 * sizeof(double));
-      S->d_bucket_id = (uint64_t*)dev_alloc(S, ng * 64 * sizeof(uint64_t));
-      S->d_best_obj = (double*)dev_alloc(S, ng * sizeof(double));
-      S->d_best_id = (uint64_t*)dev_alloc(S, ng * sizeof(uint64_t));
-      S->d_frontier = (uint64_t*)dev_alloc(S, ng * sizeof(uint64_t));
+      S->d_part_obj = (double*)dev_alloc(S, nt * 64 * sizeof(double), nullptr);
+      S->d_part_id = (uint64_t*)dev_alloc(S, nt * 64 * sizeof(uint64_t), nullptr);
+      S->d_bucket_obj = (double*)dev_alloc(S, ng * 64 * sizeof(double), nullptr);
+      S->d_bucket_id = (uint64_t*)dev_alloc(S, ng * 64 * sizeof(uint64_t), nullptr);
+      S->d_best_obj = (double*)dev_alloc(S, ng * sizeof(double), nullptr);
+      S->d_best_id = (uint64_t*)dev_alloc(S, ng * sizeof(uint64_t), nullptr);
+      S->d_frontier = (uint64_t*)dev_alloc(S, ng * sizeof(uint64_t), nullptr);
       if (!S->d_part_obj || !S->d_part_id || !S->d_bucket_obj || !S->d_bucket_id || !S->d_best_obj ||
           !S->d_best_id || !S->d_frontier)
         rc = fail(MIST_E_NOMEM, "device allocation failed: results");
     }
     if (!rc && S->A > 0) {
       const size_t A = (size_t)S->A;
-      S->d_part_aobj = (double*)dev_alloc(S, nt * A * sizeof(double));
-      S->d_part_aid = (uint64_t*)dev_alloc(S, nt * A * sizeof(uint64_t));
-      S->d_alpha_obj = (double*)dev_alloc(S, ng * A * sizeof(double));
-      S->d_alpha_id = (uint64_t*)dev_alloc(S, ng * A * sizeof(uint64_t));
+      S->d_part_aobj = (double*)dev_alloc(S, nt * A * sizeof(double), nullptr);
+      S->d_part_aid = (uint64_t*)dev_alloc(S, nt * A * sizeof(uint64_t), nullptr);
+      S->d_alpha_obj = (double*)dev_alloc(S, ng * A * sizeof(double), nullptr);
+      S->d_alpha_id = (uint64_t*)dev_alloc(S, ng * A * sizeof(uint64_t), nullptr);
       if (!S->d_part_aobj || !S->d_part_aid || !S->d_alpha_obj || !S->d_alpha_id)
         rc = fail(MIST_E_NOMEM, "device allocation failed: weight-sample results");
+    }
+    if (!rc) {
+      // The buffers came from the null stream's blocks (mist_allocator): work queued there
+      // before them finishes before any later call uses them on another stream.
+      const hipError_t e = hipStreamSynchronize(nullptr);
+      if (e != hipSuccess) rc = fail_hip(e, "hipStreamSynchronize");
     }
     if (rc) {
       dev_free_all(S);
@@ -887,30 +894,30 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
         S->h_slab_begin[t + 1] = S->h_slab_begin[t] + ((int64_t)(T.strip_end - T.strip_begin) * R2 + div - 1) / div;
       }
       const size_t n_slab = (size_t)std::max<int64_t>(S->h_slab_begin[nt], 1);
-      S->d_filt = (FiltEntry*)dev_alloc(S, std::max<size_t>(ng, 1) * 64 * sizeof(FiltEntry));
-      S->d_cnt_tile = (int32_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int32_t));
-      S->d_tile_off = (int64_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int64_t));
-      S->d_tile_end = (int64_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int64_t));
-      S->d_list = (int32_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int32_t));
-      S->d_live = (uint8_t*)dev_alloc(S, std::max<size_t>(nt, 1));
-      S->d_seg = (int64_t*)dev_alloc(S, (ng + 1) * sizeof(int64_t));
-      S->d_seg_end = (int64_t*)dev_alloc(S, std::max<size_t>(ng, 1) * sizeof(int64_t));
-      S->d_front_cnt = (int64_t*)dev_alloc(S, std::max<size_t>(ng, 1) * sizeof(int64_t));
-      S->d_slab_begin = (int64_t*)dev_alloc(S, (nt + 1) * sizeof(int64_t));
-      S->d_slab_key = (uint64_t*)dev_alloc(S, n_slab * 8);
-      S->d_slab_obj = (double*)dev_alloc(S, n_slab * 8);
-      S->d_slab_id = (uint64_t*)dev_alloc(S, n_slab * 8);
+      S->d_filt = (FiltEntry*)dev_alloc(S, std::max<size_t>(ng, 1) * 64 * sizeof(FiltEntry), st);
+      S->d_cnt_tile = (int32_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int32_t), st);
+      S->d_tile_off = (int64_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int64_t), st);
+      S->d_tile_end = (int64_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int64_t), st);
+      S->d_list = (int32_t*)dev_alloc(S, std::max<size_t>(nt, 1) * sizeof(int32_t), st);
+      S->d_live = (uint8_t*)dev_alloc(S, std::max<size_t>(nt, 1), st);
+      S->d_seg = (int64_t*)dev_alloc(S, (ng + 1) * sizeof(int64_t), st);
+      S->d_seg_end = (int64_t*)dev_alloc(S, std::max<size_t>(ng, 1) * sizeof(int64_t), st);
+      S->d_front_cnt = (int64_t*)dev_alloc(S, std::max<size_t>(ng, 1) * sizeof(int64_t), st);
+      S->d_slab_begin = (int64_t*)dev_alloc(S, (nt + 1) * sizeof(int64_t), st);
+      S->d_slab_key = (uint64_t*)dev_alloc(S, n_slab * 8, st);
+      S->d_slab_obj = (double*)dev_alloc(S, n_slab * 8, st);
+      S->d_slab_id = (uint64_t*)dev_alloc(S, n_slab * 8, st);
       // The pool holds as many slots as all windows together (at most kPoolSlots): the windows
       // of tiles that hold no candidate stay empty, so the overflow of the others can be large.
       S->pool_cap = std::min<int64_t>(kPoolSlots, std::max<int64_t>((int64_t)n_slab, 1));
       const size_t n_pool = (size_t)S->pool_cap;
-      S->d_pool_count = (unsigned long long*)dev_alloc(S, 256);
-      S->d_pool_key = (uint64_t*)dev_alloc(S, n_pool * 8);
-      S->d_pool_obj = (double*)dev_alloc(S, n_pool * 8);
-      S->d_pool_id = (uint64_t*)dev_alloc(S, n_pool * 8);
-      S->d_pool_tile = (int32_t*)dev_alloc(S, n_pool * 4);
-      S->d_pool_rank = (int32_t*)dev_alloc(S, n_pool * 4);
-      S->d_tile_drop = (uint8_t*)dev_alloc(S, std::max<size_t>(nt, 1));
+      S->d_pool_count = (unsigned long long*)dev_alloc(S, 256, st);
+      S->d_pool_key = (uint64_t*)dev_alloc(S, n_pool * 8, st);
+      S->d_pool_obj = (double*)dev_alloc(S, n_pool * 8, st);
+      S->d_pool_id = (uint64_t*)dev_alloc(S, n_pool * 8, st);
+      S->d_pool_tile = (int32_t*)dev_alloc(S, n_pool * 4, st);
+      S->d_pool_rank = (int32_t*)dev_alloc(S, n_pool * 4, st);
+      S->d_tile_drop = (uint8_t*)dev_alloc(S, std::max<size_t>(nt, 1), st);
       {
         const size_t bytes = 8 * (2 * nt + ng + 1) + 4 * (2 * nt) + 64 + 8 + nt;
         void* p = nullptr;
@@ -1004,15 +1011,15 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
                      S->d_front_key, S->d_front_id, S->d_front_obj};
       for (void* p : old) dev_free_one(S, p);
       const size_t n = (size_t)off;
-      S->d_cand_key = (uint64_t*)dev_alloc(S, n * 8);
-      S->d_cand_id = (uint64_t*)dev_alloc(S, n * 8);
-      S->d_key_sorted = (uint64_t*)dev_alloc(S, n * 8);
-      S->d_cand_obj = (double*)dev_alloc(S, n * 8);
-      S->d_idx_in = (uint32_t*)dev_alloc(S, n * 4);
-      S->d_idx_out = (uint32_t*)dev_alloc(S, n * 4);
-      S->d_front_key = (uint64_t*)dev_alloc(S, n * 8);
-      S->d_front_id = (uint64_t*)dev_alloc(S, n * 8);
-      S->d_front_obj = (double*)dev_alloc(S, n * 8);
+      S->d_cand_key = (uint64_t*)dev_alloc(S, n * 8, st);
+      S->d_cand_id = (uint64_t*)dev_alloc(S, n * 8, st);
+      S->d_key_sorted = (uint64_t*)dev_alloc(S, n * 8, st);
+      S->d_cand_obj = (double*)dev_alloc(S, n * 8, st);
+      S->d_idx_in = (uint32_t*)dev_alloc(S, n * 4, st);
+      S->d_idx_out = (uint32_t*)dev_alloc(S, n * 4, st);
+      S->d_front_key = (uint64_t*)dev_alloc(S, n * 8, st);
+      S->d_front_id = (uint64_t*)dev_alloc(S, n * 8, st);
+      S->d_front_obj = (double*)dev_alloc(S, n * 8, st);
       S->cand_cap = off;
       if (!S->d_cand_key || !S->d_cand_id || !S->d_key_sorted || !S->d_cand_obj || !S->d_idx_in ||
           !S->d_idx_out || !S->d_front_key || !S->d_front_id || !S->d_front_obj) {
@@ -1462,9 +1469,9 @@ mist_status mist_debug_eval_tiles(mist_space* S, const int32_t* tiles, int32_t n
       const hipError_t e = hipStreamSynchronize(S->exact_stream);
       if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
     }
-    TempBuf dlist(S, (size_t)n * sizeof(int32_t));
-    TempBuf doff(S, (size_t)n * sizeof(int64_t));
-    TempBuf dout(S, (size_t)std::max<int64_t>(total, 1) * 5 * sizeof(double));
+    TempBuf dlist(S, (size_t)n * sizeof(int32_t), st);
+    TempBuf doff(S, (size_t)n * sizeof(int64_t), st);
+    TempBuf dout(S, (size_t)std::max<int64_t>(total, 1) * 5 * sizeof(double), st);
     if (!dlist.p || !doff.p || !dout.p) return fail(MIST_E_NOMEM, "device allocation failed: debug tiles");
     auto drained = [&](mist_status code) {
       (void)hipStreamSynchronize(st);

@@ -100,7 +100,7 @@ def _plan_dict(p: Plan) -> dict | None:
             "stages": [_struct_to_dict(p.stage[i]) for i in range(p.PP)]}
 
 
-ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p)
+ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p)
 FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p)
 
 
@@ -263,9 +263,10 @@ class Space:
         device = torch.cuda.current_device()
         failures = self._alloc_failures = []
 
-        def alloc(nbytes, ctx):
+        def alloc(nbytes, stream, ctx):
+            # the block joins the pool of the stream the library uses it on (NULL: the null stream)
             try:
-                return torch.cuda.caching_allocator_alloc(int(nbytes), device)
+                return torch.cuda.caching_allocator_alloc(int(nbytes), device, int(stream or 0))
             except Exception as e:  # no exception may cross the C ABI
                 failures.append(e)
                 return None

@@ -305,7 +305,7 @@ def test_allocator_failure_is_reported(torch_cuda):
         live = {}
         calls = [0]
 
-        def alloc(nbytes, ctx):
+        def alloc(nbytes, stream, ctx):
             calls[0] += 1
             if calls[0] > ok_calls:
                 return None
@@ -323,6 +323,51 @@ def test_allocator_failure_is_reported(torch_cuda):
                                  ctypes.byref(h))
         assert rc == -2 and "allocation" in L.mist_last_error().decode()
         assert not live, "buffers left behind"
+
+
+def test_allocator_sees_the_stream_of_first_use(torch_cuda):
+    """The allocator callback is told the stream each block is first used on: the null stream
+    for the space's own buffers, the call's stream for the exact frontier's buffers and the
+    temporaries of mist_eval_ids; every block is returned by mist_space_destroy."""
+    import ctypes
+    from paper_2503_19050_amd import mist
+    L = mist.load()
+    wl = W.workload("tiny")
+    S = mist.from_workload(wl)
+    model, hw, space = S._model, S._hw, S._space
+    S.close()
+    live, seen = {}, []
+
+    def alloc(nbytes, stream, ctx):
+        t = torch_cuda.empty(int(nbytes), dtype=torch_cuda.uint8, device="cuda")
+        live[t.data_ptr()] = t
+        seen.append(int(stream or 0))
+        return t.data_ptr()
+
+    def free(ptr, ctx):
+        live.pop(ptr, None)
+
+    cb = (mist.ALLOC_FN(alloc), mist.FREE_FN(free))
+    al = mist.Allocator(cb[0], cb[1], None)
+    h = ctypes.c_void_p()
+    assert L.mist_space_create(ctypes.byref(model), hw, len(wl["hws"]), ctypes.byref(space), ctypes.byref(al),
+                               ctypes.byref(h)) == 0
+    assert seen and set(seen) == {0}
+    side = torch_cuda.cuda.Stream()
+    handle = side.cuda_stream
+    del seen[:]
+    assert L.mist_eval_space(h, ctypes.c_void_p(handle)) == 0
+    assert seen == []                      # evaluation allocates nothing
+    assert L.mist_eval_pareto_exact(h, ctypes.c_void_p(handle)) == 0
+    assert seen and set(seen) == {handle}
+    del seen[:]
+    ids = np.arange(5, dtype=np.uint64)
+    out = np.empty(20)
+    assert L.mist_eval_ids(h, ids.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)), 5,
+                           out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), ctypes.c_void_p(handle)) == 0
+    assert len(seen) == 2 and set(seen) == {handle}
+    L.mist_space_destroy(h)
+    assert not live, "buffers left behind"
 
 
 @pytest.mark.parametrize("chunk", range(8))
