@@ -89,7 +89,18 @@ def test_corun_measure_and_fit(torch_cuda):
         assert x["units"] >= 0     # 0: starved for the whole window (corun_s is its length)
         assert 0.0 < x["solo_s"] < 1.0 and 0.0 < x["corun_s"] < 1.0
     phi = mist.fit_phi(samples)
-    assert np.all(np.isfinite(phi)) and np.all(phi >= 1.0) and np.all(phi < 1e4)
+    assert np.all(np.isfinite(phi)) and np.all(phi >= 1.0)
+    # The least-squares factor sum(c*s) / sum(s^2) is a weighted mean of the samples' ratios
+    # corun/solo (weights s^2), raised to 1: it lies between the smallest and the largest ratio
+    # of its (mask, stream).  A starved member's ratio is at most the co-run window over one solo
+    # unit, so the bound is the measurement's own, not a guess.
+    for mask in range(16):
+        for j in range(4):
+            r = [x["corun_s"] / x["solo_s"] for x in samples if x["mask"] == mask and x["stream"] == j]
+            if not r:
+                continue
+            lo, hi = max(1.0, min(r)), max(1.0, max(r))
+            assert lo * (1 - 1e-12) <= phi[mask][j] <= hi * (1 + 1e-12), (mask, j, r, phi[mask][j])
     say("phi[15] =", phi[15])
 
 
@@ -100,7 +111,8 @@ def test_measure_eta(torch_cuda):
     model = dict(m, hidden=1024, heads=8, kv_heads=8, ffn=4096, seq=512)
     eta, sec = mist.measure_eta(model, [1, 2, 4], tp=1, peak_flops=2.5e15, reps=3)
     assert np.all(sec > 0.0) and np.all(np.isfinite(sec))
-    assert np.all(eta > 0.0) and np.all(eta < 1.5), eta
+    # bf16 GEMMs against the bf16 dense peak: an efficiency above 1 would be a wrong count or time
+    assert np.all(eta > 0.0) and np.all(eta <= 1.0), eta
     say("eta", eta)
     with pytest.raises(mist.MistError):
         mist.measure_eta(model, [1], tp=3, peak_flops=2.5e15)
