@@ -175,6 +175,7 @@ def main() -> int:
               "(sharding the groups over several GPUs needs no exchange and is not run here)", file=sys.stderr)
         return 2
 
+    import numpy as np
     import torch
     from paper_2503_19050_amd import mist
     from paper_2503_19050_amd import workloads as W
@@ -227,9 +228,9 @@ def main() -> int:
         del src, dst
 
     t0 = time.perf_counter()
-    best = S.best()
+    best = S.best_array()
     extract_ms = (time.perf_counter() - t0) * 1e3
-    feasible = sum(1 for b in best if b["id"] != mist.MIST_NONE)
+    feasible = int(np.count_nonzero(best["id"] != np.uint64(mist.MIST_NONE)))
 
     ms_per_step = total_ms / args.steps
     value = S.n_configs / (ms_per_step / 1e3)

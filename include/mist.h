@@ -295,7 +295,9 @@ mist_status mist_get_buckets(mist_space* S, int64_t g0, int64_t n, uint64_t* ids
 mist_status mist_space_info(const mist_space* S, uint64_t* n_configs, int64_t* n_groups,
                             int32_t* n_buckets);
 
-/* Key of group g into host *out.  Errors: MIST_E_RANGE. */
+/* Key of group g (the (hw, G, PP, k, l) of one candidate stage, Sec. 5.3, and its id range)
+ * into host *out.  The group-key query of the boundary; it carries a get_ prefix because the
+ * name mist_group_key is the struct type's.  Errors: MIST_E_RANGE. */
 mist_status mist_get_group_key(const mist_space* S, int64_t g, mist_group_key* out);
 
 /* Decodes a global id into host *out (host-side arithmetic only).  Errors: MIST_E_RANGE. */

@@ -201,6 +201,16 @@ def _struct_to_dict(s) -> dict:
     return out
 
 
+def _results_to_dicts(out, n: int) -> list[dict]:
+    """mist_result array -> list of dicts, through one numpy view (no per-field ctypes access)."""
+    if n == 0:
+        return []
+    rows = np.ctypeslib.as_array(out)[:n].tolist()
+    names = [f for f, _ in Result._fields_[:-1]]
+    cnames = [f for f, _ in Config._fields_]
+    return [dict(zip(names, r[:-1]), cfg=dict(zip(cnames, r[-1]))) for r in rows]
+
+
 def _stream_handle(stream):
     if stream is None:
         import torch
@@ -307,15 +317,23 @@ class Space:
     # -- results ------------------------------------------------------------------
     def best(self, g0: int = 0, n: int | None = None) -> list[dict]:
         n = self.n_groups - g0 if n is None else n
+        return _results_to_dicts(self._best_raw(g0, n), n)
+
+    def best_array(self, g0: int = 0, n: int | None = None) -> np.ndarray:
+        """best() as a numpy structured array (the mist_result layout), without per-group dicts."""
+        n = self.n_groups - g0 if n is None else n
+        return np.ctypeslib.as_array(self._best_raw(g0, n))[:n]
+
+    def _best_raw(self, g0: int, n: int):
         out = (Result * max(n, 1))()
         _check(self.L, self.L.mist_get_best(self.h, g0, n, out))
-        return [_struct_to_dict(out[i]) for i in range(n)]
+        return out
 
     def pareto(self, g: int) -> list[dict]:
         out = (Result * 64)()
         cnt = ctypes.c_int32()
         _check(self.L, self.L.mist_get_pareto(self.h, g, out, 64, ctypes.byref(cnt)))
-        return [_struct_to_dict(out[i]) for i in range(cnt.value)]
+        return _results_to_dicts(out, cnt.value)
 
     def eval_pareto_exact(self, stream=None) -> None:
         """Exact (non-bucketed) time-vs-memory frontier of every group; after eval()."""
@@ -332,7 +350,7 @@ class Space:
                 cap = n.value
                 continue
             _check(self.L, rc)
-            return [_struct_to_dict(out[i]) for i in range(n.value)]
+            return _results_to_dicts(out, n.value)
 
     def exact_group_sizes(self, g0: int = 0, n: int | None = None) -> tuple[np.ndarray, np.ndarray]:
         """Per-group candidates and pre-filter survivors of the last exact frontier."""
@@ -365,7 +383,8 @@ class Space:
         A = self.n_alphas
         out = (Result * max(n * A, 1))()
         _check(self.L, self.L.mist_get_alpha(self.h, g0, n, out))
-        return [[_struct_to_dict(out[i * A + a]) for a in range(A)] for i in range(n)]
+        flat = _results_to_dicts(out, n * A)
+        return [flat[i * A:(i + 1) * A] for i in range(n)]
 
     def buckets(self, g0: int = 0, n: int | None = None):
         """(ids[n, NB], objs[n, NB], frontier masks[n]) of groups g0..g0+n-1."""

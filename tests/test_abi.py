@@ -132,3 +132,21 @@ def test_random_small_spaces_are_valid():
         o = O.Oracle(W.random_space(seed))
         small += o.n_configs <= 1_500_000
     assert small >= 170
+
+
+def test_result_conversion_matches_field_access():
+    """The binding's numpy-view conversion of mist_result arrays gives the same dicts as reading
+    every ctypes field."""
+    import ctypes
+    n = 7
+    out = (mist.Result * n)()
+    for i in range(n):
+        out[i].id = 1000 + i
+        out[i].obj = 0.5 * i
+        out[i].t, out[i].d, out[i].mem = 1.0 + i, -0.25 * i, 3e9 + i
+        out[i].bucket = i - 1
+        out[i].cfg.hw, out[i].cfg.G, out[i].cfg.PP, out[i].cfg.ckpt = i, 2 * i, 4, i % 3
+        out[i].cfg.ao, out[i].cfg.ao_idx = 0.125 * i, i
+    assert mist._results_to_dicts(out, n) == [mist._struct_to_dict(out[i]) for i in range(n)]
+    assert mist._results_to_dicts(out, 0) == []
+    assert mist._results_to_dicts(out, 3) == [mist._struct_to_dict(out[i]) for i in range(3)]
