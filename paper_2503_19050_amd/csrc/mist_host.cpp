@@ -985,7 +985,10 @@ mist_status mist_eval_pareto_exact(mist_space* S, void* hip_stream) {
     if (e == hipSuccess) e = copy_async(S->h_pool_count, S->d_pool_count, 8, hipMemcpyDeviceToHost, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     if (e != hipSuccess) return fail_hip(e, "exact frontier: counts");
-    const int64_t n_pool = std::min<int64_t>((int64_t)*S->h_pool_count, S->pool_cap);
+    // The pool counter is cleared by the pair-constants kernel.  A space without pairs has no
+    // tile: neither that kernel nor the candidate pass runs, the counter keeps whatever its
+    // block held, and the pool is empty.
+    const int64_t n_pool = ea.n_pk > 0 ? std::min<int64_t>((int64_t)*S->h_pool_count, S->pool_cap) : 0;
     // Candidate slots in group order: a group's full-size tiles, then its small ones.  Tiles with
     // a candidate that found no place (its window and the pool full) are listed for pass 2.
     S->n_list = 0;

@@ -102,6 +102,27 @@ def test_exact_and_plan_states(torch_cuda):
     S.close()
 
 
+def test_exact_frontier_of_an_empty_space_on_reused_blocks(torch_cuda):
+    """A space without configurations launches no kernel of the candidate pass, so nothing
+    clears the overflow pool's counter: its count must not be read from the block, whatever the
+    allocator's block held before (here blocks just freed with every byte 0x01)."""
+    from paper_2503_19050_amd import mist
+    wl = W.random_space(158)
+    assert O.Oracle(wl).n_configs == 0
+    for _ in range(3):
+        junk = [torch_cuda.full((n,), 1, dtype=torch_cuda.uint8, device="cuda") for n in (256, 512, 4096) * 64]
+        torch_cuda.cuda.synchronize()
+        del junk
+        S = mist.from_workload(wl)
+        S.eval()
+        S.eval_pareto_exact()
+        torch_cuda.cuda.synchronize()
+        info = S.exact_info()
+        assert info["candidates"] == 0 and info["kept"] == 0 and info["tiles_again"] == 0, info
+        assert S.n_groups == 0
+        S.close()
+
+
 @pytest.mark.parametrize("name", ["tight", "gpt1.3b-d8", "gpt2.7b-d16"])
 def test_candidate_windows_do_not_change_results(name, torch_cuda):
     """The frontier does not depend on the candidate windows: windows as large as their tiles
