@@ -25,6 +25,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "candidate configs evaluated/sec (eval+filter+reduce); % of FP64 vector peak"
 FP64_VECTOR_PEAK_TFLOPS = 78.6   # 256 CUs x 128 FP64 FLOP/clk (64 FMA lanes) x 2.4 GHz
+# VALU issue: 256 CUs x 4 SIMDs, one wave64 VALU instruction per SIMD every 4 clocks at 2.4 GHz
+VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4
 FLOPS_FILE = os.path.join(ROOT, "tests", "golden", "flops_per_config.json")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2503_19050_amd", "csrc", "mist_kernels.hip")
@@ -51,10 +53,11 @@ def flops_per_config(name: str):
         return None, None
 
 
-def counter_record(name: str):
-    """FP64 operations the evaluation kernel executes per configuration, from the committed
-    rocprofv3 instruction counters (64 x (ADD + MUL + TRANS + 2 FMA) F64 wave instructions per
-    configuration), if they were taken on the current kernel source."""
+def counter_record(name: str, field: str = "executed_fp64_per_config"):
+    """A per-configuration figure of the evaluation kernel from the committed rocprofv3
+    instruction counters, if they were taken on the current kernel source:
+    executed_fp64_per_config = 64 x (ADD + MUL + TRANS + 2 FMA) F64 wave instructions per
+    configuration, valu_per_config = 64 x SQ_INSTS_VALU per configuration."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)[name]
@@ -62,7 +65,7 @@ def counter_record(name: str):
         return None
     if rec.get("kernel_sha") != kernel_hash():
         return None
-    return rec.get("executed_fp64_per_config")
+    return rec.get(field)
 
 
 def traffic_record(name: str, n_launch_configs: int):
@@ -256,6 +259,12 @@ def main() -> int:
         if executed is not None:
             roofline["executed_fp64_per_config"] = executed
             roofline["frac_executed"] = executed * S.n_configs / (k1_avg / 1e3) / 1e12 / FP64_VECTOR_PEAK_TFLOPS
+        valu = counter_record(wl["name"], "valu_per_config")
+        if valu is not None:
+            # The issue limit the kernel meets: executed wave64 VALU instructions per second
+            # against the chip's issue rate.
+            roofline["valu_per_config"] = valu
+            roofline["valu_issue_frac"] = valu * S.n_configs / 64 / (k1_avg / 1e3) / VALU_ISSUE_PEAK
 
     exact = None
     if args.exact_runs > 0:

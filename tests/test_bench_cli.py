@@ -55,11 +55,24 @@ def test_cpu_baseline_record():
 
 
 def test_counter_record_only_for_the_kernel_it_was_measured_on(monkeypatch, tmp_path):
-    rec = {"w": {"kernel_sha": "abc", "executed_fp64_per_config": 50.0}}
+    rec = {"w": {"kernel_sha": "abc", "executed_fp64_per_config": 50.0, "valu_per_config": 90.0}}
     p = tmp_path / "t.json"
     p.write_text(json.dumps(rec))
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(p))
     monkeypatch.setattr(bench, "kernel_hash", lambda: "abc")
     assert bench.counter_record("w") == 50.0
+    assert bench.counter_record("w", "valu_per_config") == 90.0
     monkeypatch.setattr(bench, "kernel_hash", lambda: "abd")
     assert bench.counter_record("w") is None
+    assert bench.counter_record("w", "valu_per_config") is None
+
+
+def test_committed_counter_records_match_the_kernel_source():
+    """profiles/traffic.json holds the headline workload's record, taken on the committed kernel
+    source: the bench line's traffic and counter figures are then not null."""
+    with open(bench.TRAFFIC_FILE) as f:
+        rec = json.load(f)["llama42b-d128-hw64"]
+    assert rec["kernel_sha"] == bench.kernel_hash()
+    assert bench.traffic_record("llama42b-d128-hw64", 0) == rec["bytes_per_launch"]
+    assert rec["fetch_bytes"] + rec["write_bytes"] == rec["bytes_per_launch"]
+    assert 50.0 < rec["executed_fp64_per_config"] < rec["valu_per_config"] < 200.0
