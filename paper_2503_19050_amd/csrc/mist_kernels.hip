@@ -235,18 +235,21 @@ __device__ __forceinline__ double interference(double c, double g, double h, dou
 
 // Calls whose first round uses a row known in advance: every configuration of a strip whose host
 // streams both run (pattern 15, or 13 without GPU-GPU traffic), with compute c and GPU-GPU g fixed
-// per strip.  The strip precomputes the scaled c and g, their minimum m01, and what streams 0 and 1
-// contribute to the second round's row.  After the first round a member keeps running exactly
-// when its scaled time exceeds the overlap (s_j - ov > 0, and (s_j - ov) * psi_j cannot round to
-// zero: the host's input bounds keep every non-zero stream time and difference far above the
-// subnormal range), so the second row follows from three comparisons instead of four on the
-// updated times: streams 0 and 1 both keep running when ov < m01, and those above m01 when
-// ov == m01 (ov <= m01 always).
+// per strip.  The strip precomputes the scaled c and g and their minimum m01.
+//
+// After the first round a member keeps running exactly when its scaled time exceeds the overlap
+// (s_j - ov > 0, and (s_j - ov) * psi_j cannot round to zero: the host's input bounds keep every
+// non-zero stream time and difference far above the subnormal range).  In the common case the
+// GPU-GPU stream is a member and its scaled time s1 is below every other member's: the overlap is
+// s1 itself, compute, host->device and device->host keep running, and the second round reads
+// row 13 for every such configuration, with compute's second-round scaled time y0 fixed per
+// strip.  A wave all of whose lanes are in that case takes the wave-uniform row (rounds_after_g1);
+// any other wave runs the general rounds with rows looked up per lane.
 struct KnownRow {
   double s0, s1, m01;   // c * phi0, g * phi1 (NaN when GPU-GPU is no member), min of the two
-  double f2, f3, p0, p1, p2, p3;
-  const char* row_lt;   // the table plus the second-row offset of streams 0 and 1 for ov < m01
-  const char* row_eq;   // and for ov == m01
+  double y0;            // when s1 < s0: compute's scaled time in the second round (row 13)
+  const double* row;    // the first round's row
+  double s1g;           // s1 when GPU-GPU is a member and s1 < s0, else +inf (pattern 13: s1 is NaN)
 };
 
 __device__ __forceinline__ KnownRow known_row(const double* __restrict__ tab, int pattern, double c, double g) {
@@ -255,33 +258,82 @@ __device__ __forceinline__ KnownRow known_row(const double* __restrict__ tab, in
   r.s0 = c * e[0];
   r.s1 = g * e[1];
   r.m01 = __builtin_fmin(r.s0, r.s1);
-  r.f2 = e[2];
-  r.f3 = e[3];
-  r.p0 = e[4];
-  r.p1 = e[5];
-  r.p2 = e[6];
-  r.p3 = e[7];
-  constexpr int kRowBytes = kLdsRow * (int)sizeof(double);
-  const char* t = reinterpret_cast<const char*>(tab);
-  r.row_lt = t + (pattern & 3) * kRowBytes;
-  r.row_eq = t + ((pattern & 1) && r.s0 > r.m01 ? kRowBytes : 0) + ((pattern & 2) && r.s1 > r.m01 ? 2 * kRowBytes : 0);
+  r.row = e;
+  r.s1g = r.s1 < r.s0 ? r.s1 : __builtin_huge_val();
+  r.y0 = ((r.s0 - r.s1) * e[4]) * tab[13 * kLdsRow + 0];
   return r;
 }
 
-// Host streams h, d > 0 of such a call: first round with the known row, second with the row
-// derived above, third looked up.
-__device__ __forceinline__ double interference_known(const KnownRow& r, double h, double d,
-                                                     const double* __restrict__ tab) {
-  const double s2 = h * r.f2, s3 = d * r.f3;
+// The second and third rounds of a call whose first round (row 15) ended GPU-GPU alone.  The
+// same operations on the same operands as the general rounds below, with GPU-GPU's time (NaN from
+// row 13's +inf factor) left out of the minima and the maximum it cannot win.
+__device__ __forceinline__ double rounds_after_g1(const KnownRow& r, double s2, double s3,
+                                                  const double* __restrict__ tab) {
+  const double* e15 = tab + 15 * kLdsRow;
+  const double* e13 = tab + 13 * kLdsRow;
+  const double y0 = r.y0;
+  const double y2 = ((s2 - r.s1) * e15[6]) * e13[2];
+  const double y3 = ((s3 - r.s1) * e15[7]) * e13[3];
+  const double ov2 = __builtin_fmin(y0, __builtin_fmin(y2, y3));
+  const double T2 = r.s1 + ov2;
+  // Third round: the row of the streams still running, those whose scaled time exceeds the
+  // overlap.
+  const bool q0 = y0 > ov2, q2 = y2 > ov2, q3 = y3 > ov2;
+  const double z0 = (y0 - ov2) * e13[4], z2 = (y2 - ov2) * e13[6], z3 = (y3 - ov2) * e13[7];
+  const double* e = tab + ((q0 ? 1 : 0) + (q2 ? 4 : 0) + (q3 ? 8 : 0)) * kLdsRow;
+  const double w0 = z0 * e[0], w2 = z2 * e[2], w3 = z3 * e[3];
+  const double ov3 = __builtin_fmin(__builtin_fmin(w0, w2), w3);
+  const double rem = __builtin_fmax(__builtin_fmax((w0 - ov3) * e[4], (w2 - ov3) * e[6]), (w3 - ov3) * e[7]);
+  return (T2 + ov3) + rem;
+}
+
+// General rounds of such a call with host streams h, d > 0: the first with the known row, the
+// others looked up by the lanes' patterns.
+__device__ __forceinline__ double interference_general(const KnownRow& r, double h, double d,
+                                                       const double* __restrict__ tab) {
+  const double* e = r.row;
+  const double s2 = h * e[2], s3 = d * e[3];
   const double ov = __builtin_fmin(r.m01, __builtin_fmin(s2, s3));
-  Streams x{(r.s0 - ov) * r.p0, (r.s1 - ov) * r.p1, (s2 - ov) * r.p2, (s3 - ov) * r.p3};
-  constexpr int kRowBytes = kLdsRow * (int)sizeof(double);
-  const double* e = reinterpret_cast<const double*>((ov < r.m01 ? r.row_lt : r.row_eq) + (s2 > ov ? 4 * kRowBytes : 0) +
-                                                    (s3 > ov ? 8 * kRowBytes : 0));
+  Streams x{(r.s0 - ov) * e[4], (r.s1 - ov) * e[5], (s2 - ov) * e[6], (s3 - ov) * e[7]};
   double T = ov;
-  T = T + round_row(x, e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]);
+  T = T + round_lookup<kLdsRow>(x, tab);
   T = T + round_lookup<kLdsRow>(x, tab);
   return T + remaining(x);
+}
+
+// Algorithm 1 for the first n of the N configurations of an activation-ratio block (host streams
+// h[c], d[c]), all with the strip's known first-round row.  One wave-uniform decision per
+// sub-block of SB configurations: when GPU-GPU finishes first and alone in every lane and
+// configuration of the sub-block, the rounds after it (rounds_after_g1), else the general rounds,
+// so that either path is straight-line code.  Configurations with free[c] set (their result is
+// replaced by the caller) do not take part in the decision.
+template <int N, int SB>
+__device__ __forceinline__ void interference_known_n(const KnownRow& r, const double (&h)[N], const double (&d)[N],
+                                                     const bool (&free)[N], double (&out)[N], int n,
+                                                     const double* __restrict__ tab) {
+  const double* e15 = tab + 15 * kLdsRow;  // the first-round row of every lane with a finite s1g
+#pragma unroll
+  for (int c0 = 0; c0 < N; c0 += SB) {
+    if (c0 >= n) break;
+    double s2[SB], s3[SB];
+    bool ok = true;
+#pragma unroll
+    for (int c = 0; c < SB; ++c) {
+      if (c0 + c >= n) break;
+      s2[c] = h[c0 + c] * e15[2];
+      s3[c] = d[c0 + c] * e15[3];
+      ok = ok & (free[c0 + c] | (__builtin_fmin(s2[c], s3[c]) > r.s1g));
+    }
+    if (__builtin_amdgcn_ballot_w64(ok) == __builtin_amdgcn_read_exec()) {
+#pragma unroll
+      for (int c = 0; c < SB; ++c)
+        if (c0 + c < n) out[c0 + c] = rounds_after_g1(r, s2[c], s3[c], tab);
+    } else {
+#pragma unroll
+      for (int c = 0; c < SB; ++c)
+        if (c0 + c < n) out[c0 + c] = interference_general(r, h[c0 + c], d[c0 + c], tab);
+    }
+  }
 }
 
 // Algorithm 1 on (c, g, +0, +0), c > 0: the first round uses the row of pattern 3 (compute and
@@ -404,8 +456,19 @@ __device__ __forceinline__ void pool_holes(const EvalArgs& a, unsigned long long
 
 // Activation ratios per block of the strip loop: a block keeps its stable times and the
 // per-ratio terms of its configurations in registers across the optimizer ratios.
-template <int R>
-constexpr int ia_block() { return R <= 6 ? R : (R + 2) / 3; }
+// Weight samples take larger blocks for 7 <= R <= 10 (at R = 9, 79.5 against 85.2 ms for 8
+// samples on the 64-hardware-sample Llama space).
+template <int R, int MODE>
+constexpr int ia_block() {
+  return R <= 6 ? R : (MODE == kModeAlpha && R <= 10 ? (R + 1) / 2 : (R + 2) / 3);
+}
+
+// Configurations per wave-uniform interference decision (interference_known_n).  One decision per
+// configuration measured fastest (against one per block or per half block: 0.81 against 1.16 and
+// 1.02 ms on gpt2.7b-d16, equal on the Llama spaces); the stable times and the first-microbatch
+// times of a block are still formed together, ahead of the block's reductions.
+template <int R, int MODE>
+constexpr int decide_block() { return 1; }
 
 // Waves per SIMD the register allocation aims at: four, the most the LDS use of a block
 // allows (a few strip-level values spill; the occupancy is worth more).  The exact frontier's
@@ -426,7 +489,8 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
   constexpr bool DM = MODE == kModeDump;
   constexpr int R2 = R * R;
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
-  constexpr int IB = ia_block<R>();
+  constexpr int IB = ia_block<R, MODE>();
+  constexpr int SB = decide_block<R, MODE>();
   __shared__ double s_tab[kWaves][16 * kLdsRow];
   __shared__ BucketEntry s_bucket[kWaves][65];  // entries NB..64: sinks of infeasible configurations
   __shared__ OoIn s_oo[kBlock];         // per-lane strip constants of the optimizer level
@@ -548,16 +612,31 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
 #pragma unroll
       for (int ib = 0; ib < R; ib += IB) {
         // Stable time per activation ratio (it does not depend on the optimizer ratio).
+        const int nb = R - ib < IB ? R - ib : IB;  // configurations of the block
         const KnownRow sr = known_row(tab, pats, K.C, Z.G2Gs);
         double tt[IB];
+        {
+          double hs[IB], ds[IB];
+          bool fs[IB];
 #pragma unroll
-        for (int c = 0; c < IB; ++c) {
-          const int ia = ib + c;
-          if (ia >= R) break;
-          const double H2Ds = __builtin_fma(rr[ia], K.A, W.HW) * iP;
-          const double D2Hs = __builtin_fma(rr[ia], K.A, W.DG) * iP;
-          if (ia == 0 && r0_zero) tt[c] = interference(K.C, Z.G2Gs, H2Ds, D2Hs, tab);
-          else tt[c] = interference_known(sr, H2Ds, D2Hs, tab);
+          for (int c = 0; c < IB; ++c) {
+            const int ia = ib + c;
+            if (ia >= R) break;
+            hs[c] = __builtin_fma(rr[ia], K.A, W.HW) * iP;
+            ds[c] = __builtin_fma(rr[ia], K.A, W.DG) * iP;
+            fs[c] = ia == 0 && r0_zero;
+          }
+          interference_known_n<IB, SB>(sr, hs, ds, fs, tt, nb, tab);
+          // Activation ratio 0 leaves the host streams to the weights and gradients alone: the
+          // first round's pattern is not known in advance.
+          if (ib == 0 && r0_zero) tt[0] = interference(K.C, Z.G2Gs, hs[0], ds[0], tab);
+        }
+        // Weight samples: the block's smallest stable time, for the lower bound below.
+        [[maybe_unused]] double t_min = tt[0];
+        if constexpr (AL) {
+#pragma unroll
+          for (int c = 1; c < IB; ++c)
+            if (ib + c < R) t_min = __builtin_fmin(t_min, tt[c]);
         }
 
 #pragma unroll 1
@@ -567,6 +646,20 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
           const unsigned int lid_oo = lid_strip + (unsigned int)(io * R);
           [[maybe_unused]] double dn_blk[AL ? IB : 1];  // weight samples: the block's deltas (NaN
                                                         // when infeasible)
+          double T1b[IB];
+          {
+            double hf[IB], df[IB];
+            bool fz[IB];
+#pragma unroll
+            for (int c = 0; c < IB; ++c) {
+              const int ia = ib + c;
+              if (ia >= R) break;
+              hf[c] = __builtin_fma(rr[ia], A, HW) * iP + O.H2Dx;
+              df[c] = __builtin_fma(rr[ia], A, DG) * iP + O.D2Hx;
+              fz[c] = ia == 0 && zero_oo;
+            }
+            interference_known_n<IB, SB>(fr, hf, df, fz, T1b, nb, tab);
+          }
 #pragma unroll
           for (int c = 0; c < IB; ++c) {
             const int ia = ib + c;
@@ -574,9 +667,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             const double ra = rr[ia];
             const double SO = __builtin_fma(ra, A2, om[ia] * KA);  // stash + offload buffers
             const double mem = O.Bmax + SO;
-            const double H2Df = __builtin_fma(ra, A, HW) * iP + O.H2Dx;
-            const double D2Hf = __builtin_fma(ra, A, DG) * iP + O.D2Hx;
-            double T1 = interference_known(fr, H2Df, D2Hf, tab);
+            double T1 = T1b[c];
             if (ia == 0) T1 = zero_oo ? T1z : T1;
             const double tv = tt[c];
             const double d = T1 - tv;
@@ -698,12 +789,25 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             // sample's values read once for the block; the exact sequence only when some lane
             // of the wave may win.  All lanes address the sample's single entry; the same
             // three-step LDS sequence as the buckets' keeps the lexicographic minimum.
+            //
+            // Before that, one bound per sample and block: with a = alpha*G >= 0 and
+            // b = 1 - alpha >= 0, fma(a, t, b*d) is non-decreasing in t and d under rounding to
+            // nearest, so fma(a, t_min, b*d_min) over the block's smallest t and smallest
+            // feasible d is at most every feasible configuration's value.  A sample whose bound
+            // exceeds its entry on every lane cannot be won by the block, and its per-
+            // configuration values are not formed (NaN deltas drop out of the minimum; a block
+            // without a feasible configuration has a NaN bound, which compares false).
             wave_sync();
+            double d_min = dn_blk[0];
+#pragma unroll
+            for (int c = 1; c < IB; ++c)
+              if (ib + c < R) d_min = __builtin_fmin(d_min, dn_blk[c]);
             unsigned int qmask = 0;  // samples some lane of the wave may win
 #pragma unroll 1
             for (int q = 0; q < a.n_alpha; ++q) {
               const double2 ab = s_ab[wave][q];
               const double cur = lds_load(&s_aent[wave][q].val);
+              if (!__builtin_amdgcn_ballot_w64(__builtin_fma(ab.x, t_min, ab.y * d_min) <= cur)) continue;
               bool any = false;
 #pragma unroll
               for (int c = 0; c < IB; ++c) {
