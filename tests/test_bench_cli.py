@@ -75,4 +75,10 @@ def test_committed_counter_records_match_the_kernel_source():
     assert rec["kernel_sha"] == bench.kernel_hash()
     assert bench.traffic_record("llama42b-d128-hw64", 0) == rec["bytes_per_launch"]
     assert rec["fetch_bytes"] + rec["write_bytes"] == rec["bytes_per_launch"]
-    assert 50.0 < rec["executed_fp64_per_config"] < rec["valu_per_config"] < 200.0
+    # The kernel shares more work than the oracle's loop nest, so it executes fewer FP64
+    # operations than the algorithmic unit, but at least a configuration's own: the host streams
+    # of its first microbatch, at least two interference rounds on them, its memory, bucket index,
+    # delta and objective (above 30 with fma counted as 2).
+    flops, _ = bench.flops_per_config("llama42b-d128-hw64")
+    assert 30.0 < rec["executed_fp64_per_config"] < flops
+    assert rec["executed_fp64_per_config"] < rec["valu_per_config"] < 200.0
