@@ -67,6 +67,7 @@ struct mist_space {
   std::vector<DevGroup> groups;
   std::vector<DevPair> pairs;
   std::vector<DevTile> tiles;
+  std::vector<int32_t> tile_order;  // work item -> tile (build_tile_order)
   std::vector<DevHw> hws;
   std::vector<int32_t> pk_group;  // group of each pair-constant entry
   DevModel dm;
@@ -79,6 +80,7 @@ struct mist_space {
   DevGroup* d_groups = nullptr;
   DevPair* d_pairs = nullptr;
   DevTile* d_tiles = nullptr;
+  int32_t* d_tile_order = nullptr;
   DevHw* d_hws = nullptr;
   double* d_ratio = nullptr;
   PairK* d_pk = nullptr;
@@ -490,6 +492,7 @@ mist::EvalArgs eval_args(const mist_space* S) {
   a.groups = S->d_groups;
   a.pairs = S->d_pairs;
   a.tiles = S->d_tiles;
+  a.tile_order = S->d_tile_order;
   a.hws = S->d_hws;
   a.ratio = S->d_ratio;
   a.R = S->R;
@@ -672,6 +675,49 @@ std::string build_tiles(mist_space* S, int64_t resident_waves) {
   return "";
 }
 
+// Work items of the persistent evaluation grid in tile order per XCD.  Item i < n_waves is the
+// first tile of wave i, whose block b = i / kWaves runs on XCD b mod kClaimCounters (blocks are
+// dealt to the XCDs in turn); item n_waves + x + kClaimCounters * c is claim c on counter x, which
+// the waves of XCD x draw from first.  Each XCD's items are given a contiguous range of the
+// full-size tiles followed by a contiguous range of the small ones, in proportion to its item
+// count: the pair constants, group records and hardware tables of neighbouring tiles are then
+// reused from that XCD's L2, and each XCD still ends on small tiles.  Any permutation gives the
+// same results; this one only decides which tiles share a cache.  Spaces of at most one tile
+// per wave need no claims and keep item x = tile x.
+std::string build_tile_order(mist_space* S, int64_t n_waves, int32_t n_full) {
+  const int64_t n = (int64_t)S->tiles.size();
+  S->tile_order.resize((size_t)n);
+  for (int64_t i = 0; i < n; ++i) S->tile_order[(size_t)i] = (int32_t)i;
+  if (n <= n_waves) return "";
+  int64_t cnt[kClaimCounters] = {};
+  for (int64_t i = 0; i < n_waves; ++i) ++cnt[(i / kWaves) % kClaimCounters];
+  for (int64_t i = n_waves; i < n; ++i) ++cnt[(i - n_waves) % kClaimCounters];
+  // XCD x takes full-size tiles [fc[x], fc[x+1]) and small tiles n_full + [sc[x], sc[x+1]); both
+  // cumulative counts are non-decreasing and fc[x+1] - fc[x] + sc[x+1] - sc[x] = cnt[x].
+  int64_t fc[kClaimCounters + 1], sc[kClaimCounters + 1], cum = 0;
+  for (int x = 0; x <= kClaimCounters; ++x) {
+    fc[x] = (int64_t)((__int128)n_full * cum / n);
+    sc[x] = cum - fc[x];
+    if (x < kClaimCounters) cum += cnt[x];
+  }
+  int64_t pos[kClaimCounters] = {};
+  const auto next = [&](int x) -> int32_t {
+    const int64_t k = pos[x]++;
+    const int64_t nf = fc[x + 1] - fc[x];
+    return (int32_t)(k < nf ? fc[x] + k : n_full + sc[x] + (k - nf));
+  };
+  for (int64_t i = 0; i < n_waves; ++i) S->tile_order[(size_t)i] = next((int)((i / kWaves) % kClaimCounters));
+  for (int64_t i = n_waves; i < n; ++i) S->tile_order[(size_t)i] = next((int)((i - n_waves) % kClaimCounters));
+  // A permutation of the tiles, or the kernel would skip or repeat one.
+  std::vector<uint8_t> seen((size_t)n, 0);
+  for (int64_t i = 0; i < n; ++i) {
+    const int32_t t = S->tile_order[(size_t)i];
+    if (t < 0 || t >= n || seen[(size_t)t]) return "tile order is not a permutation";
+    seen[(size_t)t] = 1;
+  }
+  return "";
+}
+
 }  // namespace
 
 extern "C" {
@@ -733,11 +779,18 @@ mist_status mist_space_create(const mist_model_desc* m, const mist_hw_desc* hw, 
     if (!rc) {
       const int64_t waves_needed = (int64_t)(S->tiles.size() + kWaves - 1) / kWaves;
       S->eval_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>(resident_blocks, waves_needed));
-      for (const DevGroup& G : S->groups) S->max_group_tiles = std::max(S->max_group_tiles, G.n_tiles + G.n_tail);
+      int32_t n_full = 0;
+      for (const DevGroup& G : S->groups) {
+        S->max_group_tiles = std::max(S->max_group_tiles, G.n_tiles + G.n_tail);
+        n_full += G.n_tiles;
+      }
+      const std::string oerr = build_tile_order(S, (int64_t)S->eval_grid * kWaves, n_full);
+      if (!oerr.empty()) rc = fail(MIST_E_INVALID, oerr);
     }
     if (!rc) rc = upload(S, &S->d_groups, S->groups, "groups");
     if (!rc) rc = upload(S, &S->d_pairs, S->pairs, "pairs");
     if (!rc) rc = upload(S, &S->d_tiles, S->tiles, "tiles");
+    if (!rc) rc = upload(S, &S->d_tile_order, S->tile_order, "tile order");
     if (!rc) rc = upload(S, &S->d_hws, S->hws, "hardware tables");
     if (!rc) rc = upload(S, &S->d_ratio, S->ratio_om, "ratios");
     if (!rc) rc = upload(S, &S->d_pk_group, S->pk_group, "pair groups");

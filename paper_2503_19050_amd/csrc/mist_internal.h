@@ -97,6 +97,8 @@ struct EvalArgs {
   const DevGroup* groups;
   const DevPair* pairs;
   const DevTile* tiles;
+  const int32_t* tile_order;  // [n_tiles] work item -> tile of the persistent grid (nullptr:
+                              // item x is tile x)
   const DevHw* hws;
   const double* ratio;   // r[0..R), then om[0..R) = 1 - r
   int32_t R, NB;

@@ -515,8 +515,8 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
   // * c goes to the claim that draws number c from counter x (counters reset to 0 by K0); a
   // wave draws from the counter of its block's XCD and moves to the next counter when one
   // runs out, until all have.  When the grid has at least as many waves as there are items
-  // no claim is made.  Item x is tile x, or tile tile_list[x] when the emit variant runs a
-  // list.
+  // no claim is made.  Item x is tile tile_order[x] (the host gives each XCD's items a
+  // contiguous range of tiles), or tile tile_list[x] when a variant runs a list.
   const bool listed = (EX || DM) && a.tile_list != nullptr;
   const int n_items = listed ? a.n_list : a.n_tiles;
   const int n_waves = (int)gridDim.x * kWaves;
@@ -528,7 +528,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
   unsigned long long pool_base = 0;
   int pool_used = kPoolChunk;
   for (int x = (int)blockIdx.x * kWaves + wave; x < n_items;) {
-    const int t = listed ? load_uniform(a.tile_list + x) : x;
+    const int t = listed ? load_uniform(a.tile_list + x) : (a.tile_order ? load_uniform(a.tile_order + x) : x);
     const DevTile tile = load_uniform(a.tiles + t);
     // The exact frontier's pass skips a tile that holds no candidate (its count stays 0).
     const int strip_end = EX && a.tile_live && !a.tile_live[t] ? tile.strip_begin : tile.strip_end;
