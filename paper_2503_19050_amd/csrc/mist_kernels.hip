@@ -306,8 +306,9 @@ __device__ __forceinline__ double interference_general(const KnownRow& r, double
 // sub-block of SB configurations: when GPU-GPU finishes first and alone in every lane and
 // configuration of the sub-block, the rounds after it (rounds_after_g1), else the general rounds,
 // so that either path is straight-line code.  Configurations with free[c] set (their result is
-// replaced by the caller) do not take part in the decision.
-template <int N, int SB>
+// replaced or unused by the caller) do not take part in the decision; with SKIP a sub-block free
+// in every lane is not evaluated (its results are NaN).
+template <int N, int SB, bool SKIP = false>
 __device__ __forceinline__ void interference_known_n(const KnownRow& r, const double (&h)[N], const double (&d)[N],
                                                      const bool (&free)[N], double (&out)[N], int n,
                                                      const double* __restrict__ tab) {
@@ -324,7 +325,17 @@ __device__ __forceinline__ void interference_known_n(const KnownRow& r, const do
       s3[c] = d[c0 + c] * e15[3];
       ok = ok & (free[c0 + c] | (__builtin_fmin(s2[c], s3[c]) > r.s1g));
     }
-    if (__builtin_amdgcn_ballot_w64(ok) == __builtin_amdgcn_read_exec()) {
+    bool busy = !SKIP;  // some lane's result is used
+    if constexpr (SKIP) {
+#pragma unroll
+      for (int c = 0; c < SB; ++c)
+        if (c0 + c < n) busy = busy | !free[c0 + c];
+    }
+    if (SKIP && !__builtin_amdgcn_ballot_w64(busy)) {  // every lane's result is unused: none is formed
+#pragma unroll
+      for (int c = 0; c < SB; ++c)
+        if (c0 + c < n) out[c0 + c] = __builtin_nan("");
+    } else if (__builtin_amdgcn_ballot_w64(ok) == __builtin_amdgcn_read_exec()) {
 #pragma unroll
       for (int c = 0; c < SB; ++c)
         if (c0 + c < n) out[c0 + c] = rounds_after_g1(r, s2[c], s3[c], tab);
@@ -608,7 +619,9 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
 
       // Activation ratios in blocks of IB: the values a block keeps across the optimizer
       // ratios fit the registers, at the price of one more optimizer-level evaluation per
-      // block.
+      // block.  A block's stable times, and per optimizer ratio its first-microbatch times, are
+      // formed before its memory, objective and reduction steps, so that the interference rounds
+      // of its configurations are straight-line code.
 #pragma unroll
       for (int ib = 0; ib < R; ib += IB) {
         // Stable time per activation ratio (it does not depend on the optimizer ratio).
@@ -657,8 +670,11 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
               hf[c] = __builtin_fma(rr[ia], A, HW) * iP + O.H2Dx;
               df[c] = __builtin_fma(rr[ia], A, DG) * iP + O.D2Hx;
               fz[c] = ia == 0 && zero_oo;
+              // The exact frontier's candidates are feasible: a configuration above the memory
+              // budget needs no first-microbatch time there (its candidate test fails on memory).
+              if constexpr (EX) fz[c] = fz[c] | !(O.Bmax + __builtin_fma(rr[ia], A2, om[ia] * KA) <= M);
             }
-            interference_known_n<IB, SB>(fr, hf, df, fz, T1b, nb, tab);
+            interference_known_n<IB, SB, EX>(fr, hf, df, fz, T1b, nb, tab);
           }
 #pragma unroll
           for (int c = 0; c < IB; ++c) {
