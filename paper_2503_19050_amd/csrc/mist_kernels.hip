@@ -932,17 +932,20 @@ __global__ __launch_bounds__(256) void k_reduce(ReduceArgs a) {
   __shared__ double s_ao[kW][kMaxAlphas];
   __shared__ uint64_t s_ai[kW][kMaxAlphas];
   const int lane = threadIdx.x & 63;
-  const int wave = kW > 1 ? (int)(threadIdx.x >> 6) : 0;  // the wave's share of the tiles
-  const int64_t g = kW > 1 ? (int64_t)blockIdx.x : (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  // Wave-uniform (stated, so that the group record arrives by scalar loads and the tile loops
+  // run on scalar registers).
+  const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int wave = kW > 1 ? wv : 0;  // the wave's share of the tiles
+  const int64_t g = kW > 1 ? (int64_t)blockIdx.x : (int64_t)blockIdx.x * 4 + wv;
   if (g >= a.n_groups) return;
-  const DevGroup grp = a.groups[g];
+  const DevGroup grp = load_uniform(a.groups + g);
   double obj = __builtin_huge_val();
   uint64_t id = kNone;
   if (lane < a.NB) {  // several tiles' loads in flight
 #pragma unroll 4
     for (int t = grp.tile_begin + wave; t < grp.tile_begin + grp.n_tiles; t += kW) {
-      const double o = a.part_obj[(size_t)t * 64 + lane];
-      const uint64_t i = a.part_id[(size_t)t * 64 + lane];
+      const double o = __builtin_nontemporal_load(a.part_obj + (size_t)t * 64 + lane);  // read once
+      const uint64_t i = __builtin_nontemporal_load(a.part_id + (size_t)t * 64 + lane);
       if (lex_less(o, i, obj, id)) {
         obj = o;
         id = i;
@@ -950,8 +953,8 @@ __global__ __launch_bounds__(256) void k_reduce(ReduceArgs a) {
     }
 #pragma unroll 4
     for (int t = grp.tail_begin + wave; t < grp.tail_begin + grp.n_tail; t += kW) {
-      const double o = a.part_obj[(size_t)t * 64 + lane];
-      const uint64_t i = a.part_id[(size_t)t * 64 + lane];
+      const double o = __builtin_nontemporal_load(a.part_obj + (size_t)t * 64 + lane);
+      const uint64_t i = __builtin_nontemporal_load(a.part_id + (size_t)t * 64 + lane);
       if (lex_less(o, i, obj, id)) {
         obj = o;
         id = i;
