@@ -284,8 +284,9 @@ def main() -> int:
         exact = {"ms_per_run": ms, "runs": len(runs), "value": S.n_configs / (ms / 1e3), "unit": "configs/s",
                  **S.exact_info(),
                  "what": "exact time-vs-memory frontier of every group after the evaluation: candidate filter, "
-                         "live tiles, one candidate pass of the evaluation kernel over them (plus the tiles whose candidates overflowed their "
-                         "window), exact pre-filter, segmented sort by memory, scan; host "
+                         "live tiles, one candidate pass of the evaluation kernel over them (candidates past a tile's window go to an "
+                         "overflow pool; a tile with a candidate that finds no place in either is evaluated again), exact "
+                         "pre-filter, segmented sort by memory, scan; host "
                          "wall time including its one synchronisation"}
 
     alpha = None
