@@ -136,3 +136,41 @@ def test_random_spaces(seed, torch_cuda):
     n_tiles = S.launch_info()["tiles"]
     _check_tiles(S, o, wl, list(range(n_tiles)), {})
     S.close()
+
+
+@pytest.mark.parametrize("chunk", range(4))
+def test_random_spaces_geometry(chunk, torch_cuda):
+    """Seeded random spaces (seeds 100-499 in four chunks), a third each with the seeded factors,
+    unit factors and factors up to 50, each with a random tile size and grid cap (so a random
+    work-item order): every configuration of every tile, and every group's bucket table, best
+    and frontier."""
+    from paper_2503_19050_amd import mist
+    n = 0
+    for seed in range(100 + 100 * chunk, 200 + 100 * chunk):
+        wl = W.random_space(seed)
+        if seed % 3 == 1:
+            wl = _unit_factors(wl)
+        elif seed % 3 == 2:
+            wl = _large_factors(wl, seed)
+        rng = np.random.default_rng(seed)
+        wl["space"]["tile_configs"] = int(rng.choice([0, 0, 64, 1000, 100000]))
+        wl["space"]["max_blocks"] = int(rng.choice([0, 0, 1, 7, 37]))
+        o = O.Oracle(wl)
+        if o.n_configs == 0 or o.n_configs > 400_000:
+            continue
+        say("kernel dump random", seed, o.n_configs, "tile", wl["space"]["tile_configs"], "grid cap",
+            wl["space"]["max_blocks"])
+        S = mist.from_workload(wl)
+        S.eval()
+        ref = o.run()
+        ids, objs, masks = S.buckets()
+        assert np.array_equal(ids, ref["bucket_id"]), seed
+        assert np.array_equal(objs, ref["bucket_obj"]), seed
+        assert np.array_equal(masks, ref["frontier"]), seed
+        n_tiles = S.launch_info()["tiles"]
+        cache = {}
+        for lo in range(0, n_tiles, 512):
+            _check_tiles(S, o, wl, list(range(lo, min(n_tiles, lo + 512))), cache)
+        S.close()
+        n += 1
+    assert n >= 60
