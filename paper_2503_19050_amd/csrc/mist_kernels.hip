@@ -481,8 +481,10 @@ constexpr int ia_block() {
 template <int R, int MODE>
 constexpr int decide_block() { return 1; }
 
-// Waves per SIMD the register allocation aims at: four, the most the LDS use of a block
-// allows (a few strip-level values spill; the occupancy is worth more).  The exact frontier's
+// Waves per SIMD the register allocation aims at: four, 128 registers per lane (a few
+// strip-level values spill; the occupancy is worth more).  Five would fit the LDS of the blocks,
+// but at 96 registers the inner loop spills: 77 against 59 ms on the 64-sample Llama space.  The
+// exact frontier's
 // candidate variant keeps more per configuration live; with a whole strip's activation ratios
 // in one block (R <= 6) three waves and fewer spills are faster (1.60 against 1.83 ms for the
 // exact frontier on gpt2.7b-d16), with larger R four.
