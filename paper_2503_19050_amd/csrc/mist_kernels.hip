@@ -264,17 +264,61 @@ __device__ __forceinline__ KnownRow known_row(const double* __restrict__ tab, in
   return r;
 }
 
+// Rows of the third round when compute and one host stream are left after the second round
+// (row 13's overlap ended the other host stream): for the stream h left (index 0: h = 2, row 5;
+// index 1: h = 3, row 9) the kTab2 doubles phi[0], phi[h], psi[0], psi[h] of that row and psi[0],
+// psi[h] of row 13, so that a lane reads its row from one per-lane offset.
+constexpr int kTab2 = 6;
+constexpr int kTab2Off = 16 * kLdsRow;  // after the sixteen pattern rows
+
 // The second and third rounds of a call whose first round (row 15) ended GPU-GPU alone.  The
 // same operations on the same operands as the general rounds below, with GPU-GPU's time (NaN from
 // row 13's +inf factor) left out of the minima and the maximum it cannot win.
-__device__ __forceinline__ double rounds_after_g1(const KnownRow& r, double s2, double s3,
+//
+// The second round (row 13: compute, host->device, device->host) ends the stream with the
+// smallest scaled time y and leaves the other two, so the third round's row is one of three.
+// When every lane of the wave (lanes with free set do not count) has compute left with exactly
+// one host stream (y0 above the smaller host time, the host times unequal), each lane reads the
+// row of compute and its larger host stream at a per-lane offset and forms only those two
+// streams' terms; when every lane has compute finish first (y0 below both host times), the row
+// of the two host streams is the same for the wave.  Otherwise (ties, mixed waves) the row is
+// looked up from all three streams' patterns.  The finished stream's terms are NaN in the
+// general form (its time 0 times the row's +inf factor) and drop out of its minimum and
+// maximum, so the two special forms give the same bits.
+__device__ __forceinline__ double rounds_after_g1(const KnownRow& r, double s2, double s3, bool free,
                                                   const double* __restrict__ tab) {
   const double* e15 = tab + 15 * kLdsRow;
   const double* e13 = tab + 13 * kLdsRow;
   const double y0 = r.y0;
   const double y2 = ((s2 - r.s1) * e15[6]) * e13[2];
   const double y3 = ((s3 - r.s1) * e15[7]) * e13[3];
-  const double ov2 = __builtin_fmin(y0, __builtin_fmin(y2, y3));
+  const double m23 = __builtin_fmin(y2, y3);
+  const bool up2 = y2 > y3;
+  const double yh = up2 ? y2 : y3;  // the larger host time (a selection: the operands are numbers)
+  // Wave masks of plain compares (combined by the scalar unit).
+  const unsigned long long ex = __builtin_amdgcn_read_exec();
+  const unsigned long long fm = __builtin_amdgcn_ballot_w64(free);
+  if (((__builtin_amdgcn_ballot_w64(y0 > m23) & __builtin_amdgcn_ballot_w64(y2 != y3)) | fm) == ex) {
+    // Compute and the larger host stream are left (row 5 or 9); the second round's overlap is
+    // the smaller host time m23.
+    const double* e = tab + kTab2Off + (up2 ? 0 : kTab2);
+    const double z0 = (y0 - m23) * e[4];
+    const double zh = (yh - m23) * e[5];
+    const double w0 = z0 * e[0], wh = zh * e[1];
+    const double ov3 = __builtin_fmin(w0, wh);
+    const double rem = __builtin_fmax((w0 - ov3) * e[2], (wh - ov3) * e[3]);
+    return ((r.s1 + m23) + ov3) + rem;
+  }
+  if ((__builtin_amdgcn_ballot_w64(y0 < m23) | fm) == ex) {
+    // Compute finished in the second round (overlap y0); both host streams are left (row 12).
+    const double* e12 = tab + 12 * kLdsRow;
+    const double w2 = ((y2 - y0) * e13[6]) * e12[2];
+    const double w3 = ((y3 - y0) * e13[7]) * e12[3];
+    const double ov3 = __builtin_fmin(w2, w3);
+    const double rem = __builtin_fmax((w2 - ov3) * e12[6], (w3 - ov3) * e12[7]);
+    return ((r.s1 + y0) + ov3) + rem;
+  }
+  const double ov2 = __builtin_fmin(y0, m23);
   const double T2 = r.s1 + ov2;
   // Third round: the row of the streams still running, those whose scaled time exceeds the
   // overlap.
@@ -338,7 +382,7 @@ __device__ __forceinline__ void interference_known_n(const KnownRow& r, const do
     } else if (__builtin_amdgcn_ballot_w64(ok) == __builtin_amdgcn_read_exec()) {
 #pragma unroll
       for (int c = 0; c < SB; ++c)
-        if (c0 + c < n) out[c0 + c] = rounds_after_g1(r, s2[c], s3[c], tab);
+        if (c0 + c < n) out[c0 + c] = rounds_after_g1(r, s2[c], s3[c], free[c0 + c], tab);
     } else {
 #pragma unroll
       for (int c = 0; c < SB; ++c)
@@ -504,7 +548,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
   constexpr int IB = ia_block<R, MODE>();
   constexpr int SB = decide_block<R, MODE>();
-  __shared__ double s_tab[kWaves][16 * kLdsRow];
+  __shared__ double s_tab[kWaves][16 * kLdsRow + 2 * kTab2];
   __shared__ BucketEntry s_bucket[kWaves][65];  // entries NB..64: sinks of infeasible configurations
   __shared__ OoIn s_oo[kBlock];         // per-lane strip constants of the optimizer level
   __shared__ double2 s_ab[AL ? kWaves : 1][kMaxAlphas];      // alpha * G, 1 - alpha
@@ -550,6 +594,12 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
     if (g.hw != loaded_hw) {  // the wave's LDS copy of the hardware tables
       for (int i = lane; i < 16 * kTabStride; i += 64)
         tab[(i / kTabStride) * kLdsRow + i % kTabStride] = (&hw.itab[0][0])[i];
+      if (lane < 2 * kTab2) {  // the third round's rows of compute and one host stream
+        const int h = 2 + lane / kTab2, i = lane % kTab2;
+        const double* row = hw.itab[1 | (1 << h)];
+        tab[kTab2Off + lane] = i == 0 ? row[0] : i == 1 ? row[h] : i == 2 ? row[4] : i == 3 ? row[4 + h]
+                                                                                      : hw.itab[13][i == 4 ? 4 : 4 + h];
+      }
       bucket[lane].edge = hw.edge[lane];
       loaded_hw = g.hw;
     }
