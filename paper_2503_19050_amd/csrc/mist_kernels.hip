@@ -237,19 +237,19 @@ __device__ __forceinline__ double interference(double c, double g, double h, dou
 // streams both run (pattern 15, or 13 without GPU-GPU traffic), with compute c and GPU-GPU g fixed
 // per strip.  The strip precomputes the scaled c and g and their minimum m01.
 //
-// After the first round a member keeps running exactly when its scaled time exceeds the overlap
+// After a round a member keeps running exactly when its scaled time exceeds the overlap
 // (s_j - ov > 0, and (s_j - ov) * psi_j cannot round to zero: the host's input bounds keep every
 // non-zero stream time and difference far above the subnormal range).  In the common case the
 // GPU-GPU stream is a member and its scaled time s1 is below every other member's: the overlap is
 // s1 itself, compute, host->device and device->host keep running, and the second round reads
 // row 13 for every such configuration, with compute's second-round scaled time y0 fixed per
-// strip.  A wave all of whose lanes are in that case takes the wave-uniform row (rounds_after_g1);
-// any other wave runs the general rounds with rows looked up per lane.
+// strip.  The second-round scaled times y_j = ((s_j - s1) * psi15_j) * phi13_j have the sign of
+// s_j - s1, so that case is y0 > 0 and y2, y3 > 0 (with pattern 13, s1 and y0 are NaN and the
+// case never holds).
 struct KnownRow {
   double s0, s1, m01;   // c * phi0, g * phi1 (NaN when GPU-GPU is no member), min of the two
-  double y0;            // when s1 < s0: compute's scaled time in the second round (row 13)
+  double y0;            // compute's scaled time in the second round (row 13) when s1 < s0
   const double* row;    // the first round's row
-  double s1g;           // s1 when GPU-GPU is a member and s1 < s0, else +inf (pattern 13: s1 is NaN)
 };
 
 __device__ __forceinline__ KnownRow known_row(const double* __restrict__ tab, int pattern, double c, double g) {
@@ -259,76 +259,8 @@ __device__ __forceinline__ KnownRow known_row(const double* __restrict__ tab, in
   r.s1 = g * e[1];
   r.m01 = __builtin_fmin(r.s0, r.s1);
   r.row = e;
-  r.s1g = r.s1 < r.s0 ? r.s1 : __builtin_huge_val();
   r.y0 = ((r.s0 - r.s1) * e[4]) * tab[13 * kLdsRow + 0];
   return r;
-}
-
-// Rows of the third round when compute and one host stream are left after the second round
-// (row 13's overlap ended the other host stream): for the stream h left (index 0: h = 2, row 5;
-// index 1: h = 3, row 9) the kTab2 doubles phi[0], phi[h], psi[0], psi[h] of that row and psi[0],
-// psi[h] of row 13, so that a lane reads its row from one per-lane offset.
-constexpr int kTab2 = 6;
-constexpr int kTab2Off = 16 * kLdsRow;  // after the sixteen pattern rows
-
-// The second and third rounds of a call whose first round (row 15) ended GPU-GPU alone.  The
-// same operations on the same operands as the general rounds below, with GPU-GPU's time (NaN from
-// row 13's +inf factor) left out of the minima and the maximum it cannot win.
-//
-// The second round (row 13: compute, host->device, device->host) ends the stream with the
-// smallest scaled time y and leaves the other two, so the third round's row is one of three.
-// When every lane of the wave (lanes with free set do not count) has compute left with exactly
-// one host stream (y0 above the smaller host time, the host times unequal), each lane reads the
-// row of compute and its larger host stream at a per-lane offset and forms only those two
-// streams' terms; when every lane has compute finish first (y0 below both host times), the row
-// of the two host streams is the same for the wave.  Otherwise (ties, mixed waves) the row is
-// looked up from all three streams' patterns.  The finished stream's terms are NaN in the
-// general form (its time 0 times the row's +inf factor) and drop out of its minimum and
-// maximum, so the two special forms give the same bits.
-__device__ __forceinline__ double rounds_after_g1(const KnownRow& r, double s2, double s3, bool free,
-                                                  const double* __restrict__ tab) {
-  const double* e15 = tab + 15 * kLdsRow;
-  const double* e13 = tab + 13 * kLdsRow;
-  const double y0 = r.y0;
-  const double y2 = ((s2 - r.s1) * e15[6]) * e13[2];
-  const double y3 = ((s3 - r.s1) * e15[7]) * e13[3];
-  const double m23 = __builtin_fmin(y2, y3);
-  const bool up2 = y2 > y3;
-  const double yh = up2 ? y2 : y3;  // the larger host time (a selection: the operands are numbers)
-  // Wave masks of plain compares (combined by the scalar unit).
-  const unsigned long long ex = __builtin_amdgcn_read_exec();
-  const unsigned long long fm = __builtin_amdgcn_ballot_w64(free);
-  if (((__builtin_amdgcn_ballot_w64(y0 > m23) & __builtin_amdgcn_ballot_w64(y2 != y3)) | fm) == ex) {
-    // Compute and the larger host stream are left (row 5 or 9); the second round's overlap is
-    // the smaller host time m23.
-    const double* e = tab + kTab2Off + (up2 ? 0 : kTab2);
-    const double z0 = (y0 - m23) * e[4];
-    const double zh = (yh - m23) * e[5];
-    const double w0 = z0 * e[0], wh = zh * e[1];
-    const double ov3 = __builtin_fmin(w0, wh);
-    const double rem = __builtin_fmax((w0 - ov3) * e[2], (wh - ov3) * e[3]);
-    return ((r.s1 + m23) + ov3) + rem;
-  }
-  if ((__builtin_amdgcn_ballot_w64(y0 < m23) | fm) == ex) {
-    // Compute finished in the second round (overlap y0); both host streams are left (row 12).
-    const double* e12 = tab + 12 * kLdsRow;
-    const double w2 = ((y2 - y0) * e13[6]) * e12[2];
-    const double w3 = ((y3 - y0) * e13[7]) * e12[3];
-    const double ov3 = __builtin_fmin(w2, w3);
-    const double rem = __builtin_fmax((w2 - ov3) * e12[6], (w3 - ov3) * e12[7]);
-    return ((r.s1 + y0) + ov3) + rem;
-  }
-  const double ov2 = __builtin_fmin(y0, m23);
-  const double T2 = r.s1 + ov2;
-  // Third round: the row of the streams still running, those whose scaled time exceeds the
-  // overlap.
-  const bool q0 = y0 > ov2, q2 = y2 > ov2, q3 = y3 > ov2;
-  const double z0 = (y0 - ov2) * e13[4], z2 = (y2 - ov2) * e13[6], z3 = (y3 - ov2) * e13[7];
-  const double* e = tab + ((q0 ? 1 : 0) + (q2 ? 4 : 0) + (q3 ? 8 : 0)) * kLdsRow;
-  const double w0 = z0 * e[0], w2 = z2 * e[2], w3 = z3 * e[3];
-  const double ov3 = __builtin_fmin(__builtin_fmin(w0, w2), w3);
-  const double rem = __builtin_fmax(__builtin_fmax((w0 - ov3) * e[4], (w2 - ov3) * e[6]), (w3 - ov3) * e[7]);
-  return (T2 + ov3) + rem;
 }
 
 // General rounds of such a call with host streams h, d > 0: the first with the known row, the
@@ -345,49 +277,93 @@ __device__ __forceinline__ double interference_general(const KnownRow& r, double
   return T + remaining(x);
 }
 
+// Rows of the third round when compute and one host stream are left after the second round
+// (row 13's overlap ended the other host stream): for the stream h left (index 0: h = 2, row 5;
+// index 1: h = 3, row 9) the kTab2 doubles phi[0], phi[h], psi[0], psi[h] of that row and psi[0],
+// psi[h] of row 13, so that a lane reads its row from one per-lane offset.
+constexpr int kTab2 = 6;
+constexpr int kTab2Off = 16 * kLdsRow;  // after the sixteen pattern rows
+
+// Algorithm 1 for one configuration of a strip with the strip's known first-round row.  Each form
+// is chosen for the whole wave (lanes with free set, whose result the caller replaces or does
+// not use, do not take part), so that every form is straight-line code:
+//   - GPU-GPU finishes first (row 15) and the second round (row 13: compute, host->device,
+//     device->host) ends the smaller host stream: compute and the larger host stream are left,
+//     and each lane reads their row (5 or 9) at a per-lane offset and forms only their terms;
+//   - GPU-GPU finishes first and compute ends the second round: both host streams are left, and
+//     the third round's row (12) is the same for the wave;
+//   - GPU-GPU finishes first otherwise (ties): the third round's row is looked up per lane from
+//     all three streams;
+//   - else the general rounds (interference_general).
+// Each form performs the same operations on the same operands as the general rounds: a stream
+// that has finished carries NaN there (its time 0 times the row's +inf factor), which drops out
+// of the minimum and the maximum that the special forms take over the streams left.
+__device__ __forceinline__ double interference_known(const KnownRow& r, double h, double d, bool free,
+                                                     const double* __restrict__ tab) {
+  const double* e15 = tab + 15 * kLdsRow;
+  const double* e13 = tab + 13 * kLdsRow;
+  const double y0 = r.y0;
+  const double y2 = ((h * e15[2] - r.s1) * e15[6]) * e13[2];
+  const double y3 = ((d * e15[3] - r.s1) * e15[7]) * e13[3];
+  const double m23 = __builtin_fmin(y2, y3);
+  const double yh = __builtin_fmax(y2, y3);
+  // Wave masks of plain compares (combined by the scalar unit).
+  const unsigned long long ex = __builtin_amdgcn_read_exec();
+  const unsigned long long fm = __builtin_amdgcn_ballot_w64(free);
+  const unsigned long long g1 = __builtin_amdgcn_ballot_w64(m23 > 0.0);  // with y0 > 0: GPU-GPU first
+  if (((__builtin_amdgcn_ballot_w64(y0 > m23) & g1 & __builtin_amdgcn_ballot_w64(yh > m23)) | fm) == ex) {
+    // Compute and the larger host stream are left (row 5 or 9); the second round's overlap is
+    // the smaller host time m23.
+    const double* e = tab + kTab2Off + (y2 > y3 ? 0 : kTab2);
+    const double z0 = (y0 - m23) * e[4];
+    const double zh = (yh - m23) * e[5];
+    const double w0 = z0 * e[0], wh = zh * e[1];
+    const double ov3 = __builtin_fmin(w0, wh);
+    const double rem = __builtin_fmax((w0 - ov3) * e[2], (wh - ov3) * e[3]);
+    return ((r.s1 + m23) + ov3) + rem;
+  }
+  const unsigned long long y0p = __builtin_amdgcn_ballot_w64(y0 > 0.0);
+  if (((__builtin_amdgcn_ballot_w64(y0 < m23) & y0p) | fm) == ex) {
+    // Compute finished in the second round (overlap y0); both host streams are left (row 12).
+    const double* e12 = tab + 12 * kLdsRow;
+    const double w2 = ((y2 - y0) * e13[6]) * e12[2];
+    const double w3 = ((y3 - y0) * e13[7]) * e12[3];
+    const double ov3 = __builtin_fmin(w2, w3);
+    const double rem = __builtin_fmax((w2 - ov3) * e12[6], (w3 - ov3) * e12[7]);
+    return ((r.s1 + y0) + ov3) + rem;
+  }
+  if (((y0p & g1) | fm) == ex) {
+    const double ov2 = __builtin_fmin(y0, m23);
+    const double T2 = r.s1 + ov2;
+    // Third round: the row of the streams still running, those whose scaled time exceeds the
+    // overlap.
+    const bool q0 = y0 > ov2, q2 = y2 > ov2, q3 = y3 > ov2;
+    const double z0 = (y0 - ov2) * e13[4], z2 = (y2 - ov2) * e13[6], z3 = (y3 - ov2) * e13[7];
+    const double* e = tab + ((q0 ? 1 : 0) + (q2 ? 4 : 0) + (q3 ? 8 : 0)) * kLdsRow;
+    const double w0 = z0 * e[0], w2 = z2 * e[2], w3 = z3 * e[3];
+    const double ov3 = __builtin_fmin(__builtin_fmin(w0, w2), w3);
+    const double rem = __builtin_fmax(__builtin_fmax((w0 - ov3) * e[4], (w2 - ov3) * e[6]), (w3 - ov3) * e[7]);
+    return (T2 + ov3) + rem;
+  }
+  return interference_general(r, h, d, tab);
+}
+
 // Algorithm 1 for the first n of the N configurations of an activation-ratio block (host streams
-// h[c], d[c]), all with the strip's known first-round row.  One wave-uniform decision per
-// sub-block of SB configurations: when GPU-GPU finishes first and alone in every lane and
-// configuration of the sub-block, the rounds after it (rounds_after_g1), else the general rounds,
-// so that either path is straight-line code.  Configurations with free[c] set (their result is
-// replaced or unused by the caller) do not take part in the decision; with SKIP a sub-block free
-// in every lane is not evaluated (its results are NaN).
-template <int N, int SB, bool SKIP = false>
+// h[c], d[c]), one wave-uniform choice of form per configuration (measured fastest against one
+// choice per block or half block: 0.81 against 1.16 and 1.02 ms on gpt2.7b-d16, equal on the
+// Llama spaces).  With SKIP a configuration free in every lane is not evaluated (its results are
+// NaN).
+template <int N, bool SKIP = false>
 __device__ __forceinline__ void interference_known_n(const KnownRow& r, const double (&h)[N], const double (&d)[N],
                                                      const bool (&free)[N], double (&out)[N], int n,
                                                      const double* __restrict__ tab) {
-  const double* e15 = tab + 15 * kLdsRow;  // the first-round row of every lane with a finite s1g
 #pragma unroll
-  for (int c0 = 0; c0 < N; c0 += SB) {
-    if (c0 >= n) break;
-    double s2[SB], s3[SB];
-    bool ok = true;
-#pragma unroll
-    for (int c = 0; c < SB; ++c) {
-      if (c0 + c >= n) break;
-      s2[c] = h[c0 + c] * e15[2];
-      s3[c] = d[c0 + c] * e15[3];
-      ok = ok & (free[c0 + c] | (__builtin_fmin(s2[c], s3[c]) > r.s1g));
-    }
-    bool busy = !SKIP;  // some lane's result is used
-    if constexpr (SKIP) {
-#pragma unroll
-      for (int c = 0; c < SB; ++c)
-        if (c0 + c < n) busy = busy | !free[c0 + c];
-    }
-    if (SKIP && !__builtin_amdgcn_ballot_w64(busy)) {  // every lane's result is unused: none is formed
-#pragma unroll
-      for (int c = 0; c < SB; ++c)
-        if (c0 + c < n) out[c0 + c] = __builtin_nan("");
-    } else if (__builtin_amdgcn_ballot_w64(ok) == __builtin_amdgcn_read_exec()) {
-#pragma unroll
-      for (int c = 0; c < SB; ++c)
-        if (c0 + c < n) out[c0 + c] = rounds_after_g1(r, s2[c], s3[c], free[c0 + c], tab);
-    } else {
-#pragma unroll
-      for (int c = 0; c < SB; ++c)
-        if (c0 + c < n) out[c0 + c] = interference_general(r, h[c0 + c], d[c0 + c], tab);
-    }
+  for (int c = 0; c < N; ++c) {
+    if (c >= n) break;
+    if (SKIP && !__builtin_amdgcn_ballot_w64(!free[c]))  // every lane's result is unused: none is formed
+      out[c] = __builtin_nan("");
+    else
+      out[c] = interference_known(r, h[c], d[c], free[c], tab);
   }
 }
 
@@ -518,13 +494,6 @@ constexpr int ia_block() {
   return R <= 6 ? R : (MODE == kModeAlpha && R <= 10 ? (R + 1) / 2 : (R + 2) / 3);
 }
 
-// Configurations per wave-uniform interference decision (interference_known_n).  One decision per
-// configuration measured fastest (against one per block or per half block: 0.81 against 1.16 and
-// 1.02 ms on gpt2.7b-d16, equal on the Llama spaces); the stable times and the first-microbatch
-// times of a block are still formed together, ahead of the block's reductions.
-template <int R, int MODE>
-constexpr int decide_block() { return 1; }
-
 // Waves per SIMD the register allocation aims at: four, 128 registers per lane (a few
 // strip-level values spill; the occupancy is worth more).  Five would fit the LDS of the blocks,
 // but at 96 registers the inner loop spills: 77 against 59 ms on the 64-sample Llama space.  The
@@ -547,7 +516,6 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
   constexpr int R2 = R * R;
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
   constexpr int IB = ia_block<R, MODE>();
-  constexpr int SB = decide_block<R, MODE>();
   __shared__ double s_tab[kWaves][16 * kLdsRow + 2 * kTab2];
   __shared__ BucketEntry s_bucket[kWaves][65];  // entries NB..64: sinks of infeasible configurations
   __shared__ OoIn s_oo[kBlock];         // per-lane strip constants of the optimizer level
@@ -691,7 +659,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             ds[c] = __builtin_fma(rr[ia], K.A, W.DG) * iP;
             fs[c] = ia == 0 && r0_zero;
           }
-          interference_known_n<IB, SB>(sr, hs, ds, fs, tt, nb, tab);
+          interference_known_n<IB>(sr, hs, ds, fs, tt, nb, tab);
           // Activation ratio 0 leaves the host streams to the weights and gradients alone: the
           // first round's pattern is not known in advance.
           if (ib == 0 && r0_zero) tt[0] = interference(K.C, Z.G2Gs, hs[0], ds[0], tab);
@@ -726,7 +694,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
               // budget needs no first-microbatch time there (its candidate test fails on memory).
               if constexpr (EX) fz[c] = fz[c] | !(O.Bmax + __builtin_fma(rr[ia], A2, om[ia] * KA) <= M);
             }
-            interference_known_n<IB, SB, EX>(fr, hf, df, fz, T1b, nb, tab);
+            interference_known_n<IB, EX>(fr, hf, df, fz, T1b, nb, tab);
           }
 #pragma unroll
           for (int c = 0; c < IB; ++c) {
