@@ -298,13 +298,21 @@ constexpr int kTab2Off = 16 * kLdsRow;  // after the sixteen pattern rows
 // Each form performs the same operations on the same operands as the general rounds: a stream
 // that has finished carries NaN there (its time 0 times the row's +inf factor), which drops out
 // of the minimum and the maximum that the special forms take over the streams left.
+// The factors every configuration's second-round scaled host times read: phi and psi of the host
+// streams in row 15 and their phi in row 13.  Wave-uniform, loaded once per tile into scalar
+// registers (as vector registers they crowd the strip loop into spilling).
+struct RowK {
+  double f2, f3;  // phi15[2], phi15[3]
+  double p2, p3;  // psi15[2], psi15[3]
+  double g2, g3;  // phi13[2], phi13[3]
+};
+
 __device__ __forceinline__ double interference_known(const KnownRow& r, double h, double d, bool free,
-                                                     const double* __restrict__ tab) {
-  const double* e15 = tab + 15 * kLdsRow;
+                                                     const double* __restrict__ tab, const RowK& K) {
   const double* e13 = tab + 13 * kLdsRow;
   const double y0 = r.y0;
-  const double y2 = ((h * e15[2] - r.s1) * e15[6]) * e13[2];
-  const double y3 = ((d * e15[3] - r.s1) * e15[7]) * e13[3];
+  const double y2 = ((h * K.f2 - r.s1) * K.p2) * K.g2;
+  const double y3 = ((d * K.f3 - r.s1) * K.p3) * K.g3;
   const double m23 = __builtin_fmin(y2, y3);
   const double yh = __builtin_fmax(y2, y3);
   // Wave masks of plain compares (combined by the scalar unit).
@@ -356,14 +364,14 @@ __device__ __forceinline__ double interference_known(const KnownRow& r, double h
 template <int N, bool SKIP = false>
 __device__ __forceinline__ void interference_known_n(const KnownRow& r, const double (&h)[N], const double (&d)[N],
                                                      const bool (&free)[N], double (&out)[N], int n,
-                                                     const double* __restrict__ tab) {
+                                                     const double* __restrict__ tab, const RowK& K) {
 #pragma unroll
   for (int c = 0; c < N; ++c) {
     if (c >= n) break;
     if (SKIP && !__builtin_amdgcn_ballot_w64(!free[c]))  // every lane's result is unused: none is formed
       out[c] = __builtin_nan("");
     else
-      out[c] = interference_known(r, h[c], d[c], free[c], tab);
+      out[c] = interference_known(r, h[c], d[c], free[c], tab, K);
   }
 }
 
@@ -603,6 +611,8 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
     wave_sync();
 
     const double iP = load_uniform(&hw.iP), kNB = load_uniform(&hw.kNB), M = load_uniform(&hw.M);
+    const RowK RK{load_uniform(&hw.itab[15][2]), load_uniform(&hw.itab[15][3]), load_uniform(&hw.itab[15][6]),
+                  load_uniform(&hw.itab[15][7]), load_uniform(&hw.itab[13][2]), load_uniform(&hw.itab[13][3])};
     const int l = g.l;
     const int64_t ke = g.k < g.G ? g.k : g.G;
 
@@ -659,7 +669,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             ds[c] = __builtin_fma(rr[ia], K.A, W.DG) * iP;
             fs[c] = ia == 0 && r0_zero;
           }
-          interference_known_n<IB>(sr, hs, ds, fs, tt, nb, tab);
+          interference_known_n<IB>(sr, hs, ds, fs, tt, nb, tab, RK);
           // Activation ratio 0 leaves the host streams to the weights and gradients alone: the
           // first round's pattern is not known in advance.
           if (ib == 0 && r0_zero) tt[0] = interference(K.C, Z.G2Gs, hs[0], ds[0], tab);
@@ -694,7 +704,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
               // budget needs no first-microbatch time there (its candidate test fails on memory).
               if constexpr (EX) fz[c] = fz[c] | !(O.Bmax + __builtin_fma(rr[ia], A2, om[ia] * KA) <= M);
             }
-            interference_known_n<IB, EX>(fr, hf, df, fz, T1b, nb, tab);
+            interference_known_n<IB, EX>(fr, hf, df, fz, T1b, nb, tab, RK);
           }
 #pragma unroll
           for (int c = 0; c < IB; ++c) {
