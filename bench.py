@@ -251,10 +251,11 @@ def main() -> int:
                     "kernel": "k_eval", "flops_per_config": fpc,
                     "flops_unit": "FP64 operations of the cost model per configuration with every loop level "
                                   "shared, as the oracle evaluates it (fma = 2)",
-                    # Labelled extras: the same definition with every level repeated per
-                    # configuration, and what the kernel executes by the instruction counters.
-                    "flops_per_config_from_scratch": fscratch,
-                    "frac_from_scratch": fscratch * S.n_configs / (k1_avg / 1e3) / 1e12 / FP64_VECTOR_PEAK_TFLOPS}
+                    # Labelled extras: the count of the same definition with every level repeated
+                    # per configuration (work neither the oracle nor the kernel does, so no
+                    # fraction of peak is formed from it), and what the kernel executes by the
+                    # instruction counters.
+                    "flops_per_config_from_scratch": fscratch}
         executed = counter_record(wl["name"])
         if executed is not None:
             roofline["executed_fp64_per_config"] = executed
