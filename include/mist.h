@@ -337,9 +337,14 @@ mist_status mist_tile_info(const mist_space* S, int32_t t, int64_t* group, uint6
 /* Parity checks of the evaluation kernel itself (the cost model of Eq. 4-6 with Algorithm 1,
  * Sec. 5.2): runs the evaluation kernel's own per-configuration path (not the per-id path of
  * mist_eval_ids) over the listed tiles and writes, for every configuration of tiles[0..n-1] in
- * that order and in id order within a tile, five doubles into host out: t, d, mem, obj and the
+ * that order and in id order within a tile, six doubles into host out: t, d, mem, obj, the
  * bucket entry the kernel chose (0..NB-1 for a feasible configuration; NB..64 for an infeasible
- * one, which the reduction ignores).  cap is the capacity of out in configurations.
+ * one, which the reduction ignores) and the forms in which it evaluated Algorithm 1 for the
+ * configuration, f1 + 8 * fs with f1 the first microbatch's form and fs the stable time's:
+ * 1 compute and the larger host stream left after the second round (per-lane third row), 2 compute
+ * finished in the second round (one third row for the wave), 3 the third row looked up per lane,
+ * 4 the general rounds, 5 the all-zero configuration's closed form, 6 three rounds from an unknown
+ * first pattern.  cap is the capacity of out in configurations.
  * Synchronous on hip_stream; allocates temporary device memory through the space's allocator.
  * Errors: MIST_E_INVALID, MIST_E_RANGE (a tile index, or cap too small), MIST_E_NOMEM,
  * MIST_E_DEVICE. */

@@ -1527,7 +1527,7 @@ mist_status mist_debug_eval_tiles(mist_space* S, const int32_t* tiles, int32_t n
     }
     TempBuf dlist(S, (size_t)n * sizeof(int32_t), st);
     TempBuf doff(S, (size_t)n * sizeof(int64_t), st);
-    TempBuf dout(S, (size_t)std::max<int64_t>(total, 1) * 5 * sizeof(double), st);
+    TempBuf dout(S, (size_t)std::max<int64_t>(total, 1) * kDumpWords * sizeof(double), st);
     if (!dlist.p || !doff.p || !dout.p) return fail(MIST_E_NOMEM, "device allocation failed: debug tiles");
     auto drained = [&](mist_status code) {
       (void)hipStreamSynchronize(st);
@@ -1544,7 +1544,7 @@ mist_status mist_debug_eval_tiles(mist_space* S, const int32_t* tiles, int32_t n
     int k = launch_pairs(ea, st);  // pair constants, and the tile counters' reset
     if (!k) k = launch_eval(ea, mode_grid(S, kModeDump), kModeDump, st);
     if (k) return drained(fail_hip((hipError_t)k, "debug tiles: launch"));
-    e = copy_async(out, dout.p, (size_t)total * 5 * sizeof(double), hipMemcpyDeviceToHost, st);
+    e = copy_async(out, dout.p, (size_t)total * kDumpWords * sizeof(double), hipMemcpyDeviceToHost, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     if (e != hipSuccess) return drained(fail_hip(e, "debug tiles: results"));
     return MIST_OK;

@@ -91,6 +91,7 @@ constexpr int kModeBuckets = 0;  // bucket minima (and per-tile partials)
 constexpr int kModeAlpha = 1;    // bucket minima and the weight-sampled argmins
 constexpr int kModeEmit = 2;     // exact frontier: write and count each tile's candidates
 constexpr int kModeDump = 3;     // per-configuration values of listed tiles (parity checks)
+constexpr int kDumpWords = 6;    // doubles per configuration in the dump variant's output
 
 struct EvalArgs {
   DevModel m;

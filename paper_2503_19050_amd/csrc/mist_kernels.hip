@@ -284,6 +284,15 @@ __device__ __forceinline__ double interference_general(const KnownRow& r, double
 constexpr int kTab2 = 6;
 constexpr int kTab2Off = 16 * kLdsRow;  // after the sixteen pattern rows
 
+// The factors every configuration's second-round scaled host times read: phi and psi of the host
+// streams in row 15 and their phi in row 13.  Wave-uniform, loaded once per tile into scalar
+// registers (as vector registers they crowd the strip loop into spilling).
+struct RowK {
+  double f2, f3;  // phi15[2], phi15[3]
+  double p2, p3;  // psi15[2], psi15[3]
+  double g2, g3;  // phi13[2], phi13[3]
+};
+
 // Algorithm 1 for one configuration of a strip with the strip's known first-round row.  Each form
 // is chosen for the whole wave (lanes with free set, whose result the caller replaces or does
 // not use, do not take part), so that every form is straight-line code:
@@ -297,18 +306,18 @@ constexpr int kTab2Off = 16 * kLdsRow;  // after the sixteen pattern rows
 //   - else the general rounds (interference_general).
 // Each form performs the same operations on the same operands as the general rounds: a stream
 // that has finished carries NaN there (its time 0 times the row's +inf factor), which drops out
-// of the minimum and the maximum that the special forms take over the streams left.
-// The factors every configuration's second-round scaled host times read: phi and psi of the host
-// streams in row 15 and their phi in row 13.  Wave-uniform, loaded once per tile into scalar
-// registers (as vector registers they crowd the strip loop into spilling).
-struct RowK {
-  double f2, f3;  // phi15[2], phi15[3]
-  double p2, p3;  // psi15[2], psi15[3]
-  double g2, g3;  // phi13[2], phi13[3]
-};
+// of the minimum and the maximum that the special forms take over the streams left.  form
+// receives the form taken (kForm*; read by the dump variant only).
+constexpr int kFormHostLeft = 1;    // compute and the larger host stream left: per-lane row 5 or 9
+constexpr int kFormHostsLeft = 2;   // compute finished in the second round: row 12
+constexpr int kFormLookup = 3;      // GPU-GPU first, third row looked up per lane
+constexpr int kFormGeneral = 4;     // the general rounds
+constexpr int kFormZero = 5;        // the all-zero configuration's closed form (first microbatch)
+constexpr int kFormGeneric = 6;     // three rounds from an unknown pattern (stable time, ratio 0)
 
 __device__ __forceinline__ double interference_known(const KnownRow& r, double h, double d, bool free,
-                                                     const double* __restrict__ tab, const RowK& K) {
+                                                     const double* __restrict__ tab, const RowK& K,
+                                                     int& form) {
   const double* e13 = tab + 13 * kLdsRow;
   const double y0 = r.y0;
   const double y2 = ((h * K.f2 - r.s1) * K.p2) * K.g2;
@@ -328,6 +337,7 @@ __device__ __forceinline__ double interference_known(const KnownRow& r, double h
     const double w0 = z0 * e[0], wh = zh * e[1];
     const double ov3 = __builtin_fmin(w0, wh);
     const double rem = __builtin_fmax((w0 - ov3) * e[2], (wh - ov3) * e[3]);
+    form = kFormHostLeft;
     return ((r.s1 + m23) + ov3) + rem;
   }
   const unsigned long long y0p = __builtin_amdgcn_ballot_w64(y0 > 0.0);
@@ -338,6 +348,7 @@ __device__ __forceinline__ double interference_known(const KnownRow& r, double h
     const double w3 = ((y3 - y0) * e13[7]) * e12[3];
     const double ov3 = __builtin_fmin(w2, w3);
     const double rem = __builtin_fmax((w2 - ov3) * e12[6], (w3 - ov3) * e12[7]);
+    form = kFormHostsLeft;
     return ((r.s1 + y0) + ov3) + rem;
   }
   if (((y0p & g1) | fm) == ex) {
@@ -351,8 +362,10 @@ __device__ __forceinline__ double interference_known(const KnownRow& r, double h
     const double w0 = z0 * e[0], w2 = z2 * e[2], w3 = z3 * e[3];
     const double ov3 = __builtin_fmin(__builtin_fmin(w0, w2), w3);
     const double rem = __builtin_fmax(__builtin_fmax((w0 - ov3) * e[4], (w2 - ov3) * e[6]), (w3 - ov3) * e[7]);
+    form = kFormLookup;
     return (T2 + ov3) + rem;
   }
+  form = kFormGeneral;
   return interference_general(r, h, d, tab);
 }
 
@@ -363,15 +376,16 @@ __device__ __forceinline__ double interference_known(const KnownRow& r, double h
 // NaN).
 template <int N, bool SKIP = false>
 __device__ __forceinline__ void interference_known_n(const KnownRow& r, const double (&h)[N], const double (&d)[N],
-                                                     const bool (&free)[N], double (&out)[N], int n,
+                                                     const bool (&free)[N], double (&out)[N], int (&form)[N], int n,
                                                      const double* __restrict__ tab, const RowK& K) {
 #pragma unroll
   for (int c = 0; c < N; ++c) {
     if (c >= n) break;
+    form[c] = 0;
     if (SKIP && !__builtin_amdgcn_ballot_w64(!free[c]))  // every lane's result is unused: none is formed
       out[c] = __builtin_nan("");
     else
-      out[c] = interference_known(r, h[c], d[c], free[c], tab, K);
+      out[c] = interference_known(r, h[c], d[c], free[c], tab, K, form[c]);
   }
 }
 
@@ -658,6 +672,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
         const int nb = R - ib < IB ? R - ib : IB;  // configurations of the block
         const KnownRow sr = known_row(tab, pats, K.C, Z.G2Gs);
         double tt[IB];
+        [[maybe_unused]] int fst[IB];  // dump variant: the form of each stable time
         {
           double hs[IB], ds[IB];
           bool fs[IB];
@@ -669,10 +684,13 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             ds[c] = __builtin_fma(rr[ia], K.A, W.DG) * iP;
             fs[c] = ia == 0 && r0_zero;
           }
-          interference_known_n<IB>(sr, hs, ds, fs, tt, nb, tab, RK);
+          interference_known_n<IB>(sr, hs, ds, fs, tt, fst, nb, tab, RK);
           // Activation ratio 0 leaves the host streams to the weights and gradients alone: the
           // first round's pattern is not known in advance.
-          if (ib == 0 && r0_zero) tt[0] = interference(K.C, Z.G2Gs, hs[0], ds[0], tab);
+          if (ib == 0 && r0_zero) {
+            tt[0] = interference(K.C, Z.G2Gs, hs[0], ds[0], tab);
+            fst[0] = kFormGeneric;
+          }
         }
         // Weight samples: the block's smallest stable time, for the lower bound below.
         [[maybe_unused]] double t_min = tt[0];
@@ -690,6 +708,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
           [[maybe_unused]] double dn_blk[AL ? IB : 1];  // weight samples: the block's deltas (NaN
                                                         // when infeasible)
           double T1b[IB];
+          [[maybe_unused]] int f1b[IB];  // dump variant: the form of each first-microbatch time
           {
             double hf[IB], df[IB];
             bool fz[IB];
@@ -704,7 +723,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
               // budget needs no first-microbatch time there (its candidate test fails on memory).
               if constexpr (EX) fz[c] = fz[c] | !(O.Bmax + __builtin_fma(rr[ia], A2, om[ia] * KA) <= M);
             }
-            interference_known_n<IB, EX>(fr, hf, df, fz, T1b, nb, tab, RK);
+            interference_known_n<IB, EX>(fr, hf, df, fz, T1b, f1b, nb, tab, RK);
           }
 #pragma unroll
           for (int c = 0; c < IB; ++c) {
@@ -733,12 +752,13 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             const double e0 = reinterpret_cast<const BucketEntry*>(b0)->edge;
             const unsigned long long k_lo = reinterpret_cast<const BucketEntry*>(b0)->key;
             if constexpr (DM) {
-              double* o = a.dump + 5 * (a.dump_off[x] + (int64_t)(s - tile.strip_begin) * R2 + io * R + ia);
+              double* o = a.dump + kDumpWords * (a.dump_off[x] + (int64_t)(s - tile.strip_begin) * R2 + io * R + ia);
               o[0] = tv;
               o[1] = d;
               o[2] = mem;
               o[3] = obj;
               o[4] = (double)(j0 + (mem > e0 ? 1 : 0));
+              o[5] = (double)((ia == 0 && zero_oo ? kFormZero : f1b[c]) + 8 * fst[c]);
               continue;
             }
             if constexpr (EX) {

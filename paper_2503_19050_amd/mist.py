@@ -425,10 +425,11 @@ class Space:
 
     def debug_eval_tiles(self, tiles, stream=None) -> np.ndarray:
         """The evaluation kernel's own per-configuration values over the listed tiles: rows of
-        (t, d, mem, obj, bucket entry) in tile order, id order within a tile."""
+        (t, d, mem, obj, bucket entry, forms of Algorithm 1 as f1 + 8 * fs) in tile order, id
+        order within a tile."""
         tl = np.ascontiguousarray(tiles, dtype=np.int32)
         total = sum(self.tile_info(int(t))["n_configs"] for t in tl)
-        out = np.empty((max(total, 1), 5), dtype=np.float64)
+        out = np.empty((max(total, 1), 6), dtype=np.float64)
         _check(self.L, self.L.mist_debug_eval_tiles(self.h, tl.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                                                     len(tl), out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
                                                     total, _stream_handle(stream)))

@@ -3,16 +3,15 @@ configuration (GPU, through the C ABI).
 
 mist_eval_ids evaluates ids one by one with the generic form of Algorithm 1; the evaluation kernel
 instead shares work across a strip (the stable time across optimizer ratios, the first round of
-each call with a row known per strip, the closed form of the all-zero configuration) and across a
-wave (when every lane sees the GPU-GPU stream finish first, the rounds after it with one row;
-otherwise rows looked up per lane).  Both kinds of wave occur in these spaces: sampled with the
-oracle's stream times, 290 of 360 first-microbatch wave iterations of the tiny space pass the
-wave-uniform test, 117 of 160 of gpt1.3b-d8's, and about 95-99 % on the benchmark spaces.
-mist_debug_eval_tiles
-runs that kernel path over listed tiles and returns t, d, mem, obj and the bucket entry it chose
-for every configuration; here they are compared bit for bit with the oracle's per-configuration
-dump (Eq. 4-6, Algorithm 1, Sec. 5.2), and the bucket with the oracle's (an infeasible
-configuration must land on a sink entry, NB..64).
+each call with a row known per strip, the closed form of the all-zero configuration) and chooses
+per wave one of four forms of the rounds (compute and the larger host stream left after the
+second round, with a per-lane third row; compute finished first, one third row; the third row
+looked up per lane; the general rounds).  mist_debug_eval_tiles runs that kernel path over
+listed tiles and returns t, d, mem, obj, the bucket entry it chose and the forms it took for
+every configuration; here the values are compared bit for bit with the oracle's
+per-configuration dump (Eq. 4-6, Algorithm 1, Sec. 5.2), the bucket with the oracle's (an
+infeasible configuration must land on a sink entry, NB..64), the closed forms with the
+configurations they belong to, and the full-size spaces must exercise every form.
 """
 
 import sys
@@ -39,9 +38,12 @@ def torch_cuda():
 
 
 def _check_tiles(S, o, wl, tiles, group_cache=None):
-    """Compares the kernel's values over the listed tiles with the oracle's dump of their groups."""
+    """Compares the kernel's values over the listed tiles with the oracle's dump of their groups;
+    returns the forms of Algorithm 1 the kernel took (f1 + 8 * fs per configuration)."""
     got = S.debug_eval_tiles(tiles)
     nb = wl["space"]["n_buckets"]
+    ratios = np.asarray(wl["space"]["ratios"], dtype=np.float64)
+    R = len(ratios)
     keys = o.group_keys()
     row = 0
     cache = {} if group_cache is None else group_cache
@@ -64,7 +66,19 @@ def _check_tiles(S, o, wl, tiles, group_cache=None):
         feasible = want[:, 4] >= 0
         assert np.array_equal(have[feasible, 4], want[feasible, 4]), "tile %d: buckets differ" % t
         assert np.all((have[~feasible, 4] >= nb) & (have[~feasible, 4] <= 64)), "tile %d: infeasible off sink" % t
+        # The closed forms belong to exactly their configurations: the first microbatch's to the one
+        # whose four offload ratios are all zero, the stable time's generic rounds to activation
+        # ratio 0 when that ratio is zero.
+        lid = np.arange(lo, lo + n, dtype=np.int64)
+        ia, io, ig, iw = lid % R, (lid // R) % R, (lid // R ** 2) % R, (lid // R ** 3) % R
+        f1, fs = have[:, 5].astype(np.int64) % 8, have[:, 5].astype(np.int64) // 8
+        zero = (ratios[ia] == 0) & (ratios[io] == 0) & (ratios[ig] == 0) & (ratios[iw] == 0)
+        assert np.array_equal(f1 == 5, zero), "tile %d: all-zero closed form" % t
+        assert np.all((f1 >= 1) & (f1 <= 5)), "tile %d: first-microbatch form" % t
+        assert np.array_equal(fs == 6, (ia == 0) & (ratios[0] == 0)), "tile %d: ratio-0 stable form" % t
+        assert np.all(((fs >= 1) & (fs <= 4)) | (fs == 6)), "tile %d: stable form" % t
     assert row == len(got)
+    return got[:, 5].astype(np.int64)
 
 
 def _unit_factors(wl):
@@ -117,8 +131,15 @@ def test_sampled_tiles_full_size(name, n, torch_cuda):
     # Full-size tiles come first in the tile table, then every group's small tail tiles.
     picks = {0, n_tiles - 1} | set(int(t) for t in rng.integers(0, n_tiles, size=n))
     tiles = sorted(picks, key=lambda t: (S.tile_info(t)["group"], t))   # one oracle group dump at a time
-    _check_tiles(S, o, wl, tiles)
+    forms = _check_tiles(S, o, wl, tiles)
     S.close()
+    f1, fs = np.bincount(forms % 8, minlength=8), np.bincount(forms // 8, minlength=8)
+    say("first-microbatch forms", f1.tolist(), "stable forms", fs.tolist())
+    # Every form of the first-microbatch call is compared somewhere on these tiles, and on
+    # gpt2.7b-d16's every form of the stable time's call as well.
+    assert np.all(f1[1:6] > 0), f1.tolist()
+    if name == "gpt2.7b-d16":
+        assert np.all(fs[[1, 2, 3, 4, 6]] > 0), fs.tolist()
 
 
 @pytest.mark.parametrize("seed", range(24))
