@@ -584,11 +584,12 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
     if (g.hw != loaded_hw) {  // the wave's LDS copy of the hardware tables
       for (int i = lane; i < 16 * kTabStride; i += 64)
         tab[(i / kTabStride) * kLdsRow + i % kTabStride] = (&hw.itab[0][0])[i];
-      if (lane < 2 * kTab2) {  // the third round's rows of compute and one host stream
+      wave_sync();
+      if (lane < 2 * kTab2) {  // the third round's rows of compute and one host stream, from the rows
         const int h = 2 + lane / kTab2, i = lane % kTab2;
-        const double* row = hw.itab[1 | (1 << h)];
-        tab[kTab2Off + lane] = i == 0 ? row[0] : i == 1 ? row[h] : i == 2 ? row[4] : i == 3 ? row[4 + h]
-                                                                                      : hw.itab[13][i == 4 ? 4 : 4 + h];
+        const int row = i < 4 ? (1 | (1 << h)) : 13;
+        const int col = ((i & 1) ? h : 0) + (i >= 2 ? 4 : 0);  // phi[0], phi[h], psi[0], psi[h], psi[0], psi[h]
+        tab[kTab2Off + lane] = tab[row * kLdsRow + col];
       }
       bucket[lane].edge = hw.edge[lane];
       loaded_hw = g.hw;
