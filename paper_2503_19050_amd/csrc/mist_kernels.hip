@@ -662,6 +662,10 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
       // traffic).
       const int pats = Z.G2Gs > 0.0 ? 15 : 13;
 
+      // Exact frontier: the larger of the strip's compute and GPU-GPU times, for the candidate
+      // pass's lower bound on the first microbatch's time.
+      [[maybe_unused]] const double mcg = __builtin_fmax(K.C, Z.G2Gf);
+
       // Activation ratios in blocks of IB: the values a block keeps across the optimizer
       // ratios fit the registers, at the price of one more optimizer-level evaluation per
       // block.  A block's stable times, and per optimizer ratio its first-microbatch times, are
@@ -710,6 +714,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
                                                         // when infeasible)
           double T1b[IB];
           [[maybe_unused]] int f1b[IB];  // dump variant: the form of each first-microbatch time
+          [[maybe_unused]] bool out[IB];  // exact frontier: cannot be a candidate (T1 not formed)
           {
             double hf[IB], df[IB];
             bool fz[IB];
@@ -720,9 +725,25 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
               hf[c] = __builtin_fma(rr[ia], A, HW) * iP + O.H2Dx;
               df[c] = __builtin_fma(rr[ia], A, DG) * iP + O.D2Hx;
               fz[c] = ia == 0 && zero_oo;
-              // The exact frontier's candidates are feasible: a configuration above the memory
-              // budget needs no first-microbatch time there (its candidate test fails on memory).
-              if constexpr (EX) fz[c] = fz[c] | !(O.Bmax + __builtin_fma(rr[ia], A2, om[ia] * KA) <= M);
+              if constexpr (EX) {
+                // The exact frontier's candidates are feasible and below every lower bucket's
+                // minimum pm of their bucket; a configuration that fails either needs no
+                // first-microbatch time (its candidate test fails).  With every slowdown factor
+                // at least 1 each stream's standalone time is progressed by at most the phase
+                // length in every round, so T1 >= max(C, G2G, H2D, D2H) and
+                // obj = G t + (T1 - t) >= (G - 1) t + max(...); the bound is lowered by a
+                // relative 2^-30, far above the rounding of either side (a few dozen
+                // operations of relative error 2^-53), so a configuration whose bound is not
+                // below pm cannot be a candidate.
+                const double mem = O.Bmax + __builtin_fma(rr[ia], A2, om[ia] * KA);
+                const int j0 = (int)__builtin_fmin(mem * kNB, 64.0);
+                const int j = min(j0 + (mem > bucket[j0].edge ? 1 : 0), 63);
+                const double lb = __builtin_fma(Gd - 1.0, tt[c], __builtin_fmax(mcg, __builtin_fmax(hf[c], df[c])));
+                out[c] = !((mem <= M) & (lb * (1.0 - 0x1p-30) < s_filt[wave][j].pm));
+                // Such a lane takes no part in the choice of form, so its T1 may be anything:
+                // the candidate test below excludes it.
+                fz[c] = fz[c] | out[c];
+              }
             }
             interference_known_n<IB, EX>(fr, hf, df, fz, T1b, f1b, nb, tab, RK);
           }
@@ -768,7 +789,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
               // both equal).  Every frontier point passes; the scan after the sort decides.
               const int j = min(j0 + (mem > e0 ? 1 : 0), 63);
               const FiltEntry f = s_filt[wave][j];
-              const bool cand = (mem <= M) & (obj < f.pm) &
+              const bool cand = !out[c] & (mem <= M) & (obj < f.pm) &
                                 !(((obj > f.bobj) & (mem >= f.bmem)) | ((obj >= f.bobj) & (mem > f.bmem)));
               const unsigned long long m = __builtin_amdgcn_ballot_w64(cand);
               int64_t slot = 0;
