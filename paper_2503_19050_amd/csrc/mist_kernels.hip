@@ -372,8 +372,8 @@ __device__ __forceinline__ double interference_known(const KnownRow& r, double h
 // Algorithm 1 for the first n of the N configurations of an activation-ratio block (host streams
 // h[c], d[c]), one wave-uniform choice of form per configuration (measured fastest against one
 // choice per block or half block: 0.81 against 1.16 and 1.02 ms on gpt2.7b-d16, equal on the
-// Llama spaces).  With SKIP a configuration free in every lane is not evaluated (its results are
-// NaN).
+// Llama spaces).  With SKIP a configuration free in every lane is not evaluated, and every free
+// lane's result is NaN.
 template <int N, bool SKIP = false>
 __device__ __forceinline__ void interference_known_n(const KnownRow& r, const double (&h)[N], const double (&d)[N],
                                                      const bool (&free)[N], double (&out)[N], int (&form)[N], int n,
@@ -386,6 +386,7 @@ __device__ __forceinline__ void interference_known_n(const KnownRow& r, const do
       out[c] = __builtin_nan("");
     else
       out[c] = interference_known(r, h[c], d[c], free[c], tab, K, form[c]);
+    if constexpr (SKIP) out[c] = free[c] ? __builtin_nan("") : out[c];
   }
 }
 
@@ -662,10 +663,6 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
       // traffic).
       const int pats = Z.G2Gs > 0.0 ? 15 : 13;
 
-      // Exact frontier: the larger of the strip's compute and GPU-GPU times, for the candidate
-      // pass's lower bound on the first microbatch's time.
-      [[maybe_unused]] const double mcg = __builtin_fmax(K.C, Z.G2Gf);
-
       // Activation ratios in blocks of IB: the values a block keeps across the optimizer
       // ratios fit the registers, at the price of one more optimizer-level evaluation per
       // block.  A block's stable times, and per optimizer ratio its first-microbatch times, are
@@ -714,7 +711,6 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
                                                         // when infeasible)
           double T1b[IB];
           [[maybe_unused]] int f1b[IB];  // dump variant: the form of each first-microbatch time
-          [[maybe_unused]] bool out[IB];  // exact frontier: cannot be a candidate (T1 not formed)
           {
             double hf[IB], df[IB];
             bool fz[IB];
@@ -730,19 +726,19 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
                 // minimum pm of their bucket; a configuration that fails either needs no
                 // first-microbatch time (its candidate test fails).  With every slowdown factor
                 // at least 1 each stream's standalone time is progressed by at most the phase
-                // length in every round, so T1 >= max(C, G2G, H2D, D2H) and
-                // obj = G t + (T1 - t) >= (G - 1) t + max(...); the bound is lowered by a
-                // relative 2^-30, far above the rounding of either side (a few dozen
-                // operations of relative error 2^-53), so a configuration whose bound is not
-                // below pm cannot be a candidate.
+                // length in every round, so T1 is at least every stream's time, in particular
+                // max(H2D, D2H), and obj = G t + (T1 - t) >= (G - 1) t + max(H2D, D2H); the
+                // bound is lowered by a relative 2^-30, far above the rounding of either side (a
+                // few dozen operations of relative error 2^-53), so a configuration whose bound
+                // is not below pm cannot be a candidate.  (Compute and GPU-GPU would tighten it
+                // little and cost registers: 92 against 72 bytes of scratch, same time.)
                 const double mem = O.Bmax + __builtin_fma(rr[ia], A2, om[ia] * KA);
                 const int j0 = (int)__builtin_fmin(mem * kNB, 64.0);
                 const int j = min(j0 + (mem > bucket[j0].edge ? 1 : 0), 63);
-                const double lb = __builtin_fma(Gd - 1.0, tt[c], __builtin_fmax(mcg, __builtin_fmax(hf[c], df[c])));
-                out[c] = !((mem <= M) & (lb * (1.0 - 0x1p-30) < s_filt[wave][j].pm));
-                // Such a lane takes no part in the choice of form, so its T1 may be anything:
-                // the candidate test below excludes it.
-                fz[c] = fz[c] | out[c];
+                const double lb = __builtin_fma(Gd - 1.0, tt[c], __builtin_fmax(hf[c], df[c]));
+                // Such a lane takes no part in the choice of form; its T1, and so its objective,
+                // is NaN, which fails the candidate test.
+                fz[c] = fz[c] | !((mem <= M) & (lb * (1.0 - 0x1p-30) < s_filt[wave][j].pm));
               }
             }
             interference_known_n<IB, EX>(fr, hf, df, fz, T1b, f1b, nb, tab, RK);
@@ -789,7 +785,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
               // both equal).  Every frontier point passes; the scan after the sort decides.
               const int j = min(j0 + (mem > e0 ? 1 : 0), 63);
               const FiltEntry f = s_filt[wave][j];
-              const bool cand = !out[c] & (mem <= M) & (obj < f.pm) &
+              const bool cand = (mem <= M) & (obj < f.pm) &
                                 !(((obj > f.bobj) & (mem >= f.bmem)) | ((obj >= f.bobj) & (mem > f.bmem)));
               const unsigned long long m = __builtin_amdgcn_ballot_w64(cand);
               int64_t slot = 0;
