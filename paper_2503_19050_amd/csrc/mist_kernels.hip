@@ -612,8 +612,8 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
     bool dropped = false;  // and whether a candidate of this lane found no place
     if constexpr (EX) {
       s_filt[wave][lane] = a.filt[(size_t)tile.group * 64 + lane];
-      n_beg = a.win_begin[t];
-      n_end = a.win_end[t];
+      n_beg = load_uniform(a.win_begin + t);  // wave-uniform: scalar registers
+      n_end = load_uniform(a.win_end + t);
       n_cand = n_beg;
     }
     if constexpr (AL) {
@@ -731,14 +731,17 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
                 // bound is lowered by a relative 2^-30, far above the rounding of either side (a
                 // few dozen operations of relative error 2^-53), so a configuration whose bound
                 // is not below pm cannot be a candidate.  (Compute and GPU-GPU would tighten it
-                // little and cost registers: 92 against 72 bytes of scratch, same time.)
+                // little and cost registers: 92 against 72 bytes of scratch, same time.)  pm does
+                // not increase with the bucket (a prefix minimum), so the estimate
+                // j0 = floor(mem * kNB) <= j of the bucket step serves: pm[j0] >= pm[j].
                 const double mem = O.Bmax + __builtin_fma(rr[ia], A2, om[ia] * KA);
-                const int j0 = (int)__builtin_fmin(mem * kNB, 64.0);
-                const int j = min(j0 + (mem > bucket[j0].edge ? 1 : 0), 63);
+                const unsigned int j0 = (unsigned int)__builtin_fmin(mem * kNB, 63.0);
+                const double pm = *reinterpret_cast<const double*>(
+                    reinterpret_cast<const char*>(s_filt[wave]) + __umul24(j0, (unsigned int)sizeof(FiltEntry)));
                 const double lb = __builtin_fma(Gd - 1.0, tt[c], __builtin_fmax(hf[c], df[c]));
                 // Such a lane takes no part in the choice of form; its T1, and so its objective,
                 // is NaN, which fails the candidate test.
-                fz[c] = fz[c] | !((mem <= M) & (lb * (1.0 - 0x1p-30) < s_filt[wave][j].pm));
+                fz[c] = fz[c] | !((mem <= M) & (lb * (1.0 - 0x1p-30) < pm));
               }
             }
             interference_known_n<IB, EX>(fr, hf, df, fz, T1b, f1b, nb, tab, RK);
@@ -752,6 +755,11 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             const double mem = O.Bmax + SO;
             double T1 = T1b[c];
             if (ia == 0) T1 = zero_oo ? T1z : T1;
+            // Exact frontier: a lane whose time was not formed (NaN) cannot hold a candidate, and
+            // when no lane of the wave has a time the configuration is done.
+            if constexpr (EX) {
+              if (!__builtin_amdgcn_ballot_w64(T1 == T1)) continue;
+            }
             const double tv = tt[c];
             const double d = T1 - tv;
             const double obj = __builtin_fma(Gd, tv, d);
@@ -788,8 +796,8 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
               const bool cand = (mem <= M) & (obj < f.pm) &
                                 !(((obj > f.bobj) & (mem >= f.bmem)) | ((obj >= f.bobj) & (mem > f.bmem)));
               const unsigned long long m = __builtin_amdgcn_ballot_w64(cand);
+              if (!m) continue;
               int64_t slot = 0;
-              const uint64_t cid = g.base + (uint64_t)(lid_oo + (unsigned int)ia);
               if (cand) {
                 const unsigned int below = __builtin_amdgcn_mbcnt_hi(
                     (unsigned int)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned int)m, 0u));
@@ -797,7 +805,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
                 if (slot < n_end) {
                   a.cand_key[slot] = (unsigned long long)__double_as_longlong(mem);
                   a.cand_obj[slot] = obj;
-                  a.cand_id[slot] = cid;
+                  a.cand_id[slot] = g.base + (uint64_t)(lid_oo + (unsigned int)ia);
                 }
               }
               // Past the window: the overflow pool, in chunks of kPoolChunk slots per wave (one
@@ -822,7 +830,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
                   if (pos < (unsigned long long)a.pool_cap) {
                     a.pool_key[pos] = (unsigned long long)__double_as_longlong(mem);
                     a.pool_obj[pos] = obj;
-                    a.pool_id[pos] = cid;
+                    a.pool_id[pos] = g.base + (uint64_t)(lid_oo + (unsigned int)ia);
                     a.pool_tile[pos] = t;
                     a.pool_rank[pos] = (int32_t)(slot - n_beg);
                   } else {
