@@ -301,8 +301,8 @@ struct RowK {
 //     and each lane reads their row (5 or 9) at a per-lane offset and forms only their terms;
 //   - GPU-GPU finishes first and compute ends the second round: both host streams are left, and
 //     the third round's row (12) is the same for the wave;
-//   - GPU-GPU finishes first otherwise (ties): the third round's row is looked up per lane from
-//     all three streams;
+//   - GPU-GPU finishes first otherwise (waves that mix the two cases above, ties): the third
+//     round's row is looked up per lane from all three streams;
 //   - else the general rounds (interference_general).
 // Each form performs the same operations on the same operands as the general rounds: a stream
 // that has finished carries NaN there (its time 0 times the row's +inf factor), which drops out
@@ -520,10 +520,9 @@ constexpr int ia_block() {
 // Waves per SIMD the register allocation aims at: four, 128 registers per lane (a few
 // strip-level values spill; the occupancy is worth more).  Five would fit the LDS of the blocks,
 // but at 96 registers the inner loop spills: 77 against 59 ms on the 64-sample Llama space.  The
-// exact frontier's
-// candidate variant keeps more per configuration live; with a whole strip's activation ratios
-// in one block (R <= 6) three waves and fewer spills are faster (1.60 against 1.83 ms for the
-// exact frontier on gpt2.7b-d16), with larger R four.
+// exact frontier's candidate variant keeps more per configuration live; with a whole strip's
+// activation ratios in one block (R <= 6) three waves and fewer spills are faster (1.60 against
+// 1.83 ms for the exact frontier on gpt2.7b-d16), with larger R four.
 template <int R, int MODE>
 constexpr int eval_waves() { return MODE == kModeEmit && R <= 6 ? 3 : 4; }
 
