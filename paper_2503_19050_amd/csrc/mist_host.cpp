@@ -42,7 +42,7 @@ hipError_t copy_async(void* dst, const void* src, size_t bytes, hipMemcpyKind ki
 constexpr int64_t kExact = (int64_t)1 << 53;  // integers below this convert to double exactly
 constexpr int64_t kStaticStrips = 512;        // strips per resident wave up to which a space is
                                               // cut into one tile per wave
-constexpr int64_t kMinTileConfigs = 8192;     // configurations per tile of a larger space, at least
+constexpr int64_t kMinTileConfigs = 16384;    // configurations per tile of a larger space, at least
 constexpr int64_t kMaxTiles = 131072;         // and tiles per space, at most
 constexpr int64_t kWindowDiv = 8;             // exact frontier: candidate window of a tile,
                                               // 1/kWindowDiv of its configurations
