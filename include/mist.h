@@ -113,7 +113,7 @@ typedef struct mist_space_desc {
                             the struct) turns the weight-sampled argmins off */
   const double* alphas;  /* host: the samples alpha_a in [0, 1] (any order, repeats allowed) */
   int64_t tile_configs;  /* launch geometry, results do not depend on it: configurations per
-                            full-size tile of the evaluation kernel, at least (0: 8192) */
+                            full-size tile of the evaluation kernel, at least (0: 16384) */
   int32_t max_blocks;    /* cap on the evaluation kernel's grid (0: every block that fits on the
                             device at once) */
   int32_t cand_window;   /* exact frontier, results do not depend on it: each tile first writes
