@@ -147,8 +147,9 @@ struct EvalArgs {
   int32_t* pool_rank;
   uint8_t* tile_drop;        // [n_tiles]
   // Dump variant (parity checks): listed item x writes, for every configuration of its tile in
-  // local-id order, t, d, mem, obj and the bucket entry the kernel chose (as a double; NB..64
-  // are the sinks of infeasible configurations) to dump[5 * (dump_off[x] + i)..].
+  // local-id order, t, d, mem, obj, the bucket entry the kernel chose (as a double; NB..64 are
+  // the sinks of infeasible configurations) and the forms of interference the kernel took
+  // (first microbatch + 8 x stable time, as a double) to dump[kDumpWords * (dump_off[x] + i)..].
   double* dump;
   const int64_t* dump_off;   // [n_list]
 };
