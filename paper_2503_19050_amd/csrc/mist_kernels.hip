@@ -517,6 +517,14 @@ constexpr int ia_block() {
   return R <= 6 ? R : (MODE == kModeAlpha && R <= 10 ? (R + 1) / 2 : (R + 2) / 3);
 }
 
+// A value every lane of the wave holds, moved to scalar registers.
+__device__ __forceinline__ double wave_uniform(double x) {
+  const unsigned long long b = (unsigned long long)__double_as_longlong(x);
+  const unsigned int lo = __builtin_amdgcn_readfirstlane((unsigned int)b);
+  const unsigned int hi = __builtin_amdgcn_readfirstlane((unsigned int)(b >> 32));
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
 // Waves per SIMD the register allocation aims at: four, 128 registers per lane (a few
 // strip-level values spill; the occupancy is worth more).  Five would fit the LDS of the blocks,
 // but at 96 registers the inner loop spills: 77 against 59 ms on the 64-sample Llama space.  The
@@ -538,6 +546,10 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
   constexpr int R2 = R * R;
   constexpr int SU = 4 * R2;  // strips per (pair, c) unit
   constexpr int IB = ia_block<R, MODE>();
+  // Exact frontier with the activation ratios in several blocks: lower bounds per strip and per
+  // block (below).  With the whole strip in one block the candidates are dense and the bounds
+  // rarely hold for a whole wave (1 % of the wave iterations on gpt2.7b-d16, simulated).
+  constexpr bool BLK = EX && IB < R;
   __shared__ double s_tab[kWaves][16 * kLdsRow + 2 * kTab2];
   __shared__ BucketEntry s_bucket[kWaves][65];  // entries NB..64: sinks of infeasible configurations
   __shared__ OoIn s_oo[kBlock];         // per-lane strip constants of the optimizer level
@@ -554,6 +566,18 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
   const double* __restrict__ rr = ratio;  // read-only and uniform: scalar loads
   const double* __restrict__ om = ratio + R;
   const bool r0_zero = rr[0] == 0.0;
+  // The smallest offload ratio and the smallest 1 - r, for the strip bounds.
+  [[maybe_unused]] double r_lo = 0.0, q_lo = 0.0;
+  if constexpr (BLK) {
+    r_lo = rr[0];
+    q_lo = om[0];
+    for (int i = 1; i < R; ++i) {
+      r_lo = __builtin_fmin(r_lo, rr[i]);
+      q_lo = __builtin_fmin(q_lo, om[i]);
+    }
+    r_lo = wave_uniform(r_lo);
+    q_lo = wave_uniform(q_lo);
+  }
   double* tab = s_tab[wave];
   BucketEntry* bucket = s_bucket[wave];
   const unsigned long long kEmpty = (unsigned long long)__double_as_longlong(__builtin_huge_val());
@@ -646,6 +670,39 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
       const ZeroK Z = zero_level(P, z);
       const double rw = rr[iw], rg = rr[ig];
       const WoGoK W = wogo_levels(P, Z, rw, om[iw], rg, om[ig]);
+      // Exact frontier: lower bounds of the optimizer level's peak and first-microbatch extras over
+      // the strip's optimizer ratios, then a first candidate bound for the whole strip.  Every
+      // input of the level is non-negative, so each of its operations is non-decreasing in the
+      // ratio r or in 1 - r; the bounds repeat the level's own operations on the smallest r and
+      // the smallest 1 - r (the resident states shrink with r, the offloaded states' buffer and
+      // the extras grow with it), and rounding to nearest is monotone: each is at most the value
+      // of every optimizer ratio, the peak's as max(forward, backward) of two lower bounds.
+      [[maybe_unused]] double Bmin = 0.0, Hxmin = 0.0, Dxmin = 0.0;
+      if constexpr (BLK) {
+        const double base = __builtin_fma(q_lo, Z.So, W.Swg) + W.Wbuf;
+        const double BF = (base + __builtin_fma(r_lo, Z.Obo, W.Og)) + P.Xd;
+        const double BB = ((base + W.Gbuf) + K.Rc) + P.Xd;
+        Bmin = __builtin_fmax(BF, BB);
+        Hxmin = __builtin_fma(r_lo, Z.So, W.DG) * iP;
+        Dxmin = __builtin_fma(r_lo, Z.So, W.DW) * iP;
+        {
+          // The strip bound, before the stable times: with every slowdown factor at least 1 a
+          // stable time is at least each of its streams' times (compute, GPU-GPU and the host
+          // streams, whose smallest values come with the smallest activation ratio), and the
+          // stash and offload buffers are at least fma(r_lo, 2A, q_lo * KA).  The bound is the
+          // block bound below with those values in place of the block's own, so it is at most
+          // every configuration's; a strip that fails in every lane of the wave is skipped whole
+          // (the relative 2^-30 covers the rounding of the stable time as well).
+          const double hsl = __builtin_fma(r_lo, K.A, W.HW) * iP, dsl = __builtin_fma(r_lo, K.A, W.DG) * iP;
+          const double mem = Bmin + __builtin_fma(r_lo, P.A2, q_lo * K.KA);
+          const unsigned int j0 = (unsigned int)__builtin_fmin(mem * kNB, 63.0);
+          const double pm = *reinterpret_cast<const double*>(
+              reinterpret_cast<const char*>(s_filt[wave]) + __umul24(j0, (unsigned int)sizeof(FiltEntry)));
+          const double tl = __builtin_fmax(__builtin_fmax(K.C, Z.G2Gs), __builtin_fmax(hsl, dsl));
+          const double lb = __builtin_fma(Gd - 1.0, tl, __builtin_fmax(hsl + Hxmin, dsl + Dxmin));
+          if (!__builtin_amdgcn_ballot_w64((mem <= M) & (lb * (1.0 - 0x1p-30) < pm))) continue;
+        }
+      }
 
       // First microbatch: every configuration of the strip with a non-zero offload ratio
       // starts with compute, both host streams and (if it carries traffic) GPU-GPU.
@@ -656,6 +713,8 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
       const double T1z = interference_zero(K.C, Z.G2Gf, tab);
       s_oo[tid] = oo_inputs(P, K, Z, W);
       const double A = K.A, KA = K.KA, A2 = P.A2, HW = W.HW, DG = W.DG;
+      // Block bound: the strip's smallest optimizer-level peak and first-microbatch extras over
+      // the optimizer ratios, each the minimum of the values the configurations use.
       const unsigned int lid_strip = (unsigned int)s * (unsigned int)R2;
       // With a positive activation ratio both host streams run, so the stable microbatch's
       // first round has the pattern compute + both host streams (+ GPU-GPU when it carries
@@ -674,6 +733,7 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
         const KnownRow sr = known_row(tab, pats, K.C, Z.G2Gs);
         double tt[IB];
         [[maybe_unused]] int fst[IB];  // dump variant: the form of each stable time
+        [[maybe_unused]] double hsmin = 0.0, dsmin = 0.0;  // block bound: the smallest host streams
         {
           double hs[IB], ds[IB];
           bool fs[IB];
@@ -686,6 +746,16 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
             fs[c] = ia == 0 && r0_zero;
           }
           interference_known_n<IB>(sr, hs, ds, fs, tt, fst, nb, tab, RK);
+          if constexpr (BLK) {
+            hsmin = hs[0];
+            dsmin = ds[0];
+#pragma unroll
+            for (int c = 1; c < IB; ++c) {
+              if (ib + c >= R) break;
+              hsmin = __builtin_fmin(hsmin, hs[c]);
+              dsmin = __builtin_fmin(dsmin, ds[c]);
+            }
+          }
           // Activation ratio 0 leaves the host streams to the weights and gradients alone: the
           // first round's pattern is not known in advance.
           if (ib == 0 && r0_zero) {
@@ -699,6 +769,32 @@ __global__ __launch_bounds__(kBlock, (eval_waves<R, MODE>())) void k_eval(EvalAr
 #pragma unroll
           for (int c = 1; c < IB; ++c)
             if (ib + c < R) t_min = __builtin_fmin(t_min, tt[c]);
+        }
+
+        if constexpr (BLK) {
+          // Exact frontier: the candidate bound of the configurations below, taken once for the
+          // block.  Each of its terms is at most, over the block's optimizer and activation
+          // ratios, the value a configuration's bound uses (its memory from the peak's bound and
+          // the smallest stash, its host streams from the smallest stable parts and the extras'
+          // bounds, the smallest stable time); rounding is monotone, so the block's memory,
+          // bucket estimate and bound are at most each configuration's, and its threshold pm at
+          // least each one's (pm does not increase with the bucket).  A block that fails in every lane of the wave holds no
+          // configuration that passes its own bound, and none that can be a candidate: the
+          // strip's all-zero configuration, whose time is formed without the bound, has host
+          // streams 0 and so an objective of at least (G - 1) t as well.
+          double tmin = tt[0], somin = __builtin_fma(rr[ib], A2, om[ib] * KA);
+#pragma unroll
+          for (int c = 1; c < IB; ++c) {
+            if (ib + c >= R) break;
+            tmin = __builtin_fmin(tmin, tt[c]);
+            somin = __builtin_fmin(somin, __builtin_fma(rr[ib + c], A2, om[ib + c] * KA));
+          }
+          const double mem = Bmin + somin;
+          const unsigned int j0 = (unsigned int)__builtin_fmin(mem * kNB, 63.0);
+          const double pm = *reinterpret_cast<const double*>(
+              reinterpret_cast<const char*>(s_filt[wave]) + __umul24(j0, (unsigned int)sizeof(FiltEntry)));
+          const double lb = __builtin_fma(Gd - 1.0, tmin, __builtin_fmax(hsmin + Hxmin, dsmin + Dxmin));
+          if (!__builtin_amdgcn_ballot_w64((mem <= M) & (lb * (1.0 - 0x1p-30) < pm))) continue;
         }
 
 #pragma unroll 1

@@ -76,6 +76,48 @@ def test_exact_frontier(name, torch_cuda):
     S.close()
 
 
+def _many_ratios(seed: int, R: int) -> dict:
+    """A random space with R offload ratios: a subset of the eighths of [0, 1] (odd seeds, R <= 9)
+    or R uniform values in [0, 1] (the first replaced by 0 for seeds divisible by 4)."""
+    wl = W.random_space(seed)
+    rng = np.random.default_rng(seed)
+    if R <= 9 and seed % 2:
+        rs = np.sort(rng.choice(9, size=R, replace=False)) / 8.0
+    else:
+        rs = np.sort(rng.uniform(0.0, 1.0, R))
+        if seed % 4 == 0:
+            rs[0] = 0.0
+    wl["space"]["ratios"] = [float(x) for x in rs]
+    return wl
+
+
+@pytest.mark.parametrize("R, seed", [(7, 501), (8, 502), (9, 503), (9, 504), (11, 503), (13, 517), (16, 521)])
+def test_exact_frontier_many_ratios(R, seed, torch_cuda):
+    """Spaces with seven or more offload ratios, whose activation ratios the candidate pass takes
+    in several blocks, with a lower bound per strip and per block: every group against the
+    oracle."""
+    from paper_2503_19050_amd import mist
+    wl = _many_ratios(seed, R)
+    assert len(set(wl["space"]["ratios"])) == R
+    S = mist.from_workload(wl)
+    S.eval()
+    S.eval_pareto_exact()
+    torch_cuda.cuda.synchronize()
+    o = O.Oracle(wl)
+    assert 0 < o.n_configs == S.n_configs
+    best = S.best(0, S.n_groups)
+    total = 0
+    for g in range(o.n_groups):
+        got, want = S.pareto_exact(g), o.pareto_exact(g)
+        assert [r["id"] for r in got] == [int(i) for i in want["id"]], g
+        assert [r["obj"] for r in got] == list(want["obj"]) and [r["mem"] for r in got] == list(want["mem"]), g
+        if got:
+            assert got[-1]["obj"] == best[g]["obj"]
+        total += len(got)
+    say("R", R, "seed", seed, "configurations", o.n_configs, "groups", o.n_groups, "frontier points", total)
+    S.close()
+
+
 def test_exact_and_plan_states(torch_cuda):
     """The exact frontier needs an evaluation first and is read only after its own pass; a
     space without weight samples still plans from each group's best."""
